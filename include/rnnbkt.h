@@ -1,0 +1,214 @@
+/*
+ * rnnbkt.h -- C ABI of librnnbkt.so: the single-GPU hot path of
+ * sequence-bucketed recurrent-network training on AMD Instinct MI355X (gfx950).
+ *
+ * Method: Khomenko et al., "Accelerating Recurrent Neural Network Training
+ * using Sequence Bucketing and Multi-GPU Data Parallelization" (arXiv
+ * 1708.05604).  The planner implements the dynamic-programming bucketing of
+ * Sec. III.A (eqs. 1-2 and the DYNAMICBUCKETING procedure); the batch
+ * schedule follows Sec. III (reshuffle every epoch) and Sec. IV.A (shortest
+ * bucket first); the model calls run one mini-batch of a stacked LSTM (the
+ * paper's model, its ref. [1]) or GRU (its ref. [2], Sec. I) forward and
+ * backward through time, with a per-frame softmax cross-entropy loss in place
+ * of the paper's CTC cost, and a plain SGD step in place of ADADELTA.
+ *
+ * Conventions for every call
+ *   - Return value: RNNBKT_OK (0) or a negative error code.  On error,
+ *     rnnbkt_last_error() returns a message (thread-local, valid until the
+ *     next call on the same thread).  No C++ exception crosses the ABI.
+ *   - Argument validation happens before any GPU work is enqueued: a call
+ *     that returns RNNBKT_EINVAL or RNNBKT_EUNSUPPORTED has launched nothing.
+ *   - "device" pointers are HIP device memory owned by the caller; "host"
+ *     pointers are read (or written) synchronously during the call.  The
+ *     library never allocates or frees device memory.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     GPU work is enqueued on it asynchronously; the library never
+ *     synchronises the device.  An asynchronous kernel fault surfaces as
+ *     RNNBKT_EHIP from a later call or from rnnbkt_sync_check().
+ */
+#ifndef RNNBKT_H
+#define RNNBKT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RNNBKT_OK 0
+#define RNNBKT_EINVAL (-1)       /* bad argument (null pointer, bad size, unsorted lengths...) */
+#define RNNBKT_EUNSUPPORTED (-2) /* valid but not supported shape/option (e.g. hidden % 32 != 0) */
+#define RNNBKT_EHIP (-3)         /* a HIP runtime call or kernel launch failed */
+
+#define RNNBKT_CELL_LSTM 0 /* gates i, f, g, o */
+#define RNNBKT_CELL_GRU 1  /* gates r, z, n */
+
+#define RNNBKT_GEMM_FP32 0 /* GEMM operands and accumulation in fp32 */
+#define RNNBKT_GEMM_BF16 1 /* GEMM operands rounded to bf16 (nearest-even), fp32 accumulate */
+
+/* Library version string, e.g. "rnnbkt 0.1.0 gfx950". */
+const char* rnnbkt_version(void);
+
+/* Message of the last error on this thread ("" if none). */
+const char* rnnbkt_last_error(void);
+
+/* Waits for `stream` and reports any asynchronous HIP error as RNNBKT_EHIP. */
+int32_t rnnbkt_sync_check(void* stream);
+
+/*
+ * rnnbkt_bucket_plan -- optimal length bucketing (Sec. III.A, the
+ * DYNAMICBUCKETING dynamic program over the length histogram).
+ *
+ * Splits the sequences, ordered by length, into K_eff = min(K, D) buckets of
+ * contiguous length ranges (D = number of distinct lengths) so that
+ * sum_b upper_b * count_b -- every sequence padded to its bucket's upper
+ * length -- is minimal.  Among equal-cost splits the one the paper's loop
+ * order selects is returned: at every level the largest split point
+ * (the DP scans split points downwards and replaces only on a strictly
+ * smaller score).
+ *
+ *   lengths       host int32[n], every value >= 1 (any order)
+ *   n             number of sequences, >= 1
+ *   K             requested number of buckets, >= 1
+ *   bucket_upper  host int32[K] out: first *K_eff entries = upper length of
+ *                 each bucket, strictly increasing, last = max(lengths)
+ *   bucket_of     host int32[n] out: bucket of each sequence (0-based), the
+ *                 smallest b with lengths[s] <= bucket_upper[b]
+ *   K_eff         host out: number of buckets actually used
+ *   padded_steps  host out: the optimum, sum_b upper_b * count_b
+ * Host-only (no GPU needed).  Errors: EINVAL for null pointers, n < 1,
+ * K < 1 or a length < 1.
+ */
+int32_t rnnbkt_bucket_plan(const int32_t* lengths, int64_t n, int32_t K,
+                           int32_t* bucket_upper, int32_t* bucket_of,
+                           int32_t* K_eff, int64_t* padded_steps);
+
+/*
+ * rnnbkt_epoch_schedule -- the mini-batches of one epoch (Sec. III: data
+ * reshuffled every epoch; Sec. IV.A: the shortest bucket is fed first, then
+ * the bucket index increases; K_eff = 1 is the paper's unbucketed baseline,
+ * a purely random split into mini-batches).
+ *
+ * For b = 0..K_eff-1: the sequences of bucket b are ordered by
+ * (keys[s], s) ascending -- the keys are the epoch's random shuffle -- and
+ * cut into consecutive batches of B (the last one may be smaller); each
+ * batch is then ordered by (length descending, index ascending), so the
+ * sequences still running at step t are a prefix of the batch.
+ *
+ *   lengths      host int32[n] (>= 1)
+ *   bucket_of    host int32[n] from rnnbkt_bucket_plan (values in [0, K_eff))
+ *   keys         host uint64[n] shuffle keys of this epoch
+ *   B            batch size >= 1
+ *   order        host int64[n] out: sequence indices, batch after batch
+ *   batch_start  host int64[n+1] out: batch i is order[batch_start[i] ..
+ *                batch_start[i+1]); only the first *num_batches+1 are set
+ *   num_batches  host out
+ * Host-only.  Errors: EINVAL.
+ */
+int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* bucket_of,
+                              int64_t n, int32_t K_eff, const uint64_t* keys,
+                              int32_t B, int64_t* order, int64_t* batch_start,
+                              int64_t* num_batches);
+
+/* Model description.  Shapes: G = 4 (LSTM) or 3 (GRU) gates, H = hidden,
+ * dirs = 2 if bidirectional else 1, D_in(layer 0) = input_dim,
+ * D_in(layer > 0) = dirs * H, H_top = dirs * H. */
+typedef struct {
+  int32_t cell;          /* RNNBKT_CELL_LSTM or RNNBKT_CELL_GRU */
+  int32_t num_layers;    /* >= 1 */
+  int32_t input_dim;     /* >= 1 */
+  int32_t hidden;        /* multiple of 32 */
+  int32_t num_classes;   /* 1..1024 */
+  int32_t bidirectional; /* 0 or 1 */
+  int32_t gemm_dtype;    /* RNNBKT_GEMM_FP32 or RNNBKT_GEMM_BF16 */
+} rnnbkt_model_desc;
+
+/*
+ * Flat fp32 parameter layout (row-major), the order of rnnbkt_param_count:
+ *   for layer = 0..num_layers-1, for direction = forward, reverse:
+ *     W_ih [G*H, D_in]  gate blocks in the order above
+ *     W_hh [G*H, H]
+ *     LSTM: b [G*H]          GRU: b_ih [3H], then b_hh [3H]
+ *   W_out [C, H_top], b_out [C]
+ * LSTM:  a = W_ih x + W_hh h + b; i,f,o = sigmoid, g = tanh;
+ *        c' = f*c + i*g; h' = o*tanh(c').
+ * GRU:   r,z = sigmoid(W_i x + b_i + W_h h + b_h) of their blocks;
+ *        n = tanh(W_in x + b_in + r*(W_hn h + b_hn)); h' = (1-z)*n + z*h.
+ * Initial states are zero; the reverse direction runs over each sequence's
+ * own length; a bidirectional layer outputs [h_fwd ; h_bwd] per frame.
+ * Returns the number of floats, or a negative error code.
+ */
+int64_t rnnbkt_param_count(const rnnbkt_model_desc* desc);
+
+/*
+ * Bytes of the two caller-owned device buffers a batch needs:
+ *   reserve   -- written by rnnbkt_lstm_fwd, read by rnnbkt_lstm_bwd of the
+ *                same batch (activations kept for backpropagation); must not
+ *                be modified in between
+ *   workspace -- scratch of either call (no content carried between calls)
+ * Depends on (desc, T_max, B, n_valid) only and is non-decreasing in each,
+ * so sizing with an epoch's maxima covers every batch of the epoch.
+ *   T_max    longest sequence of the batch;  B  batch size;
+ *   n_valid  sum of the batch's lengths.
+ */
+int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_t B,
+                            int64_t n_valid, size_t* reserve_bytes,
+                            size_t* workspace_bytes);
+
+/*
+ * rnnbkt_lstm_fwd -- forward pass and loss of one mini-batch (LSTM or GRU
+ * per desc->cell).
+ *
+ *   params     device fp32[param_count], layout above
+ *   x          device fp32[T_max][B][input_dim], time-major padded batch;
+ *              frames t >= lengths[b] are never read (may hold anything)
+ *   labels     device int32[T_max][B], class of every valid frame in
+ *              [0, num_classes); pad entries are never read
+ *   lengths    host int32[B], non-increasing, lengths[0] == T_max, all >= 1
+ *   reserve / workspace  device buffers of at least the sizes returned by
+ *              rnnbkt_buffer_sizes(desc, T_max, B, sum(lengths))
+ *   loss       device fp32[1] out: mean over the batch's valid frames of
+ *              -log softmax(W_out h_top + b_out)[label]
+ * The loss gradient w.r.t. the logits is computed here and kept in reserve.
+ * Errors: EINVAL (null pointer, bad lengths, buffers too small),
+ * EUNSUPPORTED (hidden % 32 != 0, num_classes > 1024), EHIP.
+ */
+int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* params,
+                        const float* x, const int32_t* labels,
+                        const int32_t* lengths, int32_t T_max, int32_t B,
+                        void* reserve, size_t reserve_bytes, void* workspace,
+                        size_t workspace_bytes, float* loss, void* stream);
+
+/*
+ * rnnbkt_lstm_bwd -- backpropagation through time of the batch last run
+ * through rnnbkt_lstm_fwd with the same (desc, params, x, lengths, reserve).
+ *   grads   device fp32[param_count] out: d loss / d params (overwritten
+ *           entirely, same layout as params)
+ * Other arguments as in rnnbkt_lstm_fwd (labels are not needed again).
+ * Reductions run in a fixed order: results are bitwise reproducible.
+ */
+int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
+                        const int32_t* lengths, int32_t T_max, int32_t B,
+                        const void* reserve, size_t reserve_bytes, void* workspace,
+                        size_t workspace_bytes, float* grads, void* stream);
+
+/* rnnbkt_sgd_apply -- params[i] -= lr * grads[i] for i < n (device fp32). */
+int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,
+                         void* stream);
+
+/*
+ * rnnbkt_top_hidden -- copies the top layer's per-frame output of the batch
+ * held in `reserve` (after rnnbkt_lstm_fwd) into the padded layout
+ * out[T_max][B][H_top] (device fp32); pad frames are set to 0.
+ * Arguments as in rnnbkt_lstm_fwd.
+ */
+int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
+                          int32_t T_max, int32_t B, const void* reserve,
+                          size_t reserve_bytes, float* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RNNBKT_H */

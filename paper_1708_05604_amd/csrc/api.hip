@@ -1,0 +1,512 @@
+// C-ABI entry points of the model calls: argument validation, buffer
+// carving, and the enqueue order of the kernels for one mini-batch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace rnnbkt {
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Shape {
+  int G, H, D, C, L, dirs, Htop;
+  bool bf16;
+  int cell;
+  int din(int l) const { return l == 0 ? D : dirs * H; }
+};
+
+int32_t check_desc(const rnnbkt_model_desc* d, Shape* s) {
+  RNNBKT_REQUIRE(d != nullptr, RNNBKT_EINVAL, "model desc is null");
+  RNNBKT_REQUIRE(d->cell == RNNBKT_CELL_LSTM || d->cell == RNNBKT_CELL_GRU, RNNBKT_EINVAL,
+                 "desc.cell must be 0 (LSTM) or 1 (GRU), got %d", d->cell);
+  RNNBKT_REQUIRE(d->num_layers >= 1 && d->input_dim >= 1 && d->hidden >= 1 &&
+                     d->num_classes >= 1,
+                 RNNBKT_EINVAL, "desc sizes must be >= 1");
+  RNNBKT_REQUIRE(d->bidirectional == 0 || d->bidirectional == 1, RNNBKT_EINVAL,
+                 "desc.bidirectional must be 0 or 1");
+  RNNBKT_REQUIRE(d->gemm_dtype == RNNBKT_GEMM_FP32 || d->gemm_dtype == RNNBKT_GEMM_BF16,
+                 RNNBKT_EINVAL, "desc.gemm_dtype must be 0 (fp32) or 1 (bf16)");
+  RNNBKT_REQUIRE(d->hidden % 32 == 0, RNNBKT_EUNSUPPORTED,
+                 "hidden must be a multiple of 32 (got %d)", d->hidden);
+  RNNBKT_REQUIRE(d->input_dim % 4 == 0, RNNBKT_EUNSUPPORTED,
+                 "input_dim must be a multiple of 4 (got %d)", d->input_dim);
+  RNNBKT_REQUIRE(d->num_classes % 4 == 0 && d->num_classes <= 1024, RNNBKT_EUNSUPPORTED,
+                 "num_classes must be a multiple of 4 and <= 1024 (got %d)", d->num_classes);
+  s->cell = d->cell;
+  s->G = d->cell == RNNBKT_CELL_LSTM ? 4 : 3;
+  s->H = d->hidden;
+  s->D = d->input_dim;
+  s->C = d->num_classes;
+  s->L = d->num_layers;
+  s->dirs = d->bidirectional ? 2 : 1;
+  s->Htop = s->dirs * s->H;
+  s->bf16 = d->gemm_dtype == RNNBKT_GEMM_BF16;
+  return RNNBKT_OK;
+}
+
+// Offsets (in floats) of each block of the flat parameter vector.
+struct ParamOffsets {
+  std::vector<int64_t> wih, whh, b, bhh;  // indexed by layer*dirs + dir
+  int64_t wout = 0, bout = 0, total = 0;
+};
+
+ParamOffsets param_offsets(const Shape& s) {
+  ParamOffsets p;
+  int64_t pos = 0;
+  const int64_t GH = (int64_t)s.G * s.H;
+  for (int l = 0; l < s.L; ++l)
+    for (int d = 0; d < s.dirs; ++d) {
+      p.wih.push_back(pos);
+      pos += GH * s.din(l);
+      p.whh.push_back(pos);
+      pos += GH * s.H;
+      p.b.push_back(pos);
+      pos += GH;
+      if (s.cell == RNNBKT_CELL_GRU) {
+        p.bhh.push_back(pos);
+        pos += GH;
+      } else {
+        p.bhh.push_back(-1);
+      }
+    }
+  p.wout = pos;
+  pos += (int64_t)s.C * s.Htop;
+  p.bout = pos;
+  pos += s.C;
+  p.total = pos;
+  return p;
+}
+
+// Split-K choice for the weight-gradient reductions over the frames.
+struct SplitK {
+  int S;
+  int kps;
+};
+
+SplitK choose_splitk(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  int64_t S = std::max<int64_t>(1, (512 + tiles - 1) / tiles);
+  S = std::min<int64_t>(S, std::max<int64_t>(1, K / 256));
+  int64_t kps = (K + S - 1) / S;
+  kps = (kps + 31) / 32 * 32;
+  S = std::max<int64_t>(1, (K + kps - 1) / kps);
+  return SplitK{(int)S, (int)kps};
+}
+
+constexpr int64_t kColsumRows = 512;
+
+// Byte offsets of every buffer a batch uses.
+struct Carve {
+  // reserve
+  size_t bs, off, xp, yp, prev_f, prev_r, dz;
+  std::vector<size_t> hout;        // per layer [N x dirs*H]
+  std::vector<size_t> stash, cst;  // per layer*dirs
+  size_t reserve;
+  // workspace (forward)
+  size_t gx, loss_part;
+  size_t ws_fwd;
+  // workspace (backward)
+  size_t dha, dhb, da, dah, carry, splitk, colsum;
+  size_t ws_bwd;
+  size_t workspace;
+};
+
+Carve carve(const Shape& s, int T, int B, int64_t N) {
+  Carve c{};
+  const int64_t GH = (int64_t)s.G * s.H;
+  size_t pos = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = pos;
+    pos = align_up(pos + bytes);
+    return at;
+  };
+  c.bs = take(sizeof(int32_t) * T);
+  c.off = take(sizeof(int32_t) * (T + 1));
+  c.xp = take(sizeof(float) * N * s.D);
+  c.yp = take(sizeof(int32_t) * N);
+  c.prev_f = take(sizeof(int32_t) * N);
+  c.prev_r = take(sizeof(int32_t) * N);
+  c.dz = take(sizeof(float) * N * s.C);
+  for (int l = 0; l < s.L; ++l) c.hout.push_back(take(sizeof(float) * N * s.dirs * s.H));
+  for (int l = 0; l < s.L; ++l)
+    for (int d = 0; d < s.dirs; ++d) {
+      c.stash.push_back(take(sizeof(float) * N * 4 * s.H));
+      c.cst.push_back(s.cell == RNNBKT_CELL_LSTM ? take(sizeof(float) * N * s.H) : 0);
+    }
+  c.reserve = pos;
+
+  pos = 0;
+  c.gx = take(sizeof(float) * N * GH);
+  c.loss_part = take(sizeof(float) * ((N + 15) / 16 + 1));
+  c.ws_fwd = pos;
+
+  pos = 0;
+  c.dha = take(sizeof(float) * N * s.Htop);
+  c.dhb = take(sizeof(float) * N * s.Htop);
+  c.da = take(sizeof(float) * N * GH);
+  c.dah = s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0;
+  c.carry = take(sizeof(float) * (size_t)B * s.H);
+  size_t sk = 0;
+  auto need = [&](int64_t M, int64_t Nn, int64_t K) {
+    const SplitK p = choose_splitk(M, Nn, K);
+    if (p.S > 1) sk = std::max(sk, (size_t)p.S * M * Nn);
+  };
+  need(s.C, s.Htop, N);
+  for (int l = 0; l < s.L; ++l) {
+    need(GH, s.din(l), N);
+    need(GH, s.H, N);
+  }
+  c.splitk = take(sizeof(float) * std::max<size_t>(sk, 1));
+  const int64_t cs_splits = (N + kColsumRows - 1) / kColsumRows;
+  c.colsum = take(sizeof(float) * cs_splits * std::max<int64_t>(GH, s.C));
+  c.ws_bwd = pos;
+  c.workspace = std::max(c.ws_fwd, c.ws_bwd);
+  return c;
+}
+
+int32_t check_lengths(const int32_t* lengths, int T, int B, int64_t* n_valid) {
+  RNNBKT_REQUIRE(lengths != nullptr, RNNBKT_EINVAL, "lengths is null");
+  RNNBKT_REQUIRE(B >= 1, RNNBKT_EINVAL, "batch size must be >= 1 (got %d)", B);
+  RNNBKT_REQUIRE(T >= 1, RNNBKT_EINVAL, "T_max must be >= 1 (got %d)", T);
+  RNNBKT_REQUIRE(lengths[0] == T, RNNBKT_EINVAL, "lengths[0] (%d) must equal T_max (%d)",
+                 lengths[0], T);
+  int64_t n = 0;
+  for (int b = 0; b < B; ++b) {
+    RNNBKT_REQUIRE(lengths[b] >= 1, RNNBKT_EINVAL, "lengths[%d] = %d < 1", b, lengths[b]);
+    RNNBKT_REQUIRE(b == 0 || lengths[b] <= lengths[b - 1], RNNBKT_EINVAL,
+                   "lengths must be non-increasing (lengths[%d] = %d > lengths[%d] = %d)", b,
+                   lengths[b], b - 1, lengths[b - 1]);
+    n += lengths[b];
+  }
+  RNNBKT_REQUIRE(n <= (int64_t)INT32_MAX / 4, RNNBKT_EUNSUPPORTED,
+                 "too many valid frames in one batch (%lld)", (long long)n);
+  *n_valid = n;
+  return RNNBKT_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+#define RNNBKT_HIP(expr)                                                              \
+  do {                                                                                \
+    hipError_t _e = (expr);                                                           \
+    if (_e != hipSuccess) {                                                           \
+      ::rnnbkt::set_error("%s failed: %s", #expr, hipGetErrorString(_e));             \
+      return RNNBKT_EHIP;                                                             \
+    }                                                                                 \
+  } while (0)
+
+// Host copy of the batch tables (active rows per step and frame offsets).
+void host_tables(const int32_t* len, int T, int B, std::vector<int>& bs, std::vector<int>& off) {
+  bs.assign(T, 0);
+  off.assign(T + 1, 0);
+  for (int b = 0; b < B; ++b)
+    for (int t = 0; t < len[b]; ++t) bs[t]++;
+  for (int t = 0; t < T; ++t) off[t + 1] = off[t] + bs[t];
+}
+
+template <typename P>
+P* at(void* base, size_t off) {
+  return reinterpret_cast<P*>(static_cast<char*>(base) + off);
+}
+template <typename P>
+const P* at(const void* base, size_t off) {
+  return reinterpret_cast<const P*>(static_cast<const char*>(base) + off);
+}
+
+hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t ldb, bool b_kc,
+                float* C, int64_t ldc, int M, int N, int K, const float* bias, int accumulate,
+                bool bf16, hipStream_t st, const int32_t* gather = nullptr,
+                float* splitk_buf = nullptr) {
+  GemmArgs g{};
+  g.A = A;
+  g.B = Bm;
+  g.C = C;
+  g.bias = bias;
+  g.gather_b = gather;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.accumulate = accumulate;
+  g.splits = 1;
+  g.k_per_split = (K + 31) / 32 * 32;
+  if (splitk_buf) {
+    const SplitK p = choose_splitk(M, N, K);
+    g.splits = p.S;
+    g.k_per_split = p.kps;
+    g.partial = splitk_buf;
+  }
+  if (M == 0 || N == 0) return hipSuccess;
+  hipError_t e = launch_gemm(g, a_kc, b_kc, bf16, st);
+  if (e != hipSuccess || g.splits == 1) return e;
+  return launch_splitk_reduce(splitk_buf, g.splits, M, N, C, ldc, bias, accumulate, st);
+}
+
+}  // namespace
+
+}  // namespace rnnbkt
+
+using namespace rnnbkt;
+
+extern "C" const char* rnnbkt_version(void) { return "rnnbkt 0.1.0 gfx950"; }
+
+extern "C" int32_t rnnbkt_sync_check(void* stream) {
+  clear_error();
+  RNNBKT_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+  RNNBKT_HIP(hipGetLastError());
+  return RNNBKT_OK;
+}
+
+extern "C" int64_t rnnbkt_param_count(const rnnbkt_model_desc* desc) {
+  clear_error();
+  Shape s;
+  const int32_t rc = check_desc(desc, &s);
+  if (rc != RNNBKT_OK) return rc;
+  return param_offsets(s).total;
+}
+
+extern "C" int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_t B,
+                                       int64_t n_valid, size_t* reserve_bytes,
+                                       size_t* workspace_bytes) {
+  clear_error();
+  Shape s;
+  int32_t rc = check_desc(desc, &s);
+  if (rc != RNNBKT_OK) return rc;
+  RNNBKT_REQUIRE(reserve_bytes && workspace_bytes, RNNBKT_EINVAL, "null output pointer");
+  RNNBKT_REQUIRE(T_max >= 1 && B >= 1 && n_valid >= 1 && n_valid <= (int64_t)T_max * B,
+                 RNNBKT_EINVAL, "need T_max >= 1, B >= 1, 1 <= n_valid <= T_max*B");
+  const Carve c = carve(s, T_max, B, n_valid);
+  *reserve_bytes = c.reserve;
+  *workspace_bytes = c.workspace;
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* params,
+                                   const float* x, const int32_t* labels,
+                                   const int32_t* lengths, int32_t T, int32_t B, void* reserve,
+                                   size_t reserve_bytes, void* workspace,
+                                   size_t workspace_bytes, float* loss, void* stream) {
+  clear_error();
+  Shape s;
+  int32_t rc = check_desc(desc, &s);
+  if (rc != RNNBKT_OK) return rc;
+  int64_t N = 0;
+  rc = check_lengths(lengths, T, B, &N);
+  if (rc != RNNBKT_OK) return rc;
+  RNNBKT_REQUIRE(params && x && labels && reserve && workspace && loss, RNNBKT_EINVAL,
+                 "lstm_fwd: null pointer");
+  RNNBKT_REQUIRE(aligned16(params) && aligned16(x) && aligned16(reserve) && aligned16(workspace),
+                 RNNBKT_EINVAL, "lstm_fwd: params, x, reserve and workspace must be 16-byte aligned");
+  const Carve c = carve(s, T, B, N);
+  RNNBKT_REQUIRE(reserve_bytes >= c.reserve && workspace_bytes >= c.workspace, RNNBKT_EINVAL,
+                 "lstm_fwd: buffers too small (reserve %zu < %zu or workspace %zu < %zu)",
+                 reserve_bytes, c.reserve, workspace_bytes, c.workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  RNNBKT_HIP(hipGetLastError());
+  const ParamOffsets po = param_offsets(s);
+  std::vector<int> bs, off;
+  host_tables(lengths, T, B, bs, off);
+
+  int32_t* d_bs = at<int32_t>(reserve, c.bs);
+  int32_t* d_off = at<int32_t>(reserve, c.off);
+  float* Xp = at<float>(reserve, c.xp);
+  int32_t* Yp = at<int32_t>(reserve, c.yp);
+  int32_t* pf = at<int32_t>(reserve, c.prev_f);
+  int32_t* pr = at<int32_t>(reserve, c.prev_r);
+  float* dz = at<float>(reserve, c.dz);
+  float* gx = at<float>(workspace, c.gx);
+  float* lp = at<float>(workspace, c.loss_part);
+
+  RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
+  RNNBKT_HIP(launch_pack(x, labels, d_bs, d_off, T, B, s.D, Xp, Yp, pf, pr, st));
+
+  const int GH = s.G * s.H;
+  for (int l = 0; l < s.L; ++l) {
+    const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
+    const int din = s.din(l);
+    float* hout = at<float>(reserve, c.hout[l]);
+    for (int d = 0; d < s.dirs; ++d) {
+      const int ld = l * s.dirs + d;
+      // Input projection of every valid frame at once (bias folded in).
+      RNNBKT_HIP(gemm(xin, din, true, params + po.wih[ld], din, true, gx, GH, (int)N, GH, din,
+                      params + po.b[ld], 0, s.bf16, st));
+      StepFwdArgs a{};
+      a.gx = gx;
+      a.whh = params + po.whh[ld];
+      a.bhh = s.cell == RNNBKT_CELL_GRU ? params + po.bhh[ld] : nullptr;
+      a.hout = hout + d * s.H;
+      a.stash = at<float>(reserve, c.stash[ld]);
+      a.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+      a.H = s.H;
+      a.ldh = s.dirs * s.H;
+      for (int k = 0; k < T; ++k) {
+        const int t = d == 0 ? k : T - 1 - k;
+        a.row0 = off[t];
+        a.rows = bs[t];
+        if (d == 0) {
+          a.prev0 = t > 0 ? off[t - 1] : 0;
+          a.prev_rows = t > 0 ? bs[t] : 0;
+        } else {
+          a.prev0 = t + 1 < T ? off[t + 1] : 0;
+          a.prev_rows = t + 1 < T ? bs[t + 1] : 0;
+        }
+        RNNBKT_HIP(launch_step_fwd(a, s.cell, s.bf16, st));
+      }
+    }
+  }
+  // Output layer and loss.
+  const float* top = at<float>(reserve, c.hout[s.L - 1]);
+  RNNBKT_HIP(gemm(top, s.Htop, true, params + po.wout, s.Htop, true, dz, s.C, (int)N, s.C,
+                  s.Htop, params + po.bout, 0, s.bf16, st));
+  int32_t nparts = 0;
+  RNNBKT_HIP(launch_softmax_xent(dz, Yp, N, s.C, lp, &nparts, st));
+  RNNBKT_HIP(launch_sum(lp, nparts, 1.0f / (float)N, loss, st));
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
+                                   const int32_t* lengths, int32_t T, int32_t B,
+                                   const void* reserve, size_t reserve_bytes, void* workspace,
+                                   size_t workspace_bytes, float* grads, void* stream) {
+  clear_error();
+  Shape s;
+  int32_t rc = check_desc(desc, &s);
+  if (rc != RNNBKT_OK) return rc;
+  int64_t N = 0;
+  rc = check_lengths(lengths, T, B, &N);
+  if (rc != RNNBKT_OK) return rc;
+  RNNBKT_REQUIRE(params && reserve && workspace && grads, RNNBKT_EINVAL,
+                 "lstm_bwd: null pointer");
+  RNNBKT_REQUIRE(aligned16(params) && aligned16(reserve) && aligned16(workspace) &&
+                     aligned16(grads),
+                 RNNBKT_EINVAL, "lstm_bwd: params, reserve, workspace and grads must be 16-byte aligned");
+  const Carve c = carve(s, T, B, N);
+  RNNBKT_REQUIRE(reserve_bytes >= c.reserve && workspace_bytes >= c.workspace, RNNBKT_EINVAL,
+                 "lstm_bwd: buffers too small (reserve %zu < %zu or workspace %zu < %zu)",
+                 reserve_bytes, c.reserve, workspace_bytes, c.workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  RNNBKT_HIP(hipGetLastError());
+  const ParamOffsets po = param_offsets(s);
+  std::vector<int> bs, off;
+  host_tables(lengths, T, B, bs, off);
+
+  const float* Xp = at<float>(reserve, c.xp);
+  const int32_t* pf = at<int32_t>(reserve, c.prev_f);
+  const int32_t* pr = at<int32_t>(reserve, c.prev_r);
+  const float* dz = at<float>(reserve, c.dz);
+  float* dha = at<float>(workspace, c.dha);
+  float* dhb = at<float>(workspace, c.dhb);
+  float* da = at<float>(workspace, c.da);
+  float* dah = s.cell == RNNBKT_CELL_GRU ? at<float>(workspace, c.dah) : nullptr;
+  float* carry = at<float>(workspace, c.carry);
+  float* sk = at<float>(workspace, c.splitk);
+  float* cs = at<float>(workspace, c.colsum);
+  const int GH = s.G * s.H;
+  const int n = (int)N;
+
+  // Output layer: dH_top = dZ W_out, dW_out = dZ^T H_top, db_out = colsum dZ.
+  const float* top = at<float>(reserve, c.hout[s.L - 1]);
+  RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dha, s.Htop, n, s.Htop, s.C,
+                  nullptr, 0, s.bf16, st));
+  RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
+                  nullptr, 0, s.bf16, st, nullptr, sk));
+  RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, kColsumRows, cs, grads + po.bout, st));
+
+  float* dh_in = dha;
+  float* dx = dhb;
+  for (int l = s.L - 1; l >= 0; --l) {
+    const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
+    const int din = s.din(l);
+    const float* hout = at<float>(reserve, c.hout[l]);
+    for (int d = 0; d < s.dirs; ++d) {
+      const int ld = l * s.dirs + d;
+      StepBwdArgs a{};
+      a.da_next = s.cell == RNNBKT_CELL_GRU ? dah : da;
+      a.whh = params + po.whh[ld];
+      a.dh_in = dh_in + d * s.H;
+      a.stash = at<float>(reserve, c.stash[ld]);
+      a.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+      a.hout = hout + d * s.H;
+      a.da = da;
+      a.dah = dah;
+      a.carry = carry;
+      a.H = s.H;
+      a.ldd = s.Htop;
+      a.ldh = s.dirs * s.H;
+      for (int k = 0; k < T; ++k) {
+        const int t = d == 0 ? T - 1 - k : k;
+        a.row0 = off[t];
+        a.rows = bs[t];
+        if (d == 0) {
+          a.next0 = t + 1 < T ? off[t + 1] : 0;
+          a.next_rows = t + 1 < T ? bs[t + 1] : 0;
+          a.prev0 = t > 0 ? off[t - 1] : 0;
+          a.prev_rows = t > 0 ? bs[t] : 0;
+        } else {
+          a.next0 = t > 0 ? off[t - 1] : 0;
+          a.next_rows = t > 0 ? bs[t] : 0;
+          a.prev0 = t + 1 < T ? off[t + 1] : 0;
+          a.prev_rows = t + 1 < T ? bs[t + 1] : 0;
+        }
+        RNNBKT_HIP(launch_step_bwd(a, s.cell, s.bf16, st));
+      }
+      // Weight gradients reduced over every valid frame.
+      const float* dax = da;
+      const float* dahh = s.cell == RNNBKT_CELL_GRU ? dah : da;
+      RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
+                      nullptr, 0, s.bf16, st, nullptr, sk));
+      RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
+                      s.H, GH, s.H, n, nullptr, 0, s.bf16, st, d == 0 ? pf : pr, sk));
+      RNNBKT_HIP(launch_colsum(dax, N, GH, GH, kColsumRows, cs, grads + po.b[ld], st));
+      if (s.cell == RNNBKT_CELL_GRU)
+        RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, kColsumRows, cs, grads + po.bhh[ld], st));
+      if (l > 0)
+        RNNBKT_HIP(gemm(dax, GH, true, params + po.wih[ld], din, false, dx, din, n, din, GH,
+                        nullptr, d > 0 ? 1 : 0, s.bf16, st));
+    }
+    std::swap(dh_in, dx);
+  }
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,
+                                    void* stream) {
+  clear_error();
+  RNNBKT_REQUIRE(params && grads, RNNBKT_EINVAL, "sgd_apply: null pointer");
+  RNNBKT_REQUIRE(n >= 0, RNNBKT_EINVAL, "sgd_apply: n < 0");
+  RNNBKT_REQUIRE(aligned16(params) && aligned16(grads), RNNBKT_EINVAL,
+                 "sgd_apply: params and grads must be 16-byte aligned");
+  if (n == 0) return RNNBKT_OK;
+  RNNBKT_HIP(launch_sgd(params, grads, n, lr, static_cast<hipStream_t>(stream)));
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
+                                     int32_t T, int32_t B, const void* reserve,
+                                     size_t reserve_bytes, float* out, void* stream) {
+  clear_error();
+  Shape s;
+  int32_t rc = check_desc(desc, &s);
+  if (rc != RNNBKT_OK) return rc;
+  int64_t N = 0;
+  rc = check_lengths(lengths, T, B, &N);
+  if (rc != RNNBKT_OK) return rc;
+  RNNBKT_REQUIRE(reserve && out, RNNBKT_EINVAL, "top_hidden: null pointer");
+  const Carve c = carve(s, T, B, N);
+  RNNBKT_REQUIRE(reserve_bytes >= c.reserve, RNNBKT_EINVAL, "top_hidden: reserve too small");
+  RNNBKT_HIP(launch_unpack(at<float>(reserve, c.hout[s.L - 1]), s.Htop,
+                           at<int32_t>(reserve, c.bs), at<int32_t>(reserve, c.off), T, B, out,
+                           static_cast<hipStream_t>(stream)));
+  return RNNBKT_OK;
+}

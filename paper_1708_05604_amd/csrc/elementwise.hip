@@ -1,0 +1,238 @@
+// Memory-bound kernels of the training step: batch tables and packing of the
+// padded batch into valid frames, the per-frame softmax cross-entropy with
+// its gradient, deterministic reductions, and the SGD update.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace rnnbkt {
+
+namespace {
+
+constexpr int kLenChunk = 256;
+struct LenChunk {
+  int32_t len[kLenChunk];
+};
+
+// batch_sizes[t] (+)= #{b in chunk : len[b] > t}
+__global__ void k_batch_sizes(LenChunk c, int count, int T, int32_t* bs, int first) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  int v = 0;
+  for (int b = 0; b < count; ++b) v += c.len[b] > t ? 1 : 0;
+  bs[t] = first ? v : bs[t] + v;
+}
+
+// offsets = exclusive prefix sum of batch_sizes; one 1024-thread block.
+__global__ __launch_bounds__(1024) void k_offsets(const int32_t* __restrict__ bs, int T,
+                                                  int32_t* __restrict__ off) {
+  __shared__ int32_t part[1024];
+  const int tid = threadIdx.x;
+  const int per = (T + 1023) / 1024;
+  const int t0 = tid * per;
+  const int t1 = min(T, t0 + per);
+  int32_t s = 0;
+  for (int t = t0; t < t1; ++t) s += bs[t];
+  part[tid] = s;
+  __syncthreads();
+  // Hillis-Steele inclusive scan of the 1024 partial sums.
+  for (int d = 1; d < 1024; d <<= 1) {
+    const int32_t add = tid >= d ? part[tid - d] : 0;
+    __syncthreads();
+    part[tid] += add;
+    __syncthreads();
+  }
+  int32_t run = part[tid] - s;  // exclusive
+  for (int t = t0; t < t1; ++t) {
+    off[t] = run;
+    run += bs[t];
+  }
+  if (tid == 1023) off[T] = part[1023];
+}
+
+__global__ void k_pack(const float* __restrict__ x, const int32_t* __restrict__ labels,
+                       const int32_t* __restrict__ bs, const int32_t* __restrict__ off, int T,
+                       int B, int D, float* __restrict__ Xp, int32_t* __restrict__ Yp,
+                       int32_t* __restrict__ prev_fwd, int32_t* __restrict__ prev_rev) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)T * B) return;
+  const int t = (int)(idx / B), b = (int)(idx % B);
+  if (b >= bs[t]) return;
+  const int64_t f = off[t] + b;
+  const float* src = x + idx * D;
+  float* dst = Xp + f * D;
+  for (int k = 0; k < D; ++k) dst[k] = src[k];
+  if (Yp) Yp[f] = labels[idx];
+  prev_fwd[f] = t > 0 ? off[t - 1] + b : -1;
+  prev_rev[f] = (t + 1 < T && b < bs[t + 1]) ? off[t + 1] + b : -1;
+}
+
+__global__ void k_unpack(const float* __restrict__ H, int W, const int32_t* __restrict__ bs,
+                         const int32_t* __restrict__ off, int T, int B,
+                         float* __restrict__ out) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)T * B * W) return;
+  const int64_t tb = idx / W;
+  const int w = (int)(idx % W);
+  const int t = (int)(tb / B), b = (int)(tb % B);
+  out[idx] = b < bs[t] ? H[(int64_t)(off[t] + b) * W + w] : 0.f;
+}
+
+__device__ inline float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ inline float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+constexpr int kXentRowsPerWave = 4;
+constexpr int kXentWaves = 4;
+constexpr int kXentMaxPerLane = 16;  // C <= 1024
+
+// One wave per frame: max, log-sum-exp, loss term and gradient row.
+__global__ __launch_bounds__(256) void k_softmax_xent(float* __restrict__ z,
+                                                      const int32_t* __restrict__ y, int64_t N,
+                                                      int C, float inv_n,
+                                                      float* __restrict__ partial) {
+  __shared__ float wsum[kXentWaves];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t base = ((int64_t)blockIdx.x * kXentWaves + wave) * kXentRowsPerWave;
+  float acc = 0.f;
+  for (int rr = 0; rr < kXentRowsPerWave; ++rr) {
+    const int64_t f = base + rr;
+    if (f >= N) break;
+    float* row = z + f * C;
+    float v[kXentMaxPerLane];
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kXentMaxPerLane; ++i) {
+      const int c = lane + 64 * i;
+      v[i] = c < C ? row[c] : -INFINITY;
+      m = fmaxf(m, v[i]);
+    }
+    m = wave_max(m);
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kXentMaxPerLane; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C) s += expf(v[i] - m);
+    }
+    s = wave_sum(s);
+    const float lse = m + logf(s);
+    const int label = y[f];
+    float zy = 0.f;
+#pragma unroll
+    for (int i = 0; i < kXentMaxPerLane; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C) {
+        if (c == label) zy = v[i];
+        const float p = expf(v[i] - lse);
+        row[c] = (p - (c == label ? 1.f : 0.f)) * inv_n;
+      }
+    }
+    zy = wave_sum(zy);
+    acc += (label >= 0 && label < C) ? lse - zy : NAN;
+  }
+  if (lane == 0) wsum[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+    for (int w = 0; w < kXentWaves; ++w) t += wsum[w];
+    partial[blockIdx.x] = t;
+  }
+}
+
+__global__ __launch_bounds__(1024) void k_sum(const float* __restrict__ p, int n, float scale,
+                                              float* __restrict__ out) {
+  __shared__ float red[1024];
+  float s = 0.f;
+  for (int i = threadIdx.x; i < n; i += 1024) s += p[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int d = 512; d > 0; d >>= 1) {
+    if ((int)threadIdx.x < d) red[threadIdx.x] += red[threadIdx.x + d];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0] * scale;
+}
+
+__global__ void k_sgd(float* __restrict__ p, const float* __restrict__ g, int64_t n, float lr) {
+  const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i4 + 3 < n) {
+    float4 pv = *reinterpret_cast<float4*>(p + i4);
+    const float4 gv = *reinterpret_cast<const float4*>(g + i4);
+    pv.x -= lr * gv.x;
+    pv.y -= lr * gv.y;
+    pv.z -= lr * gv.z;
+    pv.w -= lr * gv.w;
+    *reinterpret_cast<float4*>(p + i4) = pv;
+  } else {
+    for (int64_t i = i4; i < n; ++i) p[i] -= lr * g[i];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_batch_tables(const int32_t* lengths, int32_t B, int32_t T, int32_t* bs,
+                               int32_t* off, hipStream_t st) {
+  const int threads = 256;
+  for (int c0 = 0; c0 < B; c0 += kLenChunk) {
+    LenChunk c{};
+    const int cnt = std::min(kLenChunk, B - c0);
+    for (int i = 0; i < cnt; ++i) c.len[i] = lengths[c0 + i];
+    hipLaunchKernelGGL(k_batch_sizes, dim3((T + threads - 1) / threads), dim3(threads), 0, st,
+                       c, cnt, T, bs, c0 == 0 ? 1 : 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_offsets, dim3(1), dim3(1024), 0, st, bs, T, off);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const float* x, const int32_t* labels, const int32_t* bs,
+                       const int32_t* off, int32_t T, int32_t B, int32_t D, float* Xp,
+                       int32_t* Yp, int32_t* pf, int32_t* pr, hipStream_t st) {
+  const int64_t total = (int64_t)T * B;
+  const int threads = 256;
+  hipLaunchKernelGGL(k_pack, dim3((unsigned)((total + threads - 1) / threads)), dim3(threads),
+                     0, st, x, labels, bs, off, T, B, D, Xp, Yp, pf, pr);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack(const float* H, int32_t W, const int32_t* bs, const int32_t* off,
+                         int32_t T, int32_t B, float* out, hipStream_t st) {
+  const int64_t total = (int64_t)T * B * W;
+  const int threads = 256;
+  hipLaunchKernelGGL(k_unpack, dim3((unsigned)((total + threads - 1) / threads)), dim3(threads),
+                     0, st, H, W, bs, off, T, B, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_softmax_xent(float* z, const int32_t* y, int64_t N, int32_t C,
+                               float* partial, int32_t* num_partials, hipStream_t st) {
+  const int64_t rows_per_block = kXentRowsPerWave * kXentWaves;
+  const int blocks = (int)((N + rows_per_block - 1) / rows_per_block);
+  *num_partials = blocks;
+  hipLaunchKernelGGL(k_softmax_xent, dim3(blocks), dim3(256), 0, st, z, y, N, C,
+                     1.0f / (float)N, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum(const float* partial, int32_t n, float scale, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_sum, dim3(1), dim3(1024), 0, st, partial, n, scale, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd(float* p, const float* g, int64_t n, float lr, hipStream_t st) {
+  const int threads = 256;
+  const int64_t quads = (n + 3) / 4;
+  hipLaunchKernelGGL(k_sgd, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads), 0,
+                     st, p, g, n, lr);
+  return hipGetLastError();
+}
+
+}  // namespace rnnbkt

@@ -1,0 +1,121 @@
+// Internal launch interface between the C-ABI layer (api.hip) and the HIP
+// kernels.  Every launcher enqueues on `stream` and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "rnnbkt.h"
+
+namespace rnnbkt {
+
+// ---------------------------------------------------------------- GEMM
+// C[M x N] = op(A) . op(B) (+ bias[n]) (+ C if accumulate), fp32 in memory;
+// operands rounded to bf16 on the way to the matrix cores when bf16 != 0.
+//   a_kcontig: A element (m, k) at A[m*lda + k], else at A[k*lda + m]
+//   b_kcontig: B element (k, n) at B[n*ldb + k], else at B[row(k)*ldb + n]
+//              where row(k) = gather_b ? gather_b[k] : k (a negative
+//              gather entry reads as a zero row)
+// With splits > 1 the K range is cut into `splits` slices of k_per_split
+// (a multiple of 32); each slice writes partial[s][M][N] and
+// splitk_reduce() folds them in slice order (deterministic).
+struct GemmArgs {
+  const float* A;
+  const float* B;
+  float* C;
+  const float* bias;
+  const int32_t* gather_b;
+  float* partial;
+  int64_t lda, ldb, ldc;
+  int32_t M, N, K;
+  int32_t k_per_split;
+  int32_t splits;
+  int32_t accumulate;
+};
+
+hipError_t launch_gemm(const GemmArgs& g, bool a_kcontig, bool b_kcontig, bool bf16,
+                       hipStream_t stream);
+
+// out[m*ldc + n] = (accumulate ? out : 0) + sum_s partial[s][m][n] (+ bias[n])
+hipError_t launch_splitk_reduce(const float* partial, int32_t S, int32_t M, int32_t N,
+                                float* out, int64_t ldc, const float* bias, int32_t accumulate,
+                                hipStream_t stream);
+
+// Column sums of A[rows x cols] (row stride lda), deterministic:
+// partial[s][c] over row slices of `rows_per_split`, then folded into out[c].
+hipError_t launch_colsum(const float* A, int64_t rows, int32_t cols, int64_t lda,
+                         int64_t rows_per_split, float* partial, float* out,
+                         hipStream_t stream);
+
+// ---------------------------------------------------------------- batch tables
+// batch_sizes[t] = #{b : lengths[b] > t} for t < T_max (lengths copied into
+// kernel arguments in chunks), offsets[t] = sum_{t' < t} batch_sizes[t'],
+// offsets[T_max] = n_valid.
+hipError_t launch_batch_tables(const int32_t* lengths_host, int32_t B, int32_t T_max,
+                               int32_t* batch_sizes, int32_t* offsets, hipStream_t stream);
+
+// Padded time-major batch -> packed valid frames (frame of (t, b) = offsets[t] + b):
+// Xp[f][:] = x[t][b][:], Yp[f] = labels[t][b] (labels may be null),
+// prev_fwd[f] = frame of (t-1, b) or -1, prev_rev[f] = frame of (t+1, b) or -1.
+hipError_t launch_pack(const float* x, const int32_t* labels, const int32_t* batch_sizes,
+                       const int32_t* offsets, int32_t T_max, int32_t B, int32_t D, float* Xp,
+                       int32_t* Yp, int32_t* prev_fwd, int32_t* prev_rev, hipStream_t stream);
+
+// out[t][b][:] = H[offsets[t] + b][:] for b < batch_sizes[t], else 0.
+hipError_t launch_unpack(const float* H, int32_t width, const int32_t* batch_sizes,
+                         const int32_t* offsets, int32_t T_max, int32_t B, float* out,
+                         hipStream_t stream);
+
+// ---------------------------------------------------------------- loss, SGD
+// In place over logits[N x C]: dlogits = (softmax - onehot(y)) / N;
+// loss_partial[block] = sum over the block's frames of -log softmax[y].
+// Returns the number of partials through *num_partials.
+hipError_t launch_softmax_xent(float* logits, const int32_t* labels, int64_t N, int32_t C,
+                               float* loss_partial, int32_t* num_partials, hipStream_t stream);
+
+// out[0] = scale * sum_i partial[i] (fixed order).
+hipError_t launch_sum(const float* partial, int32_t n, float scale, float* out,
+                      hipStream_t stream);
+
+hipError_t launch_sgd(float* params, const float* grads, int64_t n, float lr,
+                      hipStream_t stream);
+
+// ---------------------------------------------------------------- recurrent steps
+// One time step of one layer/direction over the active rows [0, rows) of the
+// batch.  State of row b at the previous step (in recurrence order) lives in
+// frame prev0 + b when b < prev_rows, else the state is zero.
+struct StepFwdArgs {
+  const float* gx;   // [N x G*H] input projection incl. input bias
+  const float* whh;  // [G*H x H]
+  const float* bhh;  // GRU: [3H] recurrent bias; LSTM: unused
+  float* hout;       // layer output, already offset to this direction's columns
+  float* stash;      // [N x 4H] gate activations (LSTM i,f,g,o; GRU r,z,n,W_hn h + b_hn)
+  float* cst;        // LSTM: [N x H] cell state; GRU: unused
+  int32_t H, ldh;
+  int32_t row0, rows;
+  int32_t prev0, prev_rows;
+};
+
+// One step of backpropagation through time.  "next" is the following step
+// of the forward recurrence (processed just before this one here).
+struct StepBwdArgs {
+  const float* da_next;  // LSTM: dA, GRU: dAh rows of the next step
+  const float* whh;      // [G*H x H]
+  const float* dh_in;    // gradient from above, offset to this direction's columns
+  const float* stash;
+  const float* cst;      // LSTM cell state
+  const float* hout;     // GRU: layer output (previous state), offset to direction
+  float* da;             // [N x G*H] LSTM dA / GRU dAx
+  float* dah;            // GRU: [N x 3H] dAh
+  float* carry;          // [B x H] LSTM dc*f, GRU dh*z of the next step
+  int32_t H, ldd, ldh;
+  int32_t row0, rows;
+  int32_t next0, next_rows;
+  int32_t prev0, prev_rows;
+};
+
+hipError_t launch_step_fwd(const StepFwdArgs& a, int cell, bool bf16, hipStream_t stream);
+hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_t stream);
+
+}  // namespace rnnbkt

@@ -1,0 +1,225 @@
+"""ctypes binding of librnnbkt.so (declared in include/rnnbkt.h).
+
+Argument marshalling only: every computation runs in the library (host C++
+for the planner and schedule, HIP kernels for the model).  Device buffers
+are passed as torch tensors on the GPU, or as raw integer addresses; torch
+is used for nothing but device memory and the current stream.
+
+Loading fails loudly (``LibraryMissing``) when the library has not been
+built; there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librnnbkt.so")
+
+OK = 0
+EINVAL = -1
+EUNSUPPORTED = -2
+EHIP = -3
+
+CELL_LSTM = 0
+CELL_GRU = 1
+GEMM_FP32 = 0
+GEMM_BF16 = 1
+
+
+class LibraryMissing(RuntimeError):
+    pass
+
+
+class RnnbktError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"rnnbkt error {code}: {msg}")
+        self.code = code
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [("cell", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("input_dim", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("num_classes", ctypes.c_int32), ("bidirectional", ctypes.c_int32),
+                ("gemm_dtype", ctypes.c_int32)]
+
+    @classmethod
+    def of(cls, cell, num_layers, input_dim, hidden, num_classes, bidirectional, gemm_dtype):
+        return cls(int(cell), int(num_layers), int(input_dim), int(hidden), int(num_classes),
+                   int(bidirectional), int(gemm_dtype))
+
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_u64p = ctypes.POINTER(ctypes.c_uint64)
+_szp = ctypes.POINTER(ctypes.c_size_t)
+_vp = ctypes.c_void_p
+_descp = ctypes.POINTER(ModelDesc)
+
+_SIGNATURES = {
+    "rnnbkt_version": (ctypes.c_char_p, []),
+    "rnnbkt_last_error": (ctypes.c_char_p, []),
+    "rnnbkt_sync_check": (ctypes.c_int32, [_vp]),
+    "rnnbkt_bucket_plan": (ctypes.c_int32, [_i32p, ctypes.c_int64, ctypes.c_int32, _i32p, _i32p,
+                                            _i32p, _i64p]),
+    "rnnbkt_epoch_schedule": (ctypes.c_int32, [_i32p, _i32p, ctypes.c_int64, ctypes.c_int32,
+                                               _u64p, ctypes.c_int32, _i64p, _i64p, _i64p]),
+    "rnnbkt_param_count": (ctypes.c_int64, [_descp]),
+    "rnnbkt_buffer_sizes": (ctypes.c_int32, [_descp, ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.c_int64, _szp, _szp]),
+    "rnnbkt_lstm_fwd": (ctypes.c_int32, [_descp, _vp, _vp, _vp, _i32p, ctypes.c_int32,
+                                         ctypes.c_int32, _vp, ctypes.c_size_t, _vp,
+                                         ctypes.c_size_t, _vp, _vp]),
+    "rnnbkt_lstm_bwd": (ctypes.c_int32, [_descp, _vp, _i32p, ctypes.c_int32, ctypes.c_int32,
+                                         _vp, ctypes.c_size_t, _vp, ctypes.c_size_t, _vp, _vp]),
+    "rnnbkt_sgd_apply": (ctypes.c_int32, [_vp, _vp, ctypes.c_int64, ctypes.c_float, _vp]),
+    "rnnbkt_top_hidden": (ctypes.c_int32, [_descp, _i32p, ctypes.c_int32, ctypes.c_int32, _vp,
+                                           ctypes.c_size_t, _vp, _vp]),
+}
+
+_lib = None
+
+
+def load():
+    """Loads the in-tree library once; raises LibraryMissing if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise LibraryMissing(
+            f"{LIB_PATH} not found: build it with `python -m paper_1708_05604_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def exported_symbols():
+    return list(_SIGNATURES)
+
+
+def _check(code: int):
+    if code != OK:
+        raise RnnbktError(code, load().rnnbkt_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _ptr(a: np.ndarray, typ):
+    return a.ctypes.data_as(typ)
+
+
+def _dev(t) -> int:
+    """Device address of a tensor (or an int address)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def version() -> str:
+    return load().rnnbkt_version().decode()
+
+
+def last_error() -> str:
+    return load().rnnbkt_last_error().decode()
+
+
+def sync_check(stream=None):
+    _check(load().rnnbkt_sync_check(_stream(stream)))
+
+
+def bucket_plan(lengths, K: int):
+    """-> (bucket_upper int32[K_eff], bucket_of int32[n], K_eff, padded_steps)."""
+    lib = load()
+    L = _i32(lengths)
+    n = L.size
+    upper = np.zeros(max(int(K), 1), np.int32)
+    bof = np.zeros(n, np.int32)
+    keff = ctypes.c_int32(0)
+    padded = ctypes.c_int64(0)
+    _check(lib.rnnbkt_bucket_plan(_ptr(L, _i32p), n, int(K), _ptr(upper, _i32p),
+                                  _ptr(bof, _i32p), ctypes.byref(keff), ctypes.byref(padded)))
+    return upper[:keff.value].copy(), bof, keff.value, padded.value
+
+
+def epoch_schedule(lengths, bucket_of, K_eff: int, keys, B: int):
+    """-> list of int64 arrays (sequence indices of each batch, in order)."""
+    lib = load()
+    L = _i32(lengths)
+    bo = _i32(bucket_of)
+    k = np.ascontiguousarray(keys, dtype=np.uint64)
+    n = L.size
+    order = np.zeros(n, np.int64)
+    starts = np.zeros(n + 1, np.int64)
+    nb = ctypes.c_int64(0)
+    _check(lib.rnnbkt_epoch_schedule(_ptr(L, _i32p), _ptr(bo, _i32p), n, int(K_eff),
+                                     _ptr(k, _u64p), int(B), _ptr(order, _i64p),
+                                     _ptr(starts, _i64p), ctypes.byref(nb)))
+    return [order[starts[i]:starts[i + 1]].copy() for i in range(nb.value)]
+
+
+def param_count(desc: ModelDesc) -> int:
+    r = load().rnnbkt_param_count(ctypes.byref(desc))
+    if r < 0:
+        _check(int(r))
+    return int(r)
+
+
+def buffer_sizes(desc: ModelDesc, T_max: int, B: int, n_valid: int):
+    """-> (reserve_bytes, workspace_bytes)."""
+    r = ctypes.c_size_t(0)
+    w = ctypes.c_size_t(0)
+    _check(load().rnnbkt_buffer_sizes(ctypes.byref(desc), int(T_max), int(B), int(n_valid),
+                                      ctypes.byref(r), ctypes.byref(w)))
+    return r.value, w.value
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def lstm_fwd(desc, params, x, labels, lengths, reserve, workspace, loss, stream=None):
+    L = _i32(lengths)
+    _check(load().rnnbkt_lstm_fwd(ctypes.byref(desc), _dev(params), _dev(x), _dev(labels),
+                                  _ptr(L, _i32p), int(L[0]), int(L.size), _dev(reserve),
+                                  _nbytes(reserve), _dev(workspace), _nbytes(workspace),
+                                  _dev(loss), _stream(stream)))
+
+
+def lstm_bwd(desc, params, lengths, reserve, workspace, grads, stream=None):
+    L = _i32(lengths)
+    _check(load().rnnbkt_lstm_bwd(ctypes.byref(desc), _dev(params), _ptr(L, _i32p), int(L[0]),
+                                  int(L.size), _dev(reserve), _nbytes(reserve), _dev(workspace),
+                                  _nbytes(workspace), _dev(grads), _stream(stream)))
+
+
+def sgd_apply(params, grads, lr: float, stream=None, n: Optional[int] = None):
+    count = params.numel() if n is None else int(n)
+    _check(load().rnnbkt_sgd_apply(_dev(params), _dev(grads), count, float(lr),
+                                   _stream(stream)))
+
+
+def top_hidden(desc, lengths, reserve, out, stream=None):
+    L = _i32(lengths)
+    _check(load().rnnbkt_top_hidden(ctypes.byref(desc), _ptr(L, _i32p), int(L[0]), int(L.size),
+                                    _dev(reserve), _nbytes(reserve), _dev(out),
+                                    _stream(stream)))

@@ -1,0 +1,167 @@
+"""GPU parity: the library's HIP path against the float64 oracle on the same
+seeded inputs (normwise relative error per tensor and per parameter block:
+1e-4 for fp32 GEMMs, 2e-2 for bf16 GEMM operands)."""
+import numpy as np
+import pytest
+
+from oracle import bucketing as ob
+from oracle import rnn as orn
+from oracle import schedule as osch
+from paper_1708_05604_amd import lib, synth
+from tests import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lib.load()
+
+
+def test_tiny_epoch_k2():
+    """The whole tiny workload: planner, schedule, every batch fwd+bwd."""
+    w = synth.WORKLOADS["tiny"]
+    spec = H.Spec.of(w)
+    P = orn.param_count(spec.model())
+    data = synth.make_workload(w, 0, param_count=P)
+    _, bof, keff, _ = lib.bucket_plan(data.lengths, 2)
+    batches = lib.epoch_schedule(data.lengths, bof, keff, synth.shuffle_keys(0, 0, w.n), w.batch)
+    for i, order in enumerate(batches):
+        H.assert_batch_close(spec, data.params, data, order, label=f"tiny b{i}")
+
+
+SHAPES = [
+    # (label, spec, lengths)
+    ("lstm-h64-b37-ragged", H.Spec(0, 1, 0, 4, 64, 12), [31, 30, 30, 29] + list(range(28, 0, -1))
+     + [1, 1, 1, 1, 1]),
+    ("lstm-2l-bi", H.Spec(0, 2, 1, 8, 32, 8), [9, 7, 7, 3, 1]),
+    ("gru-2l-h96", H.Spec(1, 2, 0, 8, 96, 20), [17, 16, 12, 12, 12, 9, 5, 5, 4, 3, 2, 2, 1, 1, 1,
+                                                1, 1, 1, 1, 1, 1]),
+    ("gru-bi", H.Spec(1, 1, 1, 4, 32, 4), [6, 5, 2]),
+    ("lstm-bf16-2l-bi", H.Spec(0, 2, 1, 8, 64, 16, synth.BF16), [20, 18, 11, 4, 4, 1]),
+    ("gru-bf16", H.Spec(1, 1, 0, 8, 64, 16, synth.BF16), [20, 13, 2]),
+    ("b1-t1", H.Spec(0, 1, 0, 4, 32, 4), [1]),
+    ("equal-lengths", H.Spec(0, 1, 0, 4, 32, 8), [12] * 18),
+    ("one-long", H.Spec(0, 2, 1, 4, 32, 8), [40, 1, 1, 1]),
+    ("wide-classes", H.Spec(0, 1, 0, 16, 32, 1024), [5, 4]),
+]
+
+
+@pytest.mark.parametrize("label,spec,lengths", SHAPES, ids=[s[0] for s in SHAPES])
+def test_shapes(label, spec, lengths):
+    data = H.data_from_lengths(spec, lengths, seed=len(label), scale=0.3)
+    order = H.batch_order(data, range(len(lengths)))
+    H.assert_batch_close(spec, data.params, data, order, label=label)
+
+
+def test_sgd_trajectory_tiny():
+    """Three SGD steps on one batch: parameters follow the oracle's."""
+    spec = H.Spec(0, 1, 0, 4, 32, 20)
+    data = H.data_from_lengths(spec, [30, 22, 22, 9, 3], seed=5, scale=0.3)
+    order = H.batch_order(data, range(5))
+    lr = 0.5
+    gb = H.GpuBatch(spec, data.params, data, order)
+    theta = data.params.astype(np.float64)
+    for step in range(3):
+        gb.run()
+        gb.sgd(lr)
+        _, grad, _ = H.oracle_batch(spec, theta, data, order)
+        theta = orn.sgd(theta, grad, lr)
+        got = gb.params.cpu().numpy().astype(np.float64)
+        err = H.normwise_err(got - data.params, theta - data.params)
+        print(f"[case] sgd step {step} update err {err:.2e}", flush=True)
+        assert err < 1e-4
+
+
+def test_sgd_apply_exact():
+    import torch
+    rng = np.random.default_rng(0)
+    for n in (1, 5, 1027, 4096):
+        p = rng.standard_normal(n).astype(np.float32)
+        g = rng.standard_normal(n).astype(np.float32)
+        tp = torch.from_numpy(p).cuda()
+        tg = torch.from_numpy(g).cuda()
+        lib.sgd_apply(tp, tg, 0.25)
+        torch.cuda.synchronize()
+        ref = p.astype(np.float64) - 0.25 * g.astype(np.float64)
+        np.testing.assert_allclose(tp.cpu().numpy(), ref, rtol=1e-6, atol=1e-7)
+
+
+def test_nan_padding_and_determinism():
+    """Pad frames filled with NaN change nothing, and two runs are bitwise equal."""
+    spec = H.Spec(0, 2, 1, 8, 64, 12)
+    data = H.data_from_lengths(spec, [25, 20, 20, 7, 7, 7, 2], seed=9, scale=0.3)
+    order = H.batch_order(data, range(7))
+    a = H.GpuBatch(spec, data.params, data, order).run()
+    b = H.GpuBatch(spec, data.params, data, order, pad_fill=float("nan")).run()
+    c = H.GpuBatch(spec, data.params, data, order).run()
+    for u, v in ((a, b), (a, c)):
+        assert u[0] == v[0]
+        assert np.array_equal(u[1], v[1])
+        assert np.array_equal(u[2], v[2])
+
+
+@pytest.mark.parametrize("b_f", [0.0, 40.0])
+def test_closed_form_long_sequence(b_f):
+    """Zero weights: gates of 1/2 (or a forget gate of exactly 1 with a bias of
+    40), so the cell follows a closed form over 4000 steps."""
+    T = 4000
+    spec = H.Spec(0, 1, 0, 4, 32, 4)
+    m = spec.model()
+    p = {k: np.zeros(s) for k, s in orn.param_layout(m)}
+    bg = np.linspace(-0.002, 0.002, 32) if b_f else np.linspace(-2, 2, 32)
+    p[("b", 0, 0)][64:96] = bg
+    p[("b", 0, 0)][32:64] = b_f
+    theta = orn.pack(m, p).astype(np.float32)
+    data = H.data_from_lengths(spec, [T, T, 3], seed=1)
+    order = H.batch_order(data, range(3))
+    gb = H.GpuBatch(spec, theta, data, order)
+    gb.forward()
+    import torch
+    torch.cuda.synchronize()
+    top = gb.top.cpu().numpy().astype(np.float64)
+    t = np.arange(T)[:, None]
+    tb = np.tanh(bg.astype(np.float32).astype(np.float64))[None, :]
+    c = (t + 1.0) * 0.5 * tb if b_f else tb * (1.0 - 2.0 ** (-(t + 1.0)))
+    h = 0.5 * np.tanh(c)
+    for b in range(2):
+        err = H.normwise_err(top[:, b], h)
+        print(f"[case] closed form b_f={b_f} err {err:.2e}", flush=True)
+        assert err < 1e-5
+
+
+def _workload_batches(name, K, epoch=0):
+    w = synth.WORKLOADS[name]
+    spec = H.Spec.of(w)
+    P = orn.param_count(spec.model())
+    data = synth.make_workload(w, 0, param_count=P)
+    _, bof, keff, _ = lib.bucket_plan(data.lengths, K)
+    batches = lib.epoch_schedule(data.lengths, bof, keff, synth.shuffle_keys(0, epoch, w.n),
+                                 w.batch)
+    return spec, data, bof, batches
+
+
+def _first_of_bucket(data, bof, batches, bucket):
+    for bt in batches:
+        if bof[bt[0]] == bucket:
+            return bt
+    raise AssertionError("bucket not found")
+
+
+def test_lstm2_bench_config_sampled():
+    """The benchmarked configuration (2-layer LSTM, H=128, B=64, K=8): the
+    first batch of the shortest and of the longest bucket, full size."""
+    spec, data, bof, batches = _workload_batches("lstm2", 8)
+    for bucket in (0, 7):
+        order = _first_of_bucket(data, bof, batches, bucket)
+        H.assert_batch_close(spec, data.params, data, order, label=f"lstm2 bucket {bucket}")
+
+
+@pytest.mark.parametrize("name,K", [("bilstm3", 16), ("longtail", 16), ("gru2", 8)])
+def test_workload_sampled_first_bucket(name, K):
+    spec, data, bof, batches = _workload_batches(name, K)
+    order = _first_of_bucket(data, bof, batches, 0)
+    H.assert_batch_close(spec, data.params, data, order, label=f"{name} bucket 0")
