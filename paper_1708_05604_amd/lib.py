@@ -88,6 +88,10 @@ def load():
     global _lib
     if _lib is not None:
         return _lib
+    try:
+        import torch  # noqa: F401  (its HIP runtime must be the one the library binds to)
+    except ImportError:
+        pass
     if not os.path.exists(LIB_PATH):
         raise LibraryMissing(
             f"{LIB_PATH} not found: build it with `python -m paper_1708_05604_amd.build`")
@@ -117,12 +121,19 @@ def _ptr(a: np.ndarray, typ):
     return a.ctypes.data_as(typ)
 
 
-def _dev(t) -> int:
-    """Device address of a tensor (or an int address)."""
+def _dev(t, dtype: Optional[str] = None) -> int:
+    """Device address of a tensor (or an int address).  A tensor must be a
+    contiguous GPU tensor of the expected element type."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if not t.is_cuda:
+        raise ValueError("expected a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    if dtype is not None and str(t.dtype) != "torch." + dtype:
+        raise TypeError(f"expected torch.{dtype}, got {t.dtype}")
     return t.data_ptr()
 
 
@@ -197,29 +208,50 @@ def _nbytes(t) -> int:
     return t.numel() * t.element_size()
 
 
+def _need(t, count: int, what: str):
+    if not isinstance(t, int) and t.numel() < count:
+        raise ValueError(f"{what} holds {t.numel()} elements, needs {count}")
+
+
+def _htop(desc) -> int:
+    return desc.hidden * (2 if desc.bidirectional else 1)
+
+
 def lstm_fwd(desc, params, x, labels, lengths, reserve, workspace, loss, stream=None):
     L = _i32(lengths)
-    _check(load().rnnbkt_lstm_fwd(ctypes.byref(desc), _dev(params), _dev(x), _dev(labels),
-                                  _ptr(L, _i32p), int(L[0]), int(L.size), _dev(reserve),
-                                  _nbytes(reserve), _dev(workspace), _nbytes(workspace),
-                                  _dev(loss), _stream(stream)))
+    T, B = int(L[0]), int(L.size)
+    _need(params, param_count(desc), "params")
+    _need(x, T * B * desc.input_dim, "x")
+    _need(labels, T * B, "labels")
+    _need(loss, 1, "loss")
+    _check(load().rnnbkt_lstm_fwd(ctypes.byref(desc), _dev(params, "float32"),
+                                  _dev(x, "float32"), _dev(labels, "int32"), _ptr(L, _i32p),
+                                  int(L[0]), int(L.size), _dev(reserve), _nbytes(reserve),
+                                  _dev(workspace), _nbytes(workspace), _dev(loss, "float32"),
+                                  _stream(stream)))
 
 
 def lstm_bwd(desc, params, lengths, reserve, workspace, grads, stream=None):
     L = _i32(lengths)
-    _check(load().rnnbkt_lstm_bwd(ctypes.byref(desc), _dev(params), _ptr(L, _i32p), int(L[0]),
-                                  int(L.size), _dev(reserve), _nbytes(reserve), _dev(workspace),
-                                  _nbytes(workspace), _dev(grads), _stream(stream)))
+    _need(params, param_count(desc), "params")
+    _need(grads, param_count(desc), "grads")
+    _check(load().rnnbkt_lstm_bwd(ctypes.byref(desc), _dev(params, "float32"), _ptr(L, _i32p),
+                                  int(L[0]), int(L.size), _dev(reserve), _nbytes(reserve),
+                                  _dev(workspace), _nbytes(workspace), _dev(grads, "float32"),
+                                  _stream(stream)))
 
 
 def sgd_apply(params, grads, lr: float, stream=None, n: Optional[int] = None):
     count = params.numel() if n is None else int(n)
-    _check(load().rnnbkt_sgd_apply(_dev(params), _dev(grads), count, float(lr),
-                                   _stream(stream)))
+    if not isinstance(params, int) and count > min(params.numel(), grads.numel()):
+        raise ValueError("n exceeds the tensors' sizes")
+    _check(load().rnnbkt_sgd_apply(_dev(params, "float32"), _dev(grads, "float32"), count,
+                                   float(lr), _stream(stream)))
 
 
 def top_hidden(desc, lengths, reserve, out, stream=None):
     L = _i32(lengths)
+    _need(out, int(L[0]) * int(L.size) * _htop(desc), "out")
     _check(load().rnnbkt_top_hidden(ctypes.byref(desc), _ptr(L, _i32p), int(L[0]), int(L.size),
-                                    _dev(reserve), _nbytes(reserve), _dev(out),
+                                    _dev(reserve), _nbytes(reserve), _dev(out, "float32"),
                                     _stream(stream)))

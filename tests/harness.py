@@ -92,11 +92,12 @@ class GpuBatch:
         self.x = torch.from_numpy(x).to(device)
         self.y = torch.from_numpy(y).to(device)
         self.params = torch.from_numpy(np.asarray(params, np.float32)).to(device)
-        self.grads = torch.full_like(self.params, float("nan"))
+        self.grads = torch.full_like(self.params, float("nan"), dtype=torch.float32)
         self.reserve = torch.empty(rb, dtype=torch.uint8, device=device)
         self.workspace = torch.empty(wb, dtype=torch.uint8, device=device)
-        self.loss = torch.full((1,), float("nan"), device=device)
-        self.top = torch.full((T, B, spec.htop), float("nan"), device=device)
+        self.loss = torch.full((1,), float("nan"), dtype=torch.float32, device=device)
+        self.top = torch.full((T, B, spec.htop), float("nan"), dtype=torch.float32,
+                              device=device)
 
     def forward(self):
         lib.lstm_fwd(self.desc, self.params, self.x, self.y, self.lens, self.reserve,
@@ -149,7 +150,11 @@ def assert_batch_close(spec: Spec, params, data, order, rtol=None, label=""):
     loss_r, grad_r, top_r = oracle_batch(spec, params, data, order)
     lens = data.lengths[order]
     for b, L in enumerate(lens):
-        assert np.all(top_g[L:, b] == 0.0)
+        bad = np.nonzero(np.any(top_g[L:, b] != 0.0, axis=-1))[0]
+        if bad.size:
+            print(f"[case] {label} row {b} len {L}: pad steps {(bad + L)[:8].tolist()} "
+                  f"hold {top_g[L + bad[0], b, :4].tolist()}", flush=True)
+        assert bad.size == 0, "pad frames of the top-layer output are not zero"
     e_top = normwise_err(top_g, top_r)
     e_loss = abs(loss_g - loss_r) / abs(loss_r)
     errs = block_errors(spec, grad_g, grad_r)

@@ -162,3 +162,12 @@ def test_validation_errors_before_launch():
     assert rc == lib.EINVAL
     rc = L.rnnbkt_sgd_apply(18, 16, 10, 0.1, None)
     assert rc == lib.EINVAL and "aligned" in lib.last_error()
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(lib, "_lib", None)
+    monkeypatch.setattr(lib, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(lib.LibraryMissing):
+        lib.load()
+    with pytest.raises(lib.LibraryMissing):
+        lib.bucket_plan([1, 2], 1)

@@ -13,7 +13,6 @@ import torch
 
 from oracle import rnn
 
-torch.set_default_dtype(torch.float64)
 
 
 def _rand_batch(rng, lengths, D, C):
@@ -26,8 +25,9 @@ def _torch_model(m, theta):
     """Builds torch.nn.LSTM/GRU + Linear holding the oracle's parameters."""
     p = rnn.unpack(m, theta)
     cls = torch.nn.LSTM if m.cell == rnn.LSTM else torch.nn.GRU
-    net = cls(m.input_dim, m.hidden, m.num_layers, bidirectional=bool(m.bidirectional))
-    lin = torch.nn.Linear(m.hidden * m.dirs, m.num_classes)
+    net = cls(m.input_dim, m.hidden, m.num_layers, bidirectional=bool(m.bidirectional),
+              dtype=torch.float64)
+    lin = torch.nn.Linear(m.hidden * m.dirs, m.num_classes, dtype=torch.float64)
     with torch.no_grad():
         for l in range(m.num_layers):
             for d in range(m.dirs):
