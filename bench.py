@@ -1,0 +1,258 @@
+"""Throughput of bucketed LSTM training on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload lstm2] [--K 8]
+
+A step is one mini-batch of the epoch schedule through the whole hot path:
+rnnbkt_lstm_fwd (packing, input projections, recurrent steps, output layer,
+softmax cross-entropy), rnnbkt_lstm_bwd (output-layer gradients,
+backpropagation through time, weight gradients) and rnnbkt_sgd_apply.  The
+bucket plan and the epoch schedule run once on the host before timing (they
+depend only on the lengths) and are timed separately.  Every batch of the
+epoch is staged in device memory before the timed region.  Steps cycle
+through the epoch's batches; the default is one full epoch.
+
+Printed: one JSON line with the metric (useful, i.e. non-pad, timesteps per
+second of fwd+bwd+update), the same epoch at K=1 (the unbucketed baseline),
+pad-waste counts, the fraction of the matrix-core peak, the roofline entry of
+the kernel class that takes the most GPU time (measured with HIP events in a
+second pass over the same batches), and the float64 oracle timed on a
+bounded sample of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_1708_05604_amd import lib, synth  # noqa: E402
+
+METRIC = "useful (non-pad) LSTM timesteps/sec fwd+bwd on 1 GPU; MFMA util %; pad waste %"
+PEAK_TFLOPS = {synth.FP32: 157.3, synth.BF16: 2500.0}
+PEAK_HBM_GBS = 8000.0
+TILE_M = 16
+
+
+def flops_per_useful_step(w: synth.Workload) -> int:
+    """Matrix-core flops per valid frame of one training step (input and
+    recurrent products forward, the same products and the weight gradients
+    backward, output layer forward and backward)."""
+    G = 4 if w.cell == synth.LSTM else 3
+    H, dirs = w.hidden, 2 if w.bidirectional else 1
+    GH = G * H
+    total = 0
+    for layer in range(w.num_layers):
+        din = w.input_dim if layer == 0 else dirs * H
+        fwd = 2 * GH * (din + H)
+        bwd = 2 * GH * din * (2 if layer > 0 else 1) + 4 * GH * H
+        total += dirs * (fwd + bwd)
+    total += 6 * dirs * H * w.num_classes
+    return total
+
+
+def describe(w: synth.Workload, K: int) -> str:
+    cell = "LSTM" if w.cell == synth.LSTM else "GRU"
+    bi = "bidirectional " if w.bidirectional else ""
+    return (f"{w.name}: {w.num_layers}-layer {bi}{cell} D={w.input_dim} H={w.hidden} "
+            f"C={w.num_classes}, {w.n} sequences {w.law}{w.law_args}, B={w.batch}, K={K}, "
+            f"{'bf16' if w.gemm_dtype == synth.BF16 else 'fp32'} GEMMs, seed 0")
+
+
+class Epoch:
+    """One epoch's batches staged on the GPU."""
+
+    def __init__(self, w, data, K, epoch, torch, dev):
+        t0 = time.perf_counter()
+        self.upper, bof, self.keff, self.p_bucket = lib.bucket_plan(data.lengths, K)
+        self.plan_ms = (time.perf_counter() - t0) * 1e3
+        t0 = time.perf_counter()
+        self.batches = lib.epoch_schedule(data.lengths, bof, self.keff,
+                                          synth.shuffle_keys(0, epoch, w.n), w.batch)
+        self.sched_ms = (time.perf_counter() - t0) * 1e3
+        self.lens, self.x, self.y, self.useful = [], [], [], []
+        self.p_batch = 0
+        self.p_exec = 0
+        for order in self.batches:
+            x, y, L = synth.padded_batch(data, order)
+            self.lens.append(L)
+            self.x.append(torch.from_numpy(x).to(dev))
+            self.y.append(torch.from_numpy(y).to(dev))
+            self.useful.append(int(L.sum()))
+            self.p_batch += len(L) * int(L[0])
+            bt = np.bincount(L, minlength=int(L[0]) + 1)[::-1].cumsum()[::-1][1:]
+            self.p_exec += int(np.sum((bt + TILE_M - 1) // TILE_M * TILE_M))
+        self.U = int(sum(self.useful))
+        self.max_T = max(int(L[0]) for L in self.lens)
+        self.max_B = max(len(L) for L in self.lens)
+        self.max_N = max(self.useful)
+
+
+def run_steps(ep, state, first, count, torch):
+    desc, params, grads, reserve, workspace, loss, lr = state
+    useful = 0
+    nb = len(ep.batches)
+    for k in range(count):
+        i = (first + k) % nb
+        lib.lstm_fwd(desc, params, ep.x[i], ep.y[i], ep.lens[i], reserve, workspace, loss)
+        lib.lstm_bwd(desc, params, ep.lens[i], reserve, workspace, grads)
+        lib.sgd_apply(params, grads, lr)
+        useful += ep.useful[i]
+    return useful
+
+
+def timed(ep, state, warmup, steps, torch):
+    run_steps(ep, state, 0, warmup, torch)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    useful = run_steps(ep, state, warmup, steps, torch)
+    b.record()
+    torch.cuda.synchronize()
+    lib.sync_check()
+    return useful, a.elapsed_time(b) / 1e3
+
+
+def cpu_baseline(w, data, ep, budget_s=15.0):
+    """The float64 oracle on the host: first batch of each bucket in turn
+    until about `budget_s` seconds of work, BLAS pinned to one thread."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import rnn as orn
+    m = orn.Model(w.cell, w.num_layers, w.bidirectional, w.input_dim, w.hidden, w.num_classes)
+    theta = data.params.astype(np.float64)
+    firsts = []
+    seen = set()
+    for order in ep.batches:
+        b = int(np.searchsorted(ep.upper, data.lengths[order[0]]))
+        if b not in seen:
+            seen.add(b)
+            firsts.append((b, order))
+    used, useful, t_total = [], 0, 0.0
+    with threadpool_limits(limits=1):
+        for b, order in firsts:
+            xs = [data.X[data.offsets[s]:data.offsets[s + 1]] for s in order]
+            ys = [data.Y[data.offsets[s]:data.offsets[s + 1]] for s in order]
+            t0 = time.perf_counter()
+            _, g, _ = orn.forward_backward(m, theta, xs, ys)
+            orn.sgd(theta, g, 0.1)
+            t_total += time.perf_counter() - t0
+            useful += int(sum(len(y) for y in ys))
+            used.append(b)
+            if t_total >= budget_s:
+                break
+    return {"value": useful / t_total, "unit": "timesteps/s", "cores": 1, "kind": "oracle",
+            "sample": (f"float64 oracle fwd+bwd+SGD on the first batch of buckets {used} "
+                       f"of epoch 0 ({useful} useful timesteps, {t_total:.1f} s, 1 thread)")}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=0, help="0 = one full epoch")
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--workload", default="lstm2", choices=list(synth.WORKLOADS))
+    ap.add_argument("--K", type=int, default=0, help="buckets (0 = largest of the workload)")
+    ap.add_argument("--lr", type=float, default=0.1)
+    ap.add_argument("--no-k1", action="store_true", help="skip the K=1 epoch")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
+    ap.add_argument("--no-timer", action="store_true", help="skip the per-kernel pass")
+    args = ap.parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "the paper's multi-GPU map-reduce is outside this library.", file=sys.stderr)
+        return 2
+
+    import torch
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    lib.load()
+    w = synth.WORKLOADS[args.workload]
+    K = args.K or max(w.k_list)
+    desc = lib.ModelDesc.of(w.cell, w.num_layers, w.input_dim, w.hidden, w.num_classes,
+                            w.bidirectional, w.gemm_dtype)
+    P = lib.param_count(desc)
+    data = synth.make_workload(w, 0, param_count=P)
+
+    ep = Epoch(w, data, K, 0, torch, dev)
+    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev)
+    eps = [e for e in (ep, ep1) if e is not None]
+    rb, wb = lib.buffer_sizes(desc, max(e.max_T for e in eps), max(e.max_B for e in eps),
+                              max(e.max_N for e in eps))
+    reserve = torch.empty(rb, dtype=torch.uint8, device=dev)
+    workspace = torch.empty(wb, dtype=torch.uint8, device=dev)
+    params = torch.from_numpy(data.params).to(dev)
+    grads = torch.zeros_like(params)
+    loss = torch.zeros(1, dtype=torch.float32, device=dev)
+    state = (desc, params, grads, reserve, workspace, loss, args.lr)
+
+    nb = len(ep.batches)
+    steps = args.steps or nb
+    warmup = args.warmup
+    useful, secs = timed(ep, state, warmup, steps, torch)
+    value = useful / secs
+    ms_per_step = secs * 1e3 / steps
+    flops = flops_per_useful_step(w)
+    peak = PEAK_TFLOPS[w.gemm_dtype]
+    out = {
+        "metric": METRIC, "value": value, "unit": "timesteps/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.gemm_dtype == synth.BF16 else "f32", "data": "synthetic",
+        "config": {"workload": describe(w, K), "batches_per_epoch": nb,
+                   "useful_timesteps_per_epoch": ep.U, "parallelism": "single GPU"},
+        "mfma_util_pct": 100.0 * flops * value / (peak * 1e12),
+        "achieved_tflops": flops * value / 1e12,
+        "pad_waste_pct": {"P_batch": 100.0 * (1 - ep.U / ep.p_batch),
+                          "P_bucket": 100.0 * (1 - ep.U / ep.p_bucket),
+                          "P_exec": 100.0 * (1 - ep.U / ep.p_exec)},
+        "bucket_plan_ms": ep.plan_ms, "schedule_ms": ep.sched_ms,
+        "bucket_upper": [int(u) for u in ep.upper],
+    }
+    if ep1 is not None:
+        u1, s1 = timed(ep1, state, warmup, len(ep1.batches), torch)
+        out["k1"] = {"value": u1 / s1, "steps": len(ep1.batches),
+                     "pad_waste_pct_P_batch": 100.0 * (1 - ep1.U / ep1.p_batch)}
+        out["speedup_vs_k1"] = value / (u1 / s1)
+
+    if not args.no_timer:
+        torch.cuda.synchronize()
+        lib.kernel_timer(True)
+        run_steps(ep, state, warmup, steps, torch)
+        torch.cuda.synchronize()
+        lib.kernel_timer(False)
+        kinds = {k: lib.kernel_timer_read(k) for k in lib.KERNEL_KINDS}
+        total_ms = sum(v["ms"] for v in kinds.values())
+        out["kernel_time_share"] = {k: round(v["ms"] / total_ms, 4) for k, v in kinds.items()}
+        dom = max(kinds, key=lambda k: kinds[k]["ms"])
+        d = kinds[dom]
+        avg_s = d["ms"] / 1e3 / max(d["launches"], 1)
+        if d["flops"] > 0:
+            ach = d["flops"] / max(d["launches"], 1) / avg_s / 1e12
+            roof = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                    "frac": ach / peak, "traffic": None}
+        else:
+            ach = d["bytes"] / max(d["launches"], 1) / avg_s / 1e9
+            roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": ach / PEAK_HBM_GBS, "traffic": None}
+        roof.update({"kernel": dom, "avg_launch_us": avg_s * 1e6, "launches": d["launches"]})
+        out["roofline"] = roof
+        out["kernels"] = {k: {"ms": v["ms"], "launches": v["launches"],
+                              "avg_us": 1e3 * v["ms"] / max(v["launches"], 1)}
+                          for k, v in kinds.items()}
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(w, data, ep)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -117,9 +117,9 @@ int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* bucket_of,
 typedef struct {
   int32_t cell;          /* RNNBKT_CELL_LSTM or RNNBKT_CELL_GRU */
   int32_t num_layers;    /* >= 1 */
-  int32_t input_dim;     /* >= 1 */
+  int32_t input_dim;     /* multiple of 4 */
   int32_t hidden;        /* multiple of 32 */
-  int32_t num_classes;   /* 1..1024 */
+  int32_t num_classes;   /* multiple of 4, at most 1024 */
   int32_t bidirectional; /* 0 or 1 */
   int32_t gemm_dtype;    /* RNNBKT_GEMM_FP32 or RNNBKT_GEMM_BF16 */
 } rnnbkt_model_desc;
@@ -172,7 +172,8 @@ int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_
  *              -log softmax(W_out h_top + b_out)[label]
  * The loss gradient w.r.t. the logits is computed here and kept in reserve.
  * Errors: EINVAL (null pointer, bad lengths, buffers too small),
- * EUNSUPPORTED (hidden % 32 != 0, num_classes > 1024), EHIP.
+ * EUNSUPPORTED (hidden % 32 != 0, input_dim % 4 != 0, num_classes % 4 != 0
+ * or > 1024), EHIP.
  */
 int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* params,
                         const float* x, const int32_t* labels,
@@ -206,6 +207,33 @@ int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,
 int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
                           int32_t T_max, int32_t B, const void* reserve,
                           size_t reserve_bytes, float* out, void* stream);
+
+/*
+ * Kernel timer -- measurement support for the benchmark (not part of the
+ * method).  While enabled, the model calls and rnnbkt_sgd_apply bracket every
+ * kernel launch with a pair of HIP events recorded on the call's stream and
+ * note the launch's algorithmic work: recurrent steps count the flops of
+ * their h.W_hh (forward) or dA.W_hh (backward) product, GEMMs 2*M*N*K,
+ * the loss kernel 8*C+4 bytes per frame, SGD 12 bytes per parameter.
+ * Kinds: see RNNBKT_KERNEL_*.  The events add a small gap between launches,
+ * so time a run with the timer off and use the timer in a separate pass.
+ *   rnnbkt_kernel_timer(1) clears the records and starts recording,
+ *   rnnbkt_kernel_timer(0) stops.  Host-side state, one per process.
+ *   rnnbkt_kernel_timer_read waits for the recorded events and returns, for
+ *   one kind, the summed event-to-event time (ms), the number of launches
+ *   and the summed algorithmic flops and bytes.
+ */
+#define RNNBKT_KERNEL_STEP_FWD 0 /* recurrent step, forward */
+#define RNNBKT_KERNEL_STEP_BWD 1 /* recurrent step, backward through time */
+#define RNNBKT_KERNEL_GEMM 2     /* dense contractions incl. split-K folds */
+#define RNNBKT_KERNEL_XENT 3     /* softmax cross-entropy and its gradient */
+#define RNNBKT_KERNEL_SGD 4      /* parameter update */
+#define RNNBKT_KERNEL_OTHER 5    /* batch tables, packing, column sums, loss sum */
+#define RNNBKT_KERNEL_KINDS 6
+
+int32_t rnnbkt_kernel_timer(int32_t enable);
+int32_t rnnbkt_kernel_timer_read(int32_t kind, double* total_ms, int64_t* launches,
+                                 double* alg_flops, double* alg_bytes);
 
 #ifdef __cplusplus
 }

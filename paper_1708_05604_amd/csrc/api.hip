@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "common.h"
@@ -204,6 +205,53 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
     }                                                                                 \
   } while (0)
 
+// ---------------------------------------------------------------- kernel timer
+struct TimerRec {
+  int kind;
+  hipEvent_t a, b;
+  double flops, bytes;
+};
+std::mutex g_tmu;
+bool g_timer_on = false;
+std::vector<TimerRec> g_recs;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t pooled_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Brackets one launch with events when the timer is on.
+class Timed {
+ public:
+  Timed(int kind, double flops, double bytes, hipStream_t st) : st_(st) {
+    if (!g_timer_on) return;
+    std::lock_guard<std::mutex> lk(g_tmu);
+    rec_.kind = kind;
+    rec_.flops = flops;
+    rec_.bytes = bytes;
+    rec_.a = pooled_event();
+    rec_.b = pooled_event();
+    if (rec_.a && rec_.b && hipEventRecord(rec_.a, st_) == hipSuccess) active_ = true;
+  }
+  ~Timed() {
+    if (!active_) return;
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (hipEventRecord(rec_.b, st_) == hipSuccess) g_recs.push_back(rec_);
+  }
+
+ private:
+  hipStream_t st_;
+  TimerRec rec_{};
+  bool active_ = false;
+};
+
 // Host copy of the batch tables (active rows per step and frame offsets).
 void host_tables(const int32_t* len, int T, int B, std::vector<int>& bs, std::vector<int>& off) {
   bs.assign(T, 0);
@@ -248,6 +296,7 @@ hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t
     g.partial = splitk_buf;
   }
   if (M == 0 || N == 0) return hipSuccess;
+  Timed tm(RNNBKT_KERNEL_GEMM, 2.0 * M * N * K, 0.0, st);
   hipError_t e = launch_gemm(g, a_kc, b_kc, bf16, st);
   if (e != hipSuccess || g.splits == 1) return e;
   return launch_splitk_reduce(splitk_buf, g.splits, M, N, C, ldc, bias, accumulate, st);
@@ -328,8 +377,11 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   float* gx = at<float>(workspace, c.gx);
   float* lp = at<float>(workspace, c.loss_part);
 
-  RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
-  RNNBKT_HIP(launch_pack(x, labels, d_bs, d_off, T, B, s.D, Xp, Yp, pf, pr, st));
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
+    RNNBKT_HIP(launch_pack(x, labels, d_bs, d_off, T, B, s.D, Xp, Yp, pf, pr, st));
+  }
 
   const int GH = s.G * s.H;
   for (int l = 0; l < s.L; ++l) {
@@ -361,6 +413,7 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
           a.prev0 = t + 1 < T ? off[t + 1] : 0;
           a.prev_rows = t + 1 < T ? bs[t + 1] : 0;
         }
+        Timed tm(RNNBKT_KERNEL_STEP_FWD, 2.0 * a.prev_rows * GH * s.H, 0.0, st);
         RNNBKT_HIP(launch_step_fwd(a, s.cell, s.bf16, st));
       }
     }
@@ -370,8 +423,14 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   RNNBKT_HIP(gemm(top, s.Htop, true, params + po.wout, s.Htop, true, dz, s.C, (int)N, s.C,
                   s.Htop, params + po.bout, 0, s.bf16, st));
   int32_t nparts = 0;
-  RNNBKT_HIP(launch_softmax_xent(dz, Yp, N, s.C, lp, &nparts, st));
-  RNNBKT_HIP(launch_sum(lp, nparts, 1.0f / (float)N, loss, st));
+  {
+    Timed tm(RNNBKT_KERNEL_XENT, 0.0, (8.0 * s.C + 4.0) * N, st);
+    RNNBKT_HIP(launch_softmax_xent(dz, Yp, N, s.C, lp, &nparts, st));
+  }
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    RNNBKT_HIP(launch_sum(lp, nparts, 1.0f / (float)N, loss, st));
+  }
   return RNNBKT_OK;
 }
 
@@ -421,7 +480,10 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                   nullptr, 0, s.bf16, st));
   RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
                   nullptr, 0, s.bf16, st, nullptr, sk));
-  RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, kColsumRows, cs, grads + po.bout, st));
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, kColsumRows, cs, grads + po.bout, st));
+  }
 
   float* dh_in = dha;
   float* dx = dhb;
@@ -459,6 +521,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
           a.prev0 = t + 1 < T ? off[t + 1] : 0;
           a.prev_rows = t + 1 < T ? bs[t + 1] : 0;
         }
+        Timed tm(RNNBKT_KERNEL_STEP_BWD, 2.0 * a.next_rows * GH * s.H, 0.0, st);
         RNNBKT_HIP(launch_step_bwd(a, s.cell, s.bf16, st));
       }
       // Weight gradients reduced over every valid frame.
@@ -468,9 +531,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                       nullptr, 0, s.bf16, st, nullptr, sk));
       RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
                       s.H, GH, s.H, n, nullptr, 0, s.bf16, st, d == 0 ? pf : pr, sk));
-      RNNBKT_HIP(launch_colsum(dax, N, GH, GH, kColsumRows, cs, grads + po.b[ld], st));
-      if (s.cell == RNNBKT_CELL_GRU)
-        RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, kColsumRows, cs, grads + po.bhh[ld], st));
+      {
+        Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+        RNNBKT_HIP(launch_colsum(dax, N, GH, GH, kColsumRows, cs, grads + po.b[ld], st));
+        if (s.cell == RNNBKT_CELL_GRU)
+          RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, kColsumRows, cs, grads + po.bhh[ld], st));
+      }
       if (l > 0)
         RNNBKT_HIP(gemm(dax, GH, true, params + po.wih[ld], din, false, dx, din, n, din, GH,
                         nullptr, d > 0 ? 1 : 0, s.bf16, st));
@@ -488,7 +554,50 @@ extern "C" int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n
   RNNBKT_REQUIRE(aligned16(params) && aligned16(grads), RNNBKT_EINVAL,
                  "sgd_apply: params and grads must be 16-byte aligned");
   if (n == 0) return RNNBKT_OK;
-  RNNBKT_HIP(launch_sgd(params, grads, n, lr, static_cast<hipStream_t>(stream)));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Timed tm(RNNBKT_KERNEL_SGD, 0.0, 12.0 * n, st);
+  RNNBKT_HIP(launch_sgd(params, grads, n, lr, st));
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_kernel_timer(int32_t enable) {
+  clear_error();
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (enable) {
+    for (auto& r : g_recs) {
+      g_pool.push_back(r.a);
+      g_pool.push_back(r.b);
+    }
+    g_recs.clear();
+  }
+  g_timer_on = enable != 0;
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_kernel_timer_read(int32_t kind, double* total_ms, int64_t* launches,
+                                            double* alg_flops, double* alg_bytes) {
+  clear_error();
+  RNNBKT_REQUIRE(kind >= 0 && kind < RNNBKT_KERNEL_KINDS, RNNBKT_EINVAL,
+                 "kernel_timer_read: kind %d out of range", kind);
+  RNNBKT_REQUIRE(total_ms && launches && alg_flops && alg_bytes, RNNBKT_EINVAL,
+                 "kernel_timer_read: null pointer");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  double ms = 0.0, fl = 0.0, by = 0.0;
+  int64_t cnt = 0;
+  for (auto& r : g_recs) {
+    if (r.kind != kind) continue;
+    RNNBKT_HIP(hipEventSynchronize(r.b));
+    float e = 0.f;
+    RNNBKT_HIP(hipEventElapsedTime(&e, r.a, r.b));
+    ms += e;
+    fl += r.flops;
+    by += r.bytes;
+    ++cnt;
+  }
+  *total_ms = ms;
+  *launches = cnt;
+  *alg_flops = fl;
+  *alg_bytes = by;
   return RNNBKT_OK;
 }
 

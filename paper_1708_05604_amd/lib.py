@@ -78,7 +78,13 @@ _SIGNATURES = {
     "rnnbkt_sgd_apply": (ctypes.c_int32, [_vp, _vp, ctypes.c_int64, ctypes.c_float, _vp]),
     "rnnbkt_top_hidden": (ctypes.c_int32, [_descp, _i32p, ctypes.c_int32, ctypes.c_int32, _vp,
                                            ctypes.c_size_t, _vp, _vp]),
+    "rnnbkt_kernel_timer": (ctypes.c_int32, [ctypes.c_int32]),
+    "rnnbkt_kernel_timer_read": (ctypes.c_int32, [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                                                  _i64p, ctypes.POINTER(ctypes.c_double),
+                                                  ctypes.POINTER(ctypes.c_double)]),
 }
+
+KERNEL_KINDS = {"step_fwd": 0, "step_bwd": 1, "gemm": 2, "xent": 3, "sgd": 4, "other": 5}
 
 _lib = None
 
@@ -255,3 +261,18 @@ def top_hidden(desc, lengths, reserve, out, stream=None):
     _check(load().rnnbkt_top_hidden(ctypes.byref(desc), _ptr(L, _i32p), int(L[0]), int(L.size),
                                     _dev(reserve), _nbytes(reserve), _dev(out, "float32"),
                                     _stream(stream)))
+
+
+def kernel_timer(enable: bool):
+    _check(load().rnnbkt_kernel_timer(1 if enable else 0))
+
+
+def kernel_timer_read(kind: str):
+    """-> dict(ms, launches, flops, bytes) summed over the recorded launches."""
+    ms = ctypes.c_double(0)
+    fl = ctypes.c_double(0)
+    by = ctypes.c_double(0)
+    n = ctypes.c_int64(0)
+    _check(load().rnnbkt_kernel_timer_read(KERNEL_KINDS[kind], ctypes.byref(ms), ctypes.byref(n),
+                                           ctypes.byref(fl), ctypes.byref(by)))
+    return {"ms": ms.value, "launches": n.value, "flops": fl.value, "bytes": by.value}
