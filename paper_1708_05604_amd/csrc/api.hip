@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -103,7 +104,7 @@ SplitK choose_splitk(int64_t M, int64_t N, int64_t K) {
   return SplitK{(int)S, (int)kps};
 }
 
-constexpr int64_t kColsumRows = 512;
+constexpr int64_t kColsumRows = 64;
 
 // Byte offsets of every buffer a batch uses.
 struct Carve {
@@ -113,10 +114,13 @@ struct Carve {
   std::vector<size_t> stash, cst;  // per layer*dirs
   size_t reserve;
   // workspace (forward)
-  size_t gx, loss_part;
+  size_t gx[2], loss_part;
   size_t ws_fwd;
   // workspace (backward)
-  size_t dha, dhb, da, dah, carry, splitk, colsum;
+  size_t dha, dhb, da[2], dah[2], carry, splitk, colsum;
+  // workspace (both): grid-barrier counters, one per persistent launch
+  size_t barriers;
+  int nbarriers;
   size_t ws_bwd;
   size_t workspace;
 };
@@ -145,16 +149,21 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     }
   c.reserve = pos;
 
+  // Barrier counters first so the forward and backward regions can overlap.
   pos = 0;
-  c.gx = take(sizeof(float) * N * GH);
+  c.nbarriers = s.L;
+  c.barriers = take(sizeof(unsigned) * c.nbarriers);
+  const size_t common = pos;
+  for (int d = 0; d < 2; ++d) c.gx[d] = d < s.dirs ? take(sizeof(float) * N * GH) : c.gx[0];
   c.loss_part = take(sizeof(float) * ((N + 15) / 16 + 1));
   c.ws_fwd = pos;
 
-  pos = 0;
+  pos = common;
   c.dha = take(sizeof(float) * N * s.Htop);
   c.dhb = take(sizeof(float) * N * s.Htop);
-  c.da = take(sizeof(float) * N * GH);
-  c.dah = s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0;
+  for (int d = 0; d < 2; ++d) c.da[d] = d < s.dirs ? take(sizeof(float) * N * GH) : c.da[0];
+  for (int d = 0; d < 2; ++d)
+    c.dah[d] = (s.cell == RNNBKT_CELL_GRU && d < s.dirs) ? take(sizeof(float) * N * GH) : c.dah[0];
   c.carry = take(sizeof(float) * (size_t)B * s.H);
   size_t sk = 0;
   auto need = [&](int64_t M, int64_t Nn, int64_t K) {
@@ -261,6 +270,13 @@ void host_tables(const int32_t* len, int T, int B, std::vector<int>& bs, std::ve
   for (int t = 0; t < T; ++t) off[t + 1] = off[t] + bs[t];
 }
 
+// Recurrence kernels: "persistent" (default; all steps of a layer in one
+// launch) or "steps" (one launch per time step).  RNNBKT_RECURRENCE selects.
+bool use_persistent() {
+  const char* e = getenv("RNNBKT_RECURRENCE");
+  return !(e && strcmp(e, "steps") == 0);
+}
+
 template <typename P>
 P* at(void* base, size_t off) {
   return reinterpret_cast<P*>(static_cast<char*>(base) + off);
@@ -314,6 +330,11 @@ extern "C" int32_t rnnbkt_sync_check(void* stream) {
   clear_error();
   RNNBKT_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
   RNNBKT_HIP(hipGetLastError());
+  unsigned timeouts = 0;
+  RNNBKT_HIP(read_barrier_timeouts(&timeouts));
+  RNNBKT_REQUIRE(timeouts == 0, RNNBKT_EHIP,
+                 "%u grid-barrier waits timed out: results of the affected launches are invalid",
+                 timeouts);
   return RNNBKT_OK;
 }
 
@@ -374,27 +395,55 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   int32_t* pf = at<int32_t>(reserve, c.prev_f);
   int32_t* pr = at<int32_t>(reserve, c.prev_r);
   float* dz = at<float>(reserve, c.dz);
-  float* gx = at<float>(workspace, c.gx);
   float* lp = at<float>(workspace, c.loss_part);
+  unsigned* bars = at<unsigned>(workspace, c.barriers);
 
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
     RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
     RNNBKT_HIP(launch_pack(x, labels, d_bs, d_off, T, B, s.D, Xp, Yp, pf, pr, st));
+    RNNBKT_HIP(launch_zero_u32(bars, c.nbarriers, st));
   }
 
   const int GH = s.G * s.H;
+  const bool persistent = use_persistent();
   for (int l = 0; l < s.L; ++l) {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
     const int din = s.din(l);
     float* hout = at<float>(reserve, c.hout[l]);
+    // Input projection of every valid frame at once (bias folded in).
     for (int d = 0; d < s.dirs; ++d) {
       const int ld = l * s.dirs + d;
-      // Input projection of every valid frame at once (bias folded in).
-      RNNBKT_HIP(gemm(xin, din, true, params + po.wih[ld], din, true, gx, GH, (int)N, GH, din,
-                      params + po.b[ld], 0, s.bf16, st));
+      RNNBKT_HIP(gemm(xin, din, true, params + po.wih[ld], din, true, at<float>(workspace, c.gx[d]),
+                      GH, (int)N, GH, din, params + po.b[ld], 0, s.bf16, st));
+    }
+    bool done = false;
+    if (persistent) {
+      PersistFwdArgs a{};
+      for (int d = 0; d < s.dirs; ++d) {
+        const int ld = l * s.dirs + d;
+        a.gx[d] = at<float>(workspace, c.gx[d]);
+        a.whh[d] = params + po.whh[ld];
+        a.bhh[d] = s.cell == RNNBKT_CELL_GRU ? params + po.bhh[ld] : nullptr;
+        a.stash[d] = at<float>(reserve, c.stash[ld]);
+        a.cst[d] = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+      }
+      a.hout = hout;
+      a.bs = d_bs;
+      a.off = d_off;
+      a.barrier = bars + l;
+      a.H = s.H;
+      a.ldh = s.dirs * s.H;
+      a.T = T;
+      double fl = 0;
+      for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * GH * s.H;
+      Timed tm(RNNBKT_KERNEL_STEP_FWD, fl, 0.0, st);
+      RNNBKT_HIP(launch_fwd_persistent(a, s.cell, s.bf16, B, s.dirs, st, &done));
+    }
+    for (int d = 0; d < s.dirs && !done; ++d) {
+      const int ld = l * s.dirs + d;
       StepFwdArgs a{};
-      a.gx = gx;
+      a.gx = at<float>(workspace, c.gx[d]);
       a.whh = params + po.whh[ld];
       a.bhh = s.cell == RNNBKT_CELL_GRU ? params + po.bhh[ld] : nullptr;
       a.hout = hout + d * s.H;
@@ -460,19 +509,26 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   std::vector<int> bs, off;
   host_tables(lengths, T, B, bs, off);
 
+  const int32_t* d_bs = at<int32_t>(reserve, c.bs);
+  const int32_t* d_off = at<int32_t>(reserve, c.off);
   const float* Xp = at<float>(reserve, c.xp);
   const int32_t* pf = at<int32_t>(reserve, c.prev_f);
   const int32_t* pr = at<int32_t>(reserve, c.prev_r);
   const float* dz = at<float>(reserve, c.dz);
   float* dha = at<float>(workspace, c.dha);
   float* dhb = at<float>(workspace, c.dhb);
-  float* da = at<float>(workspace, c.da);
-  float* dah = s.cell == RNNBKT_CELL_GRU ? at<float>(workspace, c.dah) : nullptr;
   float* carry = at<float>(workspace, c.carry);
   float* sk = at<float>(workspace, c.splitk);
   float* cs = at<float>(workspace, c.colsum);
+  unsigned* bars = at<unsigned>(workspace, c.barriers);
   const int GH = s.G * s.H;
   const int n = (int)N;
+  const bool gru = s.cell == RNNBKT_CELL_GRU;
+  const bool persistent = use_persistent();
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    RNNBKT_HIP(launch_zero_u32(bars, c.nbarriers, st));
+  }
 
   // Output layer: dH_top = dZ W_out, dW_out = dZ^T H_top, db_out = colsum dZ.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
@@ -491,17 +547,42 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
     const int din = s.din(l);
     const float* hout = at<float>(reserve, c.hout[l]);
-    for (int d = 0; d < s.dirs; ++d) {
+    bool done = false;
+    if (persistent) {
+      PersistBwdArgs a{};
+      for (int d = 0; d < s.dirs; ++d) {
+        const int ld = l * s.dirs + d;
+        a.whh[d] = params + po.whh[ld];
+        a.stash[d] = at<float>(reserve, c.stash[ld]);
+        a.cst[d] = gru ? nullptr : at<float>(reserve, c.cst[ld]);
+        a.da[d] = at<float>(workspace, c.da[d]);
+        a.dah[d] = gru ? at<float>(workspace, c.dah[d]) : nullptr;
+      }
+      a.hout = hout;
+      a.dh_in = dh_in;
+      a.bs = d_bs;
+      a.off = d_off;
+      a.barrier = bars + l;
+      a.H = s.H;
+      a.ldh = s.dirs * s.H;
+      a.ldd = s.Htop;
+      a.T = T;
+      double fl = 0;
+      for (int t = 1; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * GH * s.H;
+      Timed tm(RNNBKT_KERNEL_STEP_BWD, fl, 0.0, st);
+      RNNBKT_HIP(launch_bwd_persistent(a, s.cell, s.bf16, B, s.dirs, st, &done));
+    }
+    for (int d = 0; d < s.dirs && !done; ++d) {
       const int ld = l * s.dirs + d;
       StepBwdArgs a{};
-      a.da_next = s.cell == RNNBKT_CELL_GRU ? dah : da;
+      a.da_next = gru ? at<float>(workspace, c.dah[d]) : at<float>(workspace, c.da[d]);
       a.whh = params + po.whh[ld];
       a.dh_in = dh_in + d * s.H;
       a.stash = at<float>(reserve, c.stash[ld]);
-      a.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+      a.cst = gru ? nullptr : at<float>(reserve, c.cst[ld]);
       a.hout = hout + d * s.H;
-      a.da = da;
-      a.dah = dah;
+      a.da = at<float>(workspace, c.da[d]);
+      a.dah = gru ? at<float>(workspace, c.dah[d]) : nullptr;
       a.carry = carry;
       a.H = s.H;
       a.ldd = s.Htop;
@@ -524,9 +605,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         Timed tm(RNNBKT_KERNEL_STEP_BWD, 2.0 * a.next_rows * GH * s.H, 0.0, st);
         RNNBKT_HIP(launch_step_bwd(a, s.cell, s.bf16, st));
       }
-      // Weight gradients reduced over every valid frame.
-      const float* dax = da;
-      const float* dahh = s.cell == RNNBKT_CELL_GRU ? dah : da;
+    }
+    // Weight gradients reduced over every valid frame.
+    for (int d = 0; d < s.dirs; ++d) {
+      const int ld = l * s.dirs + d;
+      const float* dax = at<float>(workspace, c.da[d]);
+      const float* dahh = gru ? at<float>(workspace, c.dah[d]) : dax;
       RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
                       nullptr, 0, s.bf16, st, nullptr, sk));
       RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
@@ -534,7 +618,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       {
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
         RNNBKT_HIP(launch_colsum(dax, N, GH, GH, kColsumRows, cs, grads + po.b[ld], st));
-        if (s.cell == RNNBKT_CELL_GRU)
+        if (gru)
           RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, kColsumRows, cs, grads + po.bhh[ld], st));
       }
       if (l > 0)

@@ -175,7 +175,20 @@ __global__ void k_sgd(float* __restrict__ p, const float* __restrict__ g, int64_
   }
 }
 
+__global__ void k_zero_u32(unsigned* p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
 }  // namespace
+
+hipError_t launch_zero_u32(unsigned* p, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int threads = 256;
+  hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((n + threads - 1) / threads)), dim3(threads), 0,
+                     st, p, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_batch_tables(const int32_t* lengths, int32_t B, int32_t T, int32_t* bs,
                                int32_t* off, hipStream_t st) {

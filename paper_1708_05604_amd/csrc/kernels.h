@@ -118,4 +118,50 @@ struct StepBwdArgs {
 hipError_t launch_step_fwd(const StepFwdArgs& a, int cell, bool bf16, hipStream_t stream);
 hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_t stream);
 
+// ---------------------------------------------------------------- persistent recurrence
+// All T steps of one layer (both directions) in one cooperative launch.
+// Tables bs/off are the device batch tables; `barrier` is a zeroed counter
+// owned by this launch.  *fits reports whether the grid can be resident at
+// once; when it cannot, nothing is launched.
+struct PersistFwdArgs {
+  const float* gx[2];
+  const float* whh[2];
+  const float* bhh[2];
+  float* stash[2];
+  float* cst[2];
+  float* hout;  // layer output [N x ldh]; direction d at column d*H
+  const int32_t* bs;
+  const int32_t* off;
+  unsigned* barrier;
+  int32_t H, ldh, T;
+  int32_t slices, rgroups;  // set by the launcher
+};
+
+struct PersistBwdArgs {
+  const float* whh[2];
+  const float* stash[2];
+  const float* cst[2];
+  const float* hout;   // layer output, direction d at column d*H
+  const float* dh_in;  // gradient w.r.t. the layer output, direction d at column d*H
+  float* da[2];
+  float* dah[2];
+  const int32_t* bs;
+  const int32_t* off;
+  unsigned* barrier;
+  int32_t H, ldh, ldd, T;
+  int32_t slices, rgroups;
+};
+
+hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, int dirs,
+                                 hipStream_t stream, bool* fits);
+hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
+                                 hipStream_t stream, bool* fits);
+int persistent_fwd_blocks(int H, int B, int dirs);
+int persistent_bwd_blocks(int H, int B, int dirs);
+// Number of grid-barrier waits that gave up (should stay 0).
+hipError_t read_barrier_timeouts(unsigned* count);
+
+// Fills n 32-bit words with zero (a kernel, so it may sit in a captured graph).
+hipError_t launch_zero_u32(unsigned* p, int64_t n, hipStream_t stream);
+
 }  // namespace rnnbkt

@@ -57,6 +57,37 @@ def test_shapes(label, spec, lengths):
     H.assert_batch_close(spec, data.params, data, order, label=label)
 
 
+STEP_SHAPES = [s for s in SHAPES if s[0] in ("lstm-h64-b37-ragged", "lstm-2l-bi", "gru-bi",
+                                              "lstm-bf16-2l-bi", "gru-bf16", "one-long")]
+
+
+@pytest.mark.parametrize("label,spec,lengths", STEP_SHAPES, ids=[s[0] for s in STEP_SHAPES])
+def test_shapes_per_step_kernels(label, spec, lengths, monkeypatch):
+    """The one-launch-per-step recurrence kernels (the alternative to the
+    persistent ones) on the same cases."""
+    monkeypatch.setenv("RNNBKT_RECURRENCE", "steps")
+    data = H.data_from_lengths(spec, lengths, seed=len(label), scale=0.3)
+    order = H.batch_order(data, range(len(lengths)))
+    H.assert_batch_close(spec, data.params, data, order, label="steps " + label)
+
+
+def test_persistent_and_per_step_agree():
+    """Both recurrence implementations give the same numbers (to rounding)."""
+    import os
+    spec = H.Spec(0, 2, 1, 8, 64, 12)
+    data = H.data_from_lengths(spec, [33, 20, 20, 7, 7, 7, 2, 1, 1], seed=3, scale=0.3)
+    order = H.batch_order(data, range(9))
+    a = H.GpuBatch(spec, data.params, data, order).run()
+    os.environ["RNNBKT_RECURRENCE"] = "steps"
+    try:
+        b = H.GpuBatch(spec, data.params, data, order).run()
+    finally:
+        del os.environ["RNNBKT_RECURRENCE"]
+    assert abs(a[0] - b[0]) <= 1e-6 * abs(b[0])
+    assert H.normwise_err(a[1], b[1]) < 1e-5
+    assert H.normwise_err(a[2], b[2]) < 1e-5
+
+
 def test_sgd_trajectory_tiny():
     """Three SGD steps on one batch: parameters follow the oracle's."""
     spec = H.Spec(0, 1, 0, 4, 32, 20)
