@@ -46,19 +46,23 @@ __device__ inline bf8 to_bf8(f4 lo, f4 hi) {
 
 // Every workgroup of the grid arrives once per call; returns when all
 // `target` arrivals (cumulative over the launch) have happened.  The wait
-// is bounded: after ~2^22 polls the workgroup gives up, counts a timeout
-// (reported by rnnbkt_sync_check) and continues, so the launch always ends.
+// is bounded: after ~2^20 polls (about a second) the workgroup gives up and
+// counts a timeout; once any timeout has been counted, later waits return
+// at once.  The launch therefore always ends, and rnnbkt_sync_check reports
+// the timeout as an error.
 __device__ inline void grid_barrier(unsigned* counter, unsigned target) {
   __syncthreads();
   if (threadIdx.x == 0) {
     __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    unsigned spins = 0;
-    while (__hip_atomic_load(counter, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      __builtin_amdgcn_s_sleep(1);
-      if (++spins == (1u << 22)) {
-        __hip_atomic_fetch_add(&g_barrier_timeouts, 1u, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        break;
+    if (__hip_atomic_load(&g_barrier_timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+      unsigned spins = 0;
+      while (__hip_atomic_load(counter, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++spins == (1u << 20)) {
+          __hip_atomic_fetch_add(&g_barrier_timeouts, 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
       }
     }
   }
