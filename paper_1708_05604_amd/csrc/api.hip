@@ -118,9 +118,7 @@ struct Carve {
   size_t ws_fwd;
   // workspace (backward)
   size_t dha, dhb, da[2], dah[2], carry, splitk, colsum;
-  // workspace (both): grid-barrier counters, one per persistent launch
-  size_t barriers;
-  int nbarriers;
+
   size_t ws_bwd;
   size_t workspace;
 };
@@ -149,10 +147,7 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     }
   c.reserve = pos;
 
-  // Barrier counters first so the forward and backward regions can overlap.
   pos = 0;
-  c.nbarriers = s.L;
-  c.barriers = take(sizeof(unsigned) * c.nbarriers);
   const size_t common = pos;
   for (int d = 0; d < 2; ++d) c.gx[d] = d < s.dirs ? take(sizeof(float) * N * GH) : c.gx[0];
   c.loss_part = take(sizeof(float) * ((N + 15) / 16 + 1));
@@ -331,9 +326,9 @@ extern "C" int32_t rnnbkt_sync_check(void* stream) {
   RNNBKT_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
   RNNBKT_HIP(hipGetLastError());
   unsigned timeouts = 0;
-  RNNBKT_HIP(read_barrier_timeouts(&timeouts));
+  RNNBKT_HIP(read_wait_timeouts(&timeouts));
   RNNBKT_REQUIRE(timeouts == 0, RNNBKT_EHIP,
-                 "%u grid-barrier waits timed out: results of the affected launches are invalid",
+                 "%u waits for values published by other workgroups timed out: results of the affected launches are invalid",
                  timeouts);
   return RNNBKT_OK;
 }
@@ -396,13 +391,11 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   int32_t* pr = at<int32_t>(reserve, c.prev_r);
   float* dz = at<float>(reserve, c.dz);
   float* lp = at<float>(workspace, c.loss_part);
-  unsigned* bars = at<unsigned>(workspace, c.barriers);
 
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
     RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
     RNNBKT_HIP(launch_pack(x, labels, d_bs, d_off, T, B, s.D, Xp, Yp, pf, pr, st));
-    RNNBKT_HIP(launch_zero_u32(bars, c.nbarriers, st));
   }
 
   const int GH = s.G * s.H;
@@ -431,12 +424,16 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
       a.hout = hout;
       a.bs = d_bs;
       a.off = d_off;
-      a.barrier = bars + l;
       a.H = s.H;
       a.ldh = s.dirs * s.H;
       a.T = T;
       double fl = 0;
       for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * GH * s.H;
+      {
+        Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+        RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(hout), N * s.dirs * s.H,
+                                   kPublishSentinel, st));
+      }
       Timed tm(RNNBKT_KERNEL_STEP_FWD, fl, 0.0, st);
       RNNBKT_HIP(launch_fwd_persistent(a, s.cell, s.bf16, B, s.dirs, st, &done));
     }
@@ -520,15 +517,10 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   float* carry = at<float>(workspace, c.carry);
   float* sk = at<float>(workspace, c.splitk);
   float* cs = at<float>(workspace, c.colsum);
-  unsigned* bars = at<unsigned>(workspace, c.barriers);
   const int GH = s.G * s.H;
   const int n = (int)N;
   const bool gru = s.cell == RNNBKT_CELL_GRU;
   const bool persistent = use_persistent();
-  {
-    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-    RNNBKT_HIP(launch_zero_u32(bars, c.nbarriers, st));
-  }
 
   // Output layer: dH_top = dZ W_out, dW_out = dZ^T H_top, db_out = colsum dZ.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
@@ -562,13 +554,18 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       a.dh_in = dh_in;
       a.bs = d_bs;
       a.off = d_off;
-      a.barrier = bars + l;
       a.H = s.H;
       a.ldh = s.dirs * s.H;
       a.ldd = s.Htop;
       a.T = T;
       double fl = 0;
       for (int t = 1; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * GH * s.H;
+      {
+        Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+        for (int d = 0; d < s.dirs; ++d)
+          RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(gru ? a.dah[d] : a.da[d]),
+                                     N * GH, kPublishSentinel, st));
+      }
       Timed tm(RNNBKT_KERNEL_STEP_BWD, fl, 0.0, st);
       RNNBKT_HIP(launch_bwd_persistent(a, s.cell, s.bf16, B, s.dirs, st, &done));
     }

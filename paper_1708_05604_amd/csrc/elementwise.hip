@@ -175,18 +175,23 @@ __global__ void k_sgd(float* __restrict__ p, const float* __restrict__ g, int64_
   }
 }
 
-__global__ void k_zero_u32(unsigned* p, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0u;
+__global__ void k_fill_u32(unsigned* __restrict__ p, int64_t n, unsigned v) {
+  const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i4 + 3 < n) {
+    *reinterpret_cast<uint4*>(p + i4) = make_uint4(v, v, v, v);
+  } else {
+    for (int64_t i = i4; i < n; ++i) p[i] = v;
+  }
 }
 
 }  // namespace
 
-hipError_t launch_zero_u32(unsigned* p, int64_t n, hipStream_t st) {
+hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned v, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   const int threads = 256;
-  hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((n + threads - 1) / threads)), dim3(threads), 0,
-                     st, p, n);
+  const int64_t quads = (n + 3) / 4;
+  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads),
+                     0, st, p, n, v);
   return hipGetLastError();
 }
 

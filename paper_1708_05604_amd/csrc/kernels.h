@@ -120,9 +120,11 @@ hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_
 
 // ---------------------------------------------------------------- persistent recurrence
 // All T steps of one layer (both directions) in one cooperative launch.
-// Tables bs/off are the device batch tables; `barrier` is a zeroed counter
-// owned by this launch.  *fits reports whether the grid can be resident at
-// once; when it cannot, nothing is launched.
+// Tables bs/off are the device batch tables.  The buffer the steps exchange
+// (hout forward; da for the LSTM / dah for the GRU backward) must hold the
+// sentinel 0xFFFFFFFF in every element when the launch starts.  *fits
+// reports whether the grid can be resident at once (and the shape is
+// supported); when it cannot, nothing is launched.
 struct PersistFwdArgs {
   const float* gx[2];
   const float* whh[2];
@@ -132,7 +134,6 @@ struct PersistFwdArgs {
   float* hout;  // layer output [N x ldh]; direction d at column d*H
   const int32_t* bs;
   const int32_t* off;
-  unsigned* barrier;
   int32_t H, ldh, T;
   int32_t slices, rgroups;  // set by the launcher
 };
@@ -147,7 +148,6 @@ struct PersistBwdArgs {
   float* dah[2];
   const int32_t* bs;
   const int32_t* off;
-  unsigned* barrier;
   int32_t H, ldh, ldd, T;
   int32_t slices, rgroups;
 };
@@ -156,12 +156,11 @@ hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, i
                                  hipStream_t stream, bool* fits);
 hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
                                  hipStream_t stream, bool* fits);
-int persistent_fwd_blocks(int H, int B, int dirs);
-int persistent_bwd_blocks(int H, int B, int dirs);
-// Number of grid-barrier waits that gave up (should stay 0).
-hipError_t read_barrier_timeouts(unsigned* count);
+// Number of waits for published values that gave up (should stay 0).
+hipError_t read_wait_timeouts(unsigned* count);
+constexpr unsigned kPublishSentinel = 0xFFFFFFFFu;
 
-// Fills n 32-bit words with zero (a kernel, so it may sit in a captured graph).
-hipError_t launch_zero_u32(unsigned* p, int64_t n, hipStream_t stream);
+// Fills n 32-bit words with `value` (a kernel, so it may sit in a captured graph).
+hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned value, hipStream_t stream);
 
 }  // namespace rnnbkt

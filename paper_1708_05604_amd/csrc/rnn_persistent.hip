@@ -2,20 +2,26 @@
 // launch, forward and backward through time.
 //
 // A launch keeps every workgroup resident (cooperative launch) and walks
-// the T steps of the batch itself; between steps the workgroups meet at a
-// grid barrier (a monotonic arrival counter per launch: release on arrival,
-// acquire while waiting).  Each workgroup owns a fixed block of 16 batch
-// rows and a fixed slice of hidden units, so
+// the T steps of the batch itself.  Each workgroup owns a fixed block of 16
+// batch rows and a fixed slice of hidden units, so
 //   - its slice of W_hh stays in LDS for the whole launch (read from HBM
 //     once instead of once per step),
 //   - the recurrent state of its (row, unit) pairs (c for the LSTM, h for
 //     the GRU update, the dc / dh carries backward) stays in registers,
-//   - per-step operands that do not depend on the barrier (the input
-//     projection row, the saved gate activations) are fetched before the
-//     barrier wait, so only the exchange of h (forward) or dA (backward)
-//     between workgroups sits on the critical path.
-// Rows that have already ended at a step do no work but still meet the
-// barrier, so every workgroup arrives exactly T times.
+//   - per-step operands that do not depend on other workgroups (the input
+//     projection row, the saved gate activations) are fetched early.
+//
+// Exchange between workgroups without a grid barrier: the buffer a step
+// publishes (h forward, the recurrent gate gradient backward) is filled
+// with a sentinel bit pattern before the launch; every element of it is
+// written exactly once during the launch with a relaxed device-scope atomic
+// store (a value equal to the sentinel is replaced by the canonical NaN), and
+// a reader polls its elements with relaxed device-scope atomic loads until
+// none holds the sentinel.  Single-location coherence of atomics is all this
+// needs: no fence, no cache write-back or invalidation, and a workgroup
+// waits only for the rows it reads (sequences are independent).  Polls are
+// bounded; after a timeout the wait gives up, counts it (reported by
+// rnnbkt_sync_check) and later waits return at once, so a launch always ends.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -25,7 +31,7 @@
 
 namespace rnnbkt {
 
-__device__ unsigned g_barrier_timeouts = 0;
+__device__ unsigned g_wait_timeouts = 0;
 
 namespace {
 
@@ -34,44 +40,69 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
 __device__ inline float sigm(float x) { return 1.f / (1.f + __expf(-x)); }
 
-__device__ inline bf8 to_bf8(f4 lo, f4 hi) {
-  bf8 r;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    r[e] = (__bf16)lo[e];
-    r[e + 4] = (__bf16)hi[e];
-  }
-  return r;
+
+constexpr unsigned kSentinel = 0xFFFFFFFFu;
+constexpr unsigned kCanonicalNan = 0x7FC00000u;
+
+__device__ inline void publish(float* p, float v) {
+  unsigned u = __float_as_uint(v);
+  if (u == kSentinel) u = kCanonicalNan;
+  __hip_atomic_store(reinterpret_cast<unsigned*>(p), u, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Every workgroup of the grid arrives once per call; returns when all
-// `target` arrivals (cumulative over the launch) have happened.  The wait
-// is bounded: after ~2^20 polls (about a second) the workgroup gives up and
-// counts a timeout; once any timeout has been counted, later waits return
-// at once.  The launch therefore always ends, and rnnbkt_sync_check reports
-// the timeout as an error.
-__device__ inline void grid_barrier(unsigned* counter, unsigned target) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    if (__hip_atomic_load(&g_barrier_timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
-      unsigned spins = 0;
-      while (__hip_atomic_load(counter, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
-        __builtin_amdgcn_s_sleep(1);
-        if (++spins == (1u << 20)) {
-          __hip_atomic_fetch_add(&g_barrier_timeouts, 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
-          break;
-        }
-      }
+__device__ inline unsigned peek(const float* p) {
+  return __hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A lane's share of the reduction operand of one step: for its row `arow`
+// (nullptr = zero state) the chunks c = first, first + stride, ... below
+// nchunks, each contributing CPL consecutive floats at c*CH + koff.  All
+// loads are issued first, then the lane re-polls only the elements still
+// holding the sentinel.  Returns raw bits in u[i*CPL + e].  Wave-uniform.
+template <int CPL, int MAXC>
+__device__ inline void fetch_published(const float* arow, int first, int stride, int nchunks,
+                                       int CH, int koff, unsigned (&u)[CPL * MAXC]) {
+  bool ready = true;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = first + i * stride;
+#pragma unroll
+    for (int e = 0; e < CPL; ++e) {
+      u[i * CPL + e] = (arow && c < nchunks) ? peek(arow + c * CH + koff + e) : 0u;
+      ready &= u[i * CPL + e] != kSentinel;
     }
   }
-  __syncthreads();
+  if (__all(ready)) return;
+  if (__hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+    return;
+  unsigned spins = 0;
+  for (;;) {
+    __builtin_amdgcn_s_sleep(1);
+    ready = true;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int c = first + i * stride;
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) {
+        if (u[i * CPL + e] == kSentinel) u[i * CPL + e] = peek(arow + c * CH + koff + e);
+        ready &= u[i * CPL + e] != kSentinel;
+      }
+    }
+    if (__all(ready)) return;
+    if (++spins == (1u << 20)) {
+      if ((threadIdx.x & 63) == 0)
+        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+  }
 }
 
-constexpr int kWaves = 4;
 constexpr int kFwdUnits = 4;   // hidden units per forward workgroup (x G gates <= 16 columns)
 constexpr int kBwdUnits = 16;  // hidden units per backward workgroup
+constexpr int kMaxPerLane = 32;  // reduction-operand floats a lane holds per step
 
 template <bool BF16>
 struct LdsT;
@@ -79,14 +110,47 @@ template <>
 struct LdsT<false> {
   using T = float;
   static constexpr int CH = 16;  // k per MFMA group: 4 lane groups x 4
+  static constexpr int CPL = 4;
   static constexpr int PAD = 4;
 };
 template <>
 struct LdsT<true> {
   using T = __bf16;
   static constexpr int CH = 32;  // 4 lane groups x 8
+  static constexpr int CPL = 8;
   static constexpr int PAD = 8;
 };
+
+// acc += A(16 x K) . W(K x 16) over the chunks held in u (see
+// fetch_published), W rows from LDS row `wrow` (K contiguous).
+template <bool BF16, int MAXC>
+__device__ inline f4 mma_chunks(const unsigned (&u)[LdsT<BF16>::CPL * MAXC],
+                                const typename LdsT<BF16>::T* wrow, int first, int stride,
+                                int nchunks, int koff) {
+  constexpr int CH = LdsT<BF16>::CH;
+  constexpr int CPL = LdsT<BF16>::CPL;
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = first + i * stride;
+    if (c >= nchunks) break;
+    const int kk = c * CH + koff;
+    if constexpr (BF16) {
+      bf8 av;
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) av[e] = (__bf16)__uint_as_float(u[i * CPL + e]);
+      const bf8 w = *reinterpret_cast<const bf8*>(wrow + kk);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, w, acc, 0, 0, 0);
+    } else {
+      const f4 w = *reinterpret_cast<const f4*>(wrow + kk);
+#pragma unroll
+      for (int e = 0; e < CPL; ++e)
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(u[i * CPL + e]), w[e], acc,
+                                                   0, 0, 0);
+    }
+  }
+  return acc;
+}
 
 // Step indices of launch-relative step k for direction d.
 struct StepIdx {
@@ -108,10 +172,12 @@ __device__ inline StepIdx fwd_step(const int32_t* bs, const int32_t* off, int T,
   return s;
 }
 
-template <int G, bool BF16>
-__global__ __launch_bounds__(256) void k_fwd_persistent(PersistFwdArgs a) {
+template <int G, bool BF16, int NW>
+__global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   using T = typename LdsT<BF16>::T;
   constexpr int CH = LdsT<BF16>::CH;
+  constexpr int CPL = LdsT<BF16>::CPL;
+  constexpr int MAXC = kMaxPerLane / CPL;
   constexpr int NC = 16;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int H = a.H;
@@ -151,14 +217,14 @@ __global__ __launch_bounds__(256) void k_fwd_persistent(PersistFwdArgs a) {
   float* stash = a.stash[d];
   float* cst = a.cst[d];
   float* hout = a.hout + d * H;
-  const unsigned nwg = gridDim.x;
+  const int nchunks = H / CH;
   __syncthreads();
 
   StepIdx s = fwd_step(a.bs, a.off, a.T, d, 0);
   for (int k = 0; k < a.T; ++k) {
     const bool active = r0 < s.rows;
-    // Operands that do not depend on other workgroups: the input projection
-    // of this step's rows (wave 0, epilogue lanes).
+    // The input projection of this step's rows does not depend on other
+    // workgroups: fetch it first (wave 0, epilogue lanes).
     float gxv[G];
     const bool erow_on = active && wave == 0 && erow < s.rows;
     if (erow_on) {
@@ -167,44 +233,23 @@ __global__ __launch_bounds__(256) void k_fwd_persistent(PersistFwdArgs a) {
       for (int g = 0; g < G; ++g) gxv[g] = gr[g * H + ej];
     }
     if (active) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
       const int r = r0 + lr;
-      const float* arow =
-          r < s.prev_rows ? hout + (int64_t)(s.prev0 + r) * a.ldh : nullptr;
-      const T* wrow = Ws + lr * LDW;
-      const int nchunks = H / CH;
-      for (int c = wave; c < nchunks; c += kWaves) {
-        if constexpr (BF16) {
-          const int kk = c * CH + lq * 8;
-          f4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0;
-          if (arow) {
-            a0 = *reinterpret_cast<const f4*>(arow + kk);
-            a1 = *reinterpret_cast<const f4*>(arow + kk + 4);
-          }
-          const bf8 w = *reinterpret_cast<const bf8*>(wrow + kk);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(to_bf8(a0, a1), w, acc, 0, 0, 0);
-        } else {
-          const int kk = c * CH + lq * 4;
-          f4 av = {0.f, 0.f, 0.f, 0.f};
-          if (arow) av = *reinterpret_cast<const f4*>(arow + kk);
-          const f4 w = *reinterpret_cast<const f4*>(wrow + kk);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], w[e], acc, 0, 0, 0);
-        }
-      }
+      const float* arow = r < s.prev_rows ? hout + (int64_t)(s.prev0 + r) * a.ldh : nullptr;
+      unsigned u[CPL * MAXC];
+      fetch_published<CPL, MAXC>(arow, wave, NW, nchunks, CH, lq * CPL, u);
+      const f4 acc = mma_chunks<BF16, MAXC>(u, Ws + lr * LDW, wave, NW, nchunks, lq * CPL);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
     __syncthreads();
     if (erow_on) {
-      const int rr = lane >> 2, u = lane & 3;
+      const int rr = lane >> 2, uu = lane & 3;
       float sg[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float v = 0.f;
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) v += red[w * 256 + rr * 16 + g * 4 + u];
+        for (int w = 0; w < NW; ++w) v += red[w * 256 + rr * 16 + g * 4 + uu];
         sg[g] = v;
       }
       const bool has_prev = erow < s.prev_rows;
@@ -237,12 +282,11 @@ __global__ __launch_bounds__(256) void k_fwd_persistent(PersistFwdArgs a) {
         st[2 * H + ej] = n;
         st[3 * H + ej] = ahn;
       }
-      hout[f * a.ldh + ej] = h_state;
+      publish(hout + f * a.ldh + ej, h_state);
     }
-    // Next step's indices (constant tables) before the barrier wait.
     StepIdx nxt = s;
     if (k + 1 < a.T) nxt = fwd_step(a.bs, a.off, a.T, d, k + 1);
-    grid_barrier(a.barrier, nwg * (unsigned)(k + 1));
+    __syncthreads();  // red is rewritten by the next step
     s = nxt;
   }
 }
@@ -271,10 +315,12 @@ __device__ inline BwdIdx bwd_step(const int32_t* bs, const int32_t* off, int T, 
   return s;
 }
 
-template <int G, bool BF16>
-__global__ __launch_bounds__(256) void k_bwd_persistent(PersistBwdArgs a) {
+template <int G, bool BF16, int NW>
+__global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
   using T = typename LdsT<BF16>::T;
   constexpr int CH = LdsT<BF16>::CH;
+  constexpr int CPL = LdsT<BF16>::CPL;
+  constexpr int MAXC = kMaxPerLane / CPL;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int H = a.H;
   const int GH = G * H;
@@ -297,8 +343,9 @@ __global__ __launch_bounds__(256) void k_bwd_persistent(PersistBwdArgs a) {
     const int k = i / kBwdUnits, u = i % kBwdUnits;
     Ws[u * LDW + k] = (T)whh[(int64_t)k * H + j0 + u];
   }
-  // Epilogue: thread -> row r0 + (tid >> 4), unit j0 + (tid & 15).
-  const int erow = r0 + (threadIdx.x >> 4);
+  // Epilogue: threads 0..255 -> row r0 + (tid >> 4), unit j0 + (tid & 15).
+  const bool epi = threadIdx.x < 256;
+  const int erow = r0 + ((threadIdx.x & 255) >> 4);
   const int ej = j0 + (threadIdx.x & 15);
   float carry = 0.f;
   const float* stash = a.stash[d];
@@ -308,14 +355,14 @@ __global__ __launch_bounds__(256) void k_bwd_persistent(PersistBwdArgs a) {
   float* da = a.da[d];
   float* dah = a.dah[d];
   const float* da_next = G == 3 ? dah : da;
-  const unsigned nwg = gridDim.x;
+  const int nchunks = GH / CH;
   __syncthreads();
 
   BwdIdx s = bwd_step(a.bs, a.off, a.T, d, 0);
   for (int k = 0; k < a.T; ++k) {
     const bool active = r0 < s.rows;
-    const bool erow_on = active && erow < s.rows;
-    // Barrier-independent operands of this step.
+    const bool erow_on = epi && active && erow < s.rows;
+    // Operands that do not depend on other workgroups.
     float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cp = 0.f, hp = 0.f;
     int64_t f = 0;
     if (erow_on) {
@@ -333,53 +380,33 @@ __global__ __launch_bounds__(256) void k_bwd_persistent(PersistBwdArgs a) {
         if (erow < s.prev_rows) hp = hout[(int64_t)(s.prev0 + erow) * a.ldh + ej];
       }
     }
-    if (active && r0 < s.next_rows) {
+    if (active) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
-      const int r = r0 + lr;
-      const float* arow = r < s.next_rows ? da_next + (int64_t)(s.next0 + r) * GH : nullptr;
-      const T* wrow = Ws + lr * LDW;
-      const int nchunks = GH / CH;
-      for (int c = wave; c < nchunks; c += kWaves) {
-        if constexpr (BF16) {
-          const int kk = c * CH + lq * 8;
-          f4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = a0;
-          if (arow) {
-            a0 = *reinterpret_cast<const f4*>(arow + kk);
-            a1 = *reinterpret_cast<const f4*>(arow + kk + 4);
-          }
-          const bf8 w = *reinterpret_cast<const bf8*>(wrow + kk);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(to_bf8(a0, a1), w, acc, 0, 0, 0);
-        } else {
-          const int kk = c * CH + lq * 4;
-          f4 av = {0.f, 0.f, 0.f, 0.f};
-          if (arow) av = *reinterpret_cast<const f4*>(arow + kk);
-          const f4 w = *reinterpret_cast<const f4*>(wrow + kk);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], w[e], acc, 0, 0, 0);
-        }
+      if (r0 < s.next_rows) {
+        const int r = r0 + lr;
+        const float* arow = r < s.next_rows ? da_next + (int64_t)(s.next0 + r) * GH : nullptr;
+        unsigned u[CPL * MAXC];
+        fetch_published<CPL, MAXC>(arow, wave, NW, nchunks, CH, lq * CPL, u);
+        acc = mma_chunks<BF16, MAXC>(u, Ws + lr * LDW, wave, NW, nchunks, lq * CPL);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
-    } else if (active) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = 0.f;
     }
     __syncthreads();
     if (erow_on) {
       const bool has_next = erow < s.next_rows;
       float dh_rec = 0.f;
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) dh_rec += red[w * 256 + threadIdx.x];
+      for (int w = 0; w < NW; ++w) dh_rec += red[w * 256 + threadIdx.x];
       if constexpr (G == 4) {
         const float dh = dhv + (has_next ? dh_rec : 0.f);
         const float tc = tanhf(cc);
         const float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
         float* dar = da + f * GH;
-        dar[ej] = dc * st2 * st0 * (1.f - st0);
-        dar[H + ej] = dc * cp * st1 * (1.f - st1);
-        dar[2 * H + ej] = dc * st0 * (1.f - st2 * st2);
-        dar[3 * H + ej] = dh * tc * st3 * (1.f - st3);
+        publish(dar + ej, dc * st2 * st0 * (1.f - st0));
+        publish(dar + H + ej, dc * cp * st1 * (1.f - st1));
+        publish(dar + 2 * H + ej, dc * st0 * (1.f - st2 * st2));
+        publish(dar + 3 * H + ej, dh * tc * st3 * (1.f - st3));
         carry = dc * st1;
       } else {
         const float dh = dhv + (has_next ? dh_rec + carry : 0.f);
@@ -394,15 +421,15 @@ __global__ __launch_bounds__(256) void k_bwd_persistent(PersistBwdArgs a) {
         dx[ej] = dar_;
         dx[H + ej] = daz;
         dx[2 * H + ej] = dan;
-        dhh[ej] = dar_;
-        dhh[H + ej] = daz;
-        dhh[2 * H + ej] = dan * r;
+        publish(dhh + ej, dar_);
+        publish(dhh + H + ej, daz);
+        publish(dhh + 2 * H + ej, dan * r);
         carry = dh * z;
       }
     }
     BwdIdx nxt = s;
     if (k + 1 < a.T) nxt = bwd_step(a.bs, a.off, a.T, d, k + 1);
-    grid_barrier(a.barrier, nwg * (unsigned)(k + 1));
+    __syncthreads();  // red is rewritten by the next step
     s = nxt;
   }
 }
@@ -420,92 +447,92 @@ hipError_t allow_lds(const void* kernel, size_t shmem) {
   return e;
 }
 
-template <typename K>
-hipError_t coop_launch(K kernel, int blocks, size_t shmem, void* args, hipStream_t st) {
-  void* argv[] = {args};
-  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks),
-                                    dim3(256), argv, shmem, st);
-}
-
-size_t fwd_shmem(int H, bool bf16) {
-  const size_t w = 16 * (size_t)(H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
-  return (w + 15) / 16 * 16 + sizeof(float) * kWaves * 256;
-}
-
-size_t bwd_shmem(int GH, bool bf16) {
-  const size_t w = kBwdUnits * (size_t)(GH + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
-  return (w + 15) / 16 * 16 + sizeof(float) * kWaves * 256;
-}
-
-template <typename K>
-int max_coresident(K kernel, size_t shmem) {
+// Co-resident workgroups a launch of `kernel` can have (0 on error).
+int max_coresident(const void* kernel, int threads, size_t shmem) {
   int dev = 0, cus = 0, per_cu = 0;
-  if (allow_lds(reinterpret_cast<const void*>(kernel), shmem) != hipSuccess) return 0;
+  if (allow_lds(kernel, shmem) != hipSuccess) return 0;
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kernel),
-                                                   256, shmem) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, shmem) != hipSuccess)
     return 0;
   return cus * per_cu;
 }
 
-}  // namespace
+hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem, void* args,
+                       hipStream_t st, bool* fits) {
+  if (blocks > max_coresident(kernel, threads, shmem)) {
+    *fits = false;
+    return hipSuccess;
+  }
+  *fits = true;
+  void* argv[] = {args};
+  return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
+}
 
-int persistent_fwd_blocks(int H, int B, int dirs) { return dirs * (H / kFwdUnits) * ((B + 15) / 16); }
-int persistent_bwd_blocks(int H, int B, int dirs) { return dirs * (H / kBwdUnits) * ((B + 15) / 16); }
+// Waves per workgroup so that a lane holds at most kMaxPerLane floats of
+// a K-long reduction operand (0 = too long for this kernel).
+int waves_for(int K) {
+  for (int nw : {4, 8, 16})
+    if (K <= 4 * kMaxPerLane * nw) return nw;
+  return 0;
+}
+
+template <int G, bool BF16>
+const void* fwd_kernel(int nw) {
+  switch (nw) {
+    case 4: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4>);
+    case 8: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 8>);
+    case 16: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 16>);
+  }
+  return nullptr;
+}
+
+template <int G, bool BF16>
+const void* bwd_kernel(int nw) {
+  switch (nw) {
+    case 4: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, 4>);
+    case 8: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, 8>);
+    case 16: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, 16>);
+  }
+  return nullptr;
+}
+
+}  // namespace
 
 hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, int dirs,
                                  hipStream_t st, bool* fits) {
+  *fits = false;
+  const int nw = waves_for(a.H);
+  if (nw == 0 || a.H % kFwdUnits != 0) return hipSuccess;
   a.slices = a.H / kFwdUnits;
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
-  const size_t sh = fwd_shmem(a.H, bf16);
-#define RNNBKT_FWD(G_, BF_)                                                           \
-  {                                                                                   \
-    auto kern = k_fwd_persistent<G_, BF_>;                                            \
-    if (blocks > max_coresident(kern, sh)) {                                          \
-      *fits = false;                                                                  \
-      return hipSuccess;                                                              \
-    }                                                                                 \
-    *fits = true;                                                                     \
-    return coop_launch(kern, blocks, sh, &a, st);                                     \
-  }
-  if (cell == RNNBKT_CELL_LSTM) {
-    if (bf16) RNNBKT_FWD(4, true) else RNNBKT_FWD(4, false)
-  } else {
-    if (bf16) RNNBKT_FWD(3, true) else RNNBKT_FWD(3, false)
-  }
-#undef RNNBKT_FWD
+  const size_t w = 16 * (size_t)(a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
+  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256;
+  const void* k = cell == RNNBKT_CELL_LSTM ? (bf16 ? fwd_kernel<4, true>(nw) : fwd_kernel<4, false>(nw))
+                                           : (bf16 ? fwd_kernel<3, true>(nw) : fwd_kernel<3, false>(nw));
+  return coop_launch(k, blocks, 64 * nw, sh, &a, st, fits);
 }
 
 hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
                                  hipStream_t st, bool* fits) {
+  *fits = false;
+  const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
+  const int nw = waves_for(G * a.H);
+  if (nw == 0 || a.H % kBwdUnits != 0) return hipSuccess;
   a.slices = a.H / kBwdUnits;
   a.rgroups = (B + 15) / 16;
-  const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
   const int blocks = dirs * a.slices * a.rgroups;
-  const size_t sh = bwd_shmem(G * a.H, bf16);
-#define RNNBKT_BWD(G_, BF_)                                                           \
-  {                                                                                   \
-    auto kern = k_bwd_persistent<G_, BF_>;                                            \
-    if (blocks > max_coresident(kern, sh)) {                                          \
-      *fits = false;                                                                  \
-      return hipSuccess;                                                              \
-    }                                                                                 \
-    *fits = true;                                                                     \
-    return coop_launch(kern, blocks, sh, &a, st);                                     \
-  }
-  if (cell == RNNBKT_CELL_LSTM) {
-    if (bf16) RNNBKT_BWD(4, true) else RNNBKT_BWD(4, false)
-  } else {
-    if (bf16) RNNBKT_BWD(3, true) else RNNBKT_BWD(3, false)
-  }
-#undef RNNBKT_BWD
+  const size_t w = kBwdUnits * (size_t)(G * a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
+  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256;
+  const void* k = cell == RNNBKT_CELL_LSTM ? (bf16 ? bwd_kernel<4, true>(nw) : bwd_kernel<4, false>(nw))
+                                           : (bf16 ? bwd_kernel<3, true>(nw) : bwd_kernel<3, false>(nw));
+  return coop_launch(k, blocks, 64 * nw, sh, &a, st, fits);
 }
 
-hipError_t read_barrier_timeouts(unsigned* count) {
-  return hipMemcpyFromSymbol(count, HIP_SYMBOL(g_barrier_timeouts), sizeof(unsigned), 0,
+hipError_t read_wait_timeouts(unsigned* count) {
+  return hipMemcpyFromSymbol(count, HIP_SYMBOL(g_wait_timeouts), sizeof(unsigned), 0,
                              hipMemcpyDeviceToHost);
 }
 
