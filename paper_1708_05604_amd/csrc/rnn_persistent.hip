@@ -57,46 +57,35 @@ __device__ inline unsigned peek(const float* p) {
 }
 
 // A lane's share of the reduction operand of one step: for its row `arow`
-// (nullptr = zero state) the chunks c = first, first + stride, ... below
-// nchunks, each contributing CPL consecutive floats at c*CH + koff.  All
-// loads are issued first, then the lane re-polls only the elements still
-// holding the sentinel.  Returns raw bits in u[i*CPL + e].  Wave-uniform.
+// (nullptr = zero state) the chunks c = first + i*stride (i < MAXC, c below
+// nchunks), each contributing CPL consecutive floats at c*CH + koff.  Every
+// round issues all loads back to back and then checks them; the wave retries
+// until no element holds the sentinel.  Raw bits in u[i*CPL + e].
 template <int CPL, int MAXC>
 __device__ inline void fetch_published(const float* arow, int first, int stride, int nchunks,
                                        int CH, int koff, unsigned (&u)[CPL * MAXC]) {
-  bool ready = true;
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = first + i * stride;
-#pragma unroll
-    for (int e = 0; e < CPL; ++e) {
-      u[i * CPL + e] = (arow && c < nchunks) ? peek(arow + c * CH + koff + e) : 0u;
-      ready &= u[i * CPL + e] != kSentinel;
-    }
-  }
-  if (__all(ready)) return;
-  if (__hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
-    return;
   unsigned spins = 0;
   for (;;) {
-    __builtin_amdgcn_s_sleep(1);
-    ready = true;
+    bool ready = true;
 #pragma unroll
     for (int i = 0; i < MAXC; ++i) {
       const int c = first + i * stride;
+      const bool on = arow != nullptr && c < nchunks;
 #pragma unroll
-      for (int e = 0; e < CPL; ++e) {
-        if (u[i * CPL + e] == kSentinel) u[i * CPL + e] = peek(arow + c * CH + koff + e);
-        ready &= u[i * CPL + e] != kSentinel;
-      }
+      for (int e = 0; e < CPL; ++e) u[i * CPL + e] = on ? peek(arow + c * CH + koff + e) : 0u;
     }
+#pragma unroll
+    for (int j = 0; j < CPL * MAXC; ++j) ready &= u[j] != kSentinel;
     if (__all(ready)) return;
+    if (spins == 0 && __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) != 0u)
+      return;
     if (++spins == (1u << 20)) {
       if ((threadIdx.x & 63) == 0)
-        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return;
     }
+    __builtin_amdgcn_s_sleep(1);
   }
 }
 
@@ -172,12 +161,11 @@ __device__ inline StepIdx fwd_step(const int32_t* bs, const int32_t* off, int T,
   return s;
 }
 
-template <int G, bool BF16, int NW>
+template <int G, bool BF16, int NW, int MAXC>
 __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   using T = typename LdsT<BF16>::T;
   constexpr int CH = LdsT<BF16>::CH;
   constexpr int CPL = LdsT<BF16>::CPL;
-  constexpr int MAXC = kMaxPerLane / CPL;
   constexpr int NC = 16;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int H = a.H;
@@ -220,18 +208,21 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   const int nchunks = H / CH;
   __syncthreads();
 
-  StepIdx s = fwd_step(a.bs, a.off, a.T, d, 0);
-  for (int k = 0; k < a.T; ++k) {
-    const bool active = r0 < s.rows;
-    // The input projection of this step's rows does not depend on other
-    // workgroups: fetch it first (wave 0, epilogue lanes).
-    float gxv[G];
-    const bool erow_on = active && wave == 0 && erow < s.rows;
-    if (erow_on) {
-      const float* gr = gxd + (int64_t)(s.row0 + erow) * GH;
+  // The input projection of a step's rows does not depend on other
+  // workgroups: wave 0 fetches it one step ahead.
+  float gxv[G];
+  auto load_gx = [&](const StepIdx& q) {
+    if (wave == 0 && r0 < q.rows && erow < q.rows) {
+      const float* gr = gxd + (int64_t)(q.row0 + erow) * GH;
 #pragma unroll
       for (int g = 0; g < G; ++g) gxv[g] = gr[g * H + ej];
     }
+  };
+  StepIdx s = fwd_step(a.bs, a.off, a.T, d, 0);
+  load_gx(s);
+  for (int k = 0; k < a.T; ++k) {
+    const bool active = r0 < s.rows;
+    const bool erow_on = active && wave == 0 && erow < s.rows;
     if (active) {
       const int r = r0 + lr;
       const float* arow = r < s.prev_rows ? hout + (int64_t)(s.prev0 + r) * a.ldh : nullptr;
@@ -284,10 +275,11 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
       }
       publish(hout + f * a.ldh + ej, h_state);
     }
-    StepIdx nxt = s;
-    if (k + 1 < a.T) nxt = fwd_step(a.bs, a.off, a.T, d, k + 1);
+    if (k + 1 < a.T) {
+      s = fwd_step(a.bs, a.off, a.T, d, k + 1);
+      load_gx(s);
+    }
     __syncthreads();  // red is rewritten by the next step
-    s = nxt;
   }
 }
 
@@ -315,12 +307,11 @@ __device__ inline BwdIdx bwd_step(const int32_t* bs, const int32_t* off, int T, 
   return s;
 }
 
-template <int G, bool BF16, int NW>
+template <int G, bool BF16, int NW, int MAXC>
 __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
   using T = typename LdsT<BF16>::T;
   constexpr int CH = LdsT<BF16>::CH;
   constexpr int CPL = LdsT<BF16>::CPL;
-  constexpr int MAXC = kMaxPerLane / CPL;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int H = a.H;
   const int GH = G * H;
@@ -427,10 +418,8 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
         carry = dh * z;
       }
     }
-    BwdIdx nxt = s;
-    if (k + 1 < a.T) nxt = bwd_step(a.bs, a.off, a.T, d, k + 1);
+    if (k + 1 < a.T) s = bwd_step(a.bs, a.off, a.T, d, k + 1);
     __syncthreads();  // red is rewritten by the next step
-    s = nxt;
   }
 }
 
@@ -470,48 +459,65 @@ hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem
   return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
 }
 
-// Waves per workgroup so that a lane holds at most kMaxPerLane floats of
-// a K-long reduction operand (0 = too long for this kernel).
-int waves_for(int K) {
-  for (int nw : {4, 8, 16})
-    if (K <= 4 * kMaxPerLane * nw) return nw;
-  return 0;
+// Waves per workgroup and chunks per wave for a K-long reduction: the
+// fewest waves (4 or 16) for which a wave's share fits a lane's budget of
+// kMaxPerLane floats; MAXC is the chunks a wave handles rounded up to a
+// power of two.  Returns false if K is too long for these kernels.
+bool split_for(int K, bool bf16, int* nw, int* maxc) {
+  const int ch = bf16 ? 32 : 16, cpl = bf16 ? 8 : 4;
+  const int nchunks = K / ch;
+  for (int w : {4, 16}) {
+    const int per = (nchunks + w - 1) / w;
+    int m = 1;
+    while (m < per) m *= 2;
+    if (m * cpl <= kMaxPerLane) {
+      *nw = w;
+      *maxc = m;
+      return true;
+    }
+  }
+  return false;
 }
 
-template <int G, bool BF16>
-const void* fwd_kernel(int nw) {
-  switch (nw) {
-    case 4: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4>);
-    case 8: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 8>);
-    case 16: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 16>);
-  }
+#define RNNBKT_PICK(KERN, G_, BF_)                                                   \
+  switch (nw * 100 + maxc) {                                                         \
+    case 401: return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 1>);             \
+    case 402: return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 2>);             \
+    case 404: return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 4>);             \
+    case 1601: return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 1>);           \
+    case 1602: return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 2>);           \
+    case 1604: return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 4>);           \
+  }                                                                                  \
+  if constexpr (!BF_) {                                                              \
+    if (nw * 100 + maxc == 408) return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 8>);   \
+    if (nw * 100 + maxc == 1608) return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 8>); \
+  }                                                                                  \
   return nullptr;
-}
 
 template <int G, bool BF16>
-const void* bwd_kernel(int nw) {
-  switch (nw) {
-    case 4: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, 4>);
-    case 8: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, 8>);
-    case 16: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, 16>);
-  }
-  return nullptr;
-}
+const void* fwd_kernel(int nw, int maxc) { RNNBKT_PICK(k_fwd_persistent, G, BF16) }
+
+template <int G, bool BF16>
+const void* bwd_kernel(int nw, int maxc) { RNNBKT_PICK(k_bwd_persistent, G, BF16) }
+
+#undef RNNBKT_PICK
 
 }  // namespace
 
 hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, int dirs,
                                  hipStream_t st, bool* fits) {
   *fits = false;
-  const int nw = waves_for(a.H);
-  if (nw == 0 || a.H % kFwdUnits != 0) return hipSuccess;
+  int nw = 0, maxc = 0;
+  if (!split_for(a.H, bf16, &nw, &maxc) || a.H % kFwdUnits != 0) return hipSuccess;
   a.slices = a.H / kFwdUnits;
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
   const size_t w = 16 * (size_t)(a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
   const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256;
-  const void* k = cell == RNNBKT_CELL_LSTM ? (bf16 ? fwd_kernel<4, true>(nw) : fwd_kernel<4, false>(nw))
-                                           : (bf16 ? fwd_kernel<3, true>(nw) : fwd_kernel<3, false>(nw));
+  const void* k = cell == RNNBKT_CELL_LSTM
+                      ? (bf16 ? fwd_kernel<4, true>(nw, maxc) : fwd_kernel<4, false>(nw, maxc))
+                      : (bf16 ? fwd_kernel<3, true>(nw, maxc) : fwd_kernel<3, false>(nw, maxc));
+  if (!k) return hipSuccess;
   return coop_launch(k, blocks, 64 * nw, sh, &a, st, fits);
 }
 
@@ -519,15 +525,17 @@ hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, i
                                  hipStream_t st, bool* fits) {
   *fits = false;
   const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
-  const int nw = waves_for(G * a.H);
-  if (nw == 0 || a.H % kBwdUnits != 0) return hipSuccess;
+  int nw = 0, maxc = 0;
+  if (!split_for(G * a.H, bf16, &nw, &maxc) || a.H % kBwdUnits != 0) return hipSuccess;
   a.slices = a.H / kBwdUnits;
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
   const size_t w = kBwdUnits * (size_t)(G * a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
   const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256;
-  const void* k = cell == RNNBKT_CELL_LSTM ? (bf16 ? bwd_kernel<4, true>(nw) : bwd_kernel<4, false>(nw))
-                                           : (bf16 ? bwd_kernel<3, true>(nw) : bwd_kernel<3, false>(nw));
+  const void* k = cell == RNNBKT_CELL_LSTM
+                      ? (bf16 ? bwd_kernel<4, true>(nw, maxc) : bwd_kernel<4, false>(nw, maxc))
+                      : (bf16 ? bwd_kernel<3, true>(nw, maxc) : bwd_kernel<3, false>(nw, maxc));
+  if (!k) return hipSuccess;
   return coop_launch(k, blocks, 64 * nw, sh, &a, st, fits);
 }
 
