@@ -424,6 +424,8 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
       a.hout = hout;
       a.bs = d_bs;
       a.off = d_off;
+      const uint64_t pub = sizeof(float) * (uint64_t)N * s.dirs * s.H;
+      a.pub_bytes = pub < 0x7FFFFFF0u ? (uint32_t)pub : 0u;
       a.H = s.H;
       a.ldh = s.dirs * s.H;
       a.T = T;
@@ -554,6 +556,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       a.dh_in = dh_in;
       a.bs = d_bs;
       a.off = d_off;
+      const uint64_t pub = sizeof(float) * (uint64_t)N * GH;
+      a.pub_bytes = pub < 0x7FFFFFF0u ? (uint32_t)pub : 0u;
       a.H = s.H;
       a.ldh = s.dirs * s.H;
       a.ldd = s.Htop;

@@ -134,6 +134,7 @@ struct PersistFwdArgs {
   float* hout;  // layer output [N x ldh]; direction d at column d*H
   const int32_t* bs;
   const int32_t* off;
+  uint32_t pub_bytes;  // bytes of hout (the published array); must be < 2^31 - 16
   int32_t H, ldh, T;
   int32_t slices, rgroups;  // set by the launcher
 };
@@ -148,6 +149,7 @@ struct PersistBwdArgs {
   float* dah[2];
   const int32_t* bs;
   const int32_t* off;
+  uint32_t pub_bytes;  // bytes of each published da (LSTM) / dah (GRU); < 2^31 - 16
   int32_t H, ldh, ldd, T;
   int32_t slices, rgroups;
 };

@@ -51,29 +51,47 @@ __device__ inline void publish(float* p, float v) {
                      __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ inline unsigned peek(const float* p) {
-  return __hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-}
 
-// A lane's share of the reduction operand of one step: for its row `arow`
-// (nullptr = zero state) the chunks c = first + i*stride (i < MAXC, c below
-// nchunks), each contributing CPL consecutive floats at c*CH + koff.  Every
-// round issues all loads back to back and then checks them; the wave retries
-// until no element holds the sentinel.  Raw bits in u[i*CPL + e].
+typedef unsigned u4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource over a published array of `bytes` bytes.  Loads through it
+// use the device-scope cache policy (sc1), the policy of a relaxed
+// device-scope atomic load; every 32-bit element of a 128-bit load is read
+// atomically, which is all the sentinel protocol needs.  Offsets at or past
+// `bytes` read as zero.
+__device__ inline __amdgpu_buffer_rsrc_t published_rsrc(const float* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, (int)bytes, 0x00020000);
+}
+constexpr unsigned kNoRow = 0x7FFFFFF0u;  // an offset past every published array
+constexpr int kDeviceScope = 16;           // sc1
+
+// A lane's share of the reduction operand of one step: for its row at byte
+// offset `row_off` (kNoRow = zero state) the chunks c = first + i*stride
+// (i < MAXC, c below nchunks), each contributing CPL consecutive floats at
+// float offset c*CH + koff.  Every round issues all loads back to back and
+// then checks them; the wave retries until no element holds the sentinel.
+// Raw bits in u[i*CPL + e].
 template <int CPL, int MAXC>
-__device__ inline void fetch_published(const float* arow, int first, int stride, int nchunks,
-                                       int CH, int koff, unsigned (&u)[CPL * MAXC]) {
+__device__ inline void fetch_published(__amdgpu_buffer_rsrc_t rsrc, unsigned row_off, int first,
+                                       int stride, int nchunks, int CH, int koff,
+                                       unsigned (&u)[CPL * MAXC]) {
+  unsigned offs[MAXC];
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = first + i * stride;
+    offs[i] = (row_off != kNoRow && c < nchunks) ? row_off + 4u * (unsigned)(c * CH + koff) : kNoRow;
+  }
   unsigned spins = 0;
   for (;;) {
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+#pragma unroll
+      for (int v = 0; v < CPL / 4; ++v) {
+        const u4 x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, offs[i] + 16u * v, 0, kDeviceScope);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) u[i * CPL + 4 * v + e] = x[e];
+      }
     bool ready = true;
-#pragma unroll
-    for (int i = 0; i < MAXC; ++i) {
-      const int c = first + i * stride;
-      const bool on = arow != nullptr && c < nchunks;
-#pragma unroll
-      for (int e = 0; e < CPL; ++e) u[i * CPL + e] = on ? peek(arow + c * CH + koff + e) : 0u;
-    }
 #pragma unroll
     for (int j = 0; j < CPL * MAXC; ++j) ready &= u[j] != kSentinel;
     if (__all(ready)) return;
@@ -89,6 +107,7 @@ __device__ inline void fetch_published(const float* arow, int first, int stride,
   }
 }
 
+constexpr int kMaxSteps = 6144;  // batch tables kept in LDS: T_max above this is not handled here
 constexpr int kFwdUnits = 4;   // hidden units per forward workgroup (x G gates <= 16 columns)
 constexpr int kBwdUnits = 16;  // hidden units per backward workgroup
 constexpr int kMaxPerLane = 32;  // reduction-operand floats a lane holds per step
@@ -172,6 +191,12 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   const int LDW = H + LdsT<BF16>::PAD;
   T* Ws = reinterpret_cast<T*>(smem);
   float* red = reinterpret_cast<float*>(smem + ((NC * LDW * sizeof(T) + 15) / 16) * 16);
+  int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
+  int32_t* toff = tbs + a.T;                                  // offsets [T+1]
+  for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
+    if (i < a.T) tbs[i] = a.bs[i];
+    toff[i] = a.off[i];
+  }
 
   const int per_dir = a.slices * a.rgroups;
   const int d = blockIdx.x / per_dir;
@@ -206,28 +231,36 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   float* cst = a.cst[d];
   float* hout = a.hout + d * H;
   const int nchunks = H / CH;
+  const __amdgpu_buffer_rsrc_t hsrc = published_rsrc(a.hout, a.pub_bytes);
   __syncthreads();
 
   // The input projection of a step's rows does not depend on other
   // workgroups: wave 0 fetches it one step ahead.
+  // Loads are unconditional within wave 0 (rows past the active ones read
+  // frame 0 and are ignored) so no branch forces a wait on older loads.
   float gxv[G];
   auto load_gx = [&](const StepIdx& q) {
-    if (wave == 0 && r0 < q.rows && erow < q.rows) {
-      const float* gr = gxd + (int64_t)(q.row0 + erow) * GH;
+    if (wave == 0) {
+      const int64_t fr = erow < q.rows ? q.row0 + erow : 0;
+      const float* gr = gxd + fr * GH;
 #pragma unroll
       for (int g = 0; g < G; ++g) gxv[g] = gr[g * H + ej];
     }
   };
-  StepIdx s = fwd_step(a.bs, a.off, a.T, d, 0);
+  StepIdx s = fwd_step(tbs, toff, a.T, d, 0);
   load_gx(s);
   for (int k = 0; k < a.T; ++k) {
+    // Next step's table entries first, so no later wait has to cover them.
+    StepIdx nx = s;
+    if (k + 1 < a.T) nx = fwd_step(tbs, toff, a.T, d, k + 1);
     const bool active = r0 < s.rows;
     const bool erow_on = active && wave == 0 && erow < s.rows;
     if (active) {
       const int r = r0 + lr;
-      const float* arow = r < s.prev_rows ? hout + (int64_t)(s.prev0 + r) * a.ldh : nullptr;
+      const unsigned row_off =
+          r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + d * H) : kNoRow;
       unsigned u[CPL * MAXC];
-      fetch_published<CPL, MAXC>(arow, wave, NW, nchunks, CH, lq * CPL, u);
+      fetch_published<CPL, MAXC>(hsrc, row_off, wave, NW, nchunks, CH, lq * CPL, u);
       const f4 acc = mma_chunks<BF16, MAXC>(u, Ws + lr * LDW, wave, NW, nchunks, lq * CPL);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
@@ -275,10 +308,8 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
       }
       publish(hout + f * a.ldh + ej, h_state);
     }
-    if (k + 1 < a.T) {
-      s = fwd_step(a.bs, a.off, a.T, d, k + 1);
-      load_gx(s);
-    }
+    s = nx;
+    if (k + 1 < a.T) load_gx(s);
     __syncthreads();  // red is rewritten by the next step
   }
 }
@@ -318,6 +349,12 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
   const int LDW = GH + LdsT<BF16>::PAD;
   T* Ws = reinterpret_cast<T*>(smem);  // Ws[u][k] = W_hh[k][j0 + u]
   float* red = reinterpret_cast<float*>(smem + ((kBwdUnits * LDW * sizeof(T) + 15) / 16) * 16);
+  int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
+  int32_t* toff = tbs + a.T;                                  // offsets [T+1]
+  for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
+    if (i < a.T) tbs[i] = a.bs[i];
+    toff[i] = a.off[i];
+  }
 
   const int per_dir = a.slices * a.rgroups;
   const int d = blockIdx.x / per_dir;
@@ -347,17 +384,24 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
   float* dah = a.dah[d];
   const float* da_next = G == 3 ? dah : da;
   const int nchunks = GH / CH;
+  const __amdgpu_buffer_rsrc_t dsrc = published_rsrc(da_next, a.pub_bytes);
   __syncthreads();
 
-  BwdIdx s = bwd_step(a.bs, a.off, a.T, d, 0);
+  BwdIdx s = bwd_step(tbs, toff, a.T, d, 0);
   for (int k = 0; k < a.T; ++k) {
+    // Next step's table entries first, so no later wait has to cover them.
+    BwdIdx nx = s;
+    if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, d, k + 1);
     const bool active = r0 < s.rows;
     const bool erow_on = epi && active && erow < s.rows;
-    // Operands that do not depend on other workgroups.
-    float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cp = 0.f, hp = 0.f;
-    int64_t f = 0;
-    if (erow_on) {
-      f = s.row0 + erow;
+    // Operands that do not depend on other workgroups, loaded without
+    // branches inside the epilogue waves (inactive rows read frame 0 and are
+    // ignored) so no branch forces a wait on older loads.
+    float dhv, st0, st1, st2, st3, cc, cprev;
+    const int64_t f = erow < s.rows ? s.row0 + erow : 0;
+    const bool has_prev = erow < s.prev_rows;
+    if (epi) {
+      const int64_t fp = has_prev ? s.prev0 + erow : 0;
       dhv = dh_in[f * a.ldd + ej];
       const float* st = stash + f * 4 * H;
       st0 = st[ej];
@@ -366,18 +410,20 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
       st3 = st[3 * H + ej];
       if constexpr (G == 4) {
         cc = cst[f * H + ej];
-        if (erow < s.prev_rows) cp = cst[(int64_t)(s.prev0 + erow) * H + ej];
+        cprev = cst[fp * H + ej];
       } else {
-        if (erow < s.prev_rows) hp = hout[(int64_t)(s.prev0 + erow) * a.ldh + ej];
+        cc = 0.f;
+        cprev = hout[fp * a.ldh + ej];
       }
     }
     if (active) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       if (r0 < s.next_rows) {
         const int r = r0 + lr;
-        const float* arow = r < s.next_rows ? da_next + (int64_t)(s.next0 + r) * GH : nullptr;
+        const unsigned row_off =
+            r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
         unsigned u[CPL * MAXC];
-        fetch_published<CPL, MAXC>(arow, wave, NW, nchunks, CH, lq * CPL, u);
+        fetch_published<CPL, MAXC>(dsrc, row_off, wave, NW, nchunks, CH, lq * CPL, u);
         acc = mma_chunks<BF16, MAXC>(u, Ws + lr * LDW, wave, NW, nchunks, lq * CPL);
       }
 #pragma unroll
@@ -393,6 +439,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
         const float dh = dhv + (has_next ? dh_rec : 0.f);
         const float tc = tanhf(cc);
         const float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
+        const float cp = has_prev ? cprev : 0.f;
         float* dar = da + f * GH;
         publish(dar + ej, dc * st2 * st0 * (1.f - st0));
         publish(dar + H + ej, dc * cp * st1 * (1.f - st1));
@@ -402,6 +449,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
       } else {
         const float dh = dhv + (has_next ? dh_rec + carry : 0.f);
         const float r = st0, z = st1, n = st2, ahn = st3;
+        const float hp = has_prev ? cprev : 0.f;
         const float dn = dh * (1.f - z);
         const float dz = dh * (hp - n);
         const float dan = dn * (1.f - n * n);
@@ -418,7 +466,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
         carry = dh * z;
       }
     }
-    if (k + 1 < a.T) s = bwd_step(a.bs, a.off, a.T, d, k + 1);
+    s = nx;
     __syncthreads();  // red is rewritten by the next step
   }
 }
@@ -509,11 +557,13 @@ hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, i
   *fits = false;
   int nw = 0, maxc = 0;
   if (!split_for(a.H, bf16, &nw, &maxc) || a.H % kFwdUnits != 0) return hipSuccess;
+  if (a.pub_bytes == 0 || a.pub_bytes >= kNoRow) return hipSuccess;
   a.slices = a.H / kFwdUnits;
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
+  if (a.T > kMaxSteps) return hipSuccess;
   const size_t w = 16 * (size_t)(a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
-  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256;
+  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
   const void* k = cell == RNNBKT_CELL_LSTM
                       ? (bf16 ? fwd_kernel<4, true>(nw, maxc) : fwd_kernel<4, false>(nw, maxc))
                       : (bf16 ? fwd_kernel<3, true>(nw, maxc) : fwd_kernel<3, false>(nw, maxc));
@@ -527,11 +577,13 @@ hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, i
   const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
   int nw = 0, maxc = 0;
   if (!split_for(G * a.H, bf16, &nw, &maxc) || a.H % kBwdUnits != 0) return hipSuccess;
+  if (a.pub_bytes == 0 || a.pub_bytes >= kNoRow) return hipSuccess;
   a.slices = a.H / kBwdUnits;
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
+  if (a.T > kMaxSteps) return hipSuccess;
   const size_t w = kBwdUnits * (size_t)(G * a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
-  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256;
+  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
   const void* k = cell == RNNBKT_CELL_LSTM
                       ? (bf16 ? bwd_kernel<4, true>(nw, maxc) : bwd_kernel<4, false>(nw, maxc))
                       : (bf16 ? bwd_kernel<3, true>(nw, maxc) : bwd_kernel<3, false>(nw, maxc));
