@@ -164,6 +164,10 @@ def main(argv=None):
     ap.add_argument("--no-k1", action="store_true", help="skip the K=1 epoch")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--no-timer", action="store_true", help="skip the per-kernel pass")
+    ap.add_argument("--calibrate", type=int, default=0, metavar="MIB",
+                    help="first run rnnbkt_sgd_apply once over MIB MiB of parameters (reads "
+                         "2x, writes 1x that many bytes): a streaming kernel of known size "
+                         "for scaling hardware byte counters")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -181,6 +185,14 @@ def main(argv=None):
                             w.bidirectional, w.gemm_dtype)
     P = lib.param_count(desc)
     data = synth.make_workload(w, 0, param_count=P)
+
+    if args.calibrate:
+        nf = args.calibrate * (1 << 20) // 4
+        cp = torch.zeros(nf, dtype=torch.float32, device=dev)
+        cg = torch.ones(nf, dtype=torch.float32, device=dev)
+        lib.sgd_apply(cp, cg, 0.5)
+        torch.cuda.synchronize()
+        del cp, cg
 
     ep = Epoch(w, data, K, 0, torch, dev)
     ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev)
