@@ -24,6 +24,8 @@
 // rnnbkt_sync_check) and later waits return at once, so a launch always ends.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
+#include <cstring>
 #include <mutex>
 #include <vector>
 
@@ -496,6 +498,11 @@ int max_coresident(const void* kernel, int threads, size_t shmem) {
   return cus * per_cu;
 }
 
+// Launches a grid that must be resident all at once.  By default the
+// runtime's cooperative launch guarantees it; RNNBKT_LAUNCH=plain uses an
+// ordinary launch instead (for tools that cannot follow cooperative
+// launches), relying on the occupancy check alone -- if another stream
+// occupied the GPU, waits would time out and rnnbkt_sync_check reports it.
 hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem, void* args,
                        hipStream_t st, bool* fits) {
   if (blocks > max_coresident(kernel, threads, shmem)) {
@@ -504,6 +511,9 @@ hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem
   }
   *fits = true;
   void* argv[] = {args};
+  const char* mode = getenv("RNNBKT_LAUNCH");
+  if (mode && strcmp(mode, "plain") == 0)
+    return hipLaunchKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
   return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
 }
 
