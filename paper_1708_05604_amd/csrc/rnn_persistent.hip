@@ -4,8 +4,8 @@
 // A launch keeps every workgroup resident (cooperative launch) and walks
 // the T steps of the batch itself.  Each workgroup owns a fixed block of 16
 // batch rows and a fixed slice of hidden units, so
-//   - its slice of W_hh stays in LDS for the whole launch (read from HBM
-//     once instead of once per step),
+//   - its slice of W_hh stays in registers for the whole launch (each lane
+//     holds the MFMA operand fragments it feeds; read from HBM once),
 //   - the recurrent state of its (row, unit) pairs (c for the LSTM, h for
 //     the GRU update, the dc / dh carries backward) stays in registers,
 //   - per-step operands that do not depend on other workgroups (the input
@@ -114,52 +114,81 @@ constexpr int kFwdUnits = 4;   // hidden units per forward workgroup (x G gates 
 constexpr int kBwdUnits = 16;  // hidden units per backward workgroup
 constexpr int kMaxPerLane = 32;  // reduction-operand floats a lane holds per step
 
+// Reduction-dimension chunking of one MFMA group: fp32 16x16x4 takes 4
+// k per lane group (4 groups), bf16 16x16x32 takes 8.
 template <bool BF16>
-struct LdsT;
+struct Chunk;
 template <>
-struct LdsT<false> {
-  using T = float;
-  static constexpr int CH = 16;  // k per MFMA group: 4 lane groups x 4
+struct Chunk<false> {
+  static constexpr int CH = 16;
   static constexpr int CPL = 4;
-  static constexpr int PAD = 4;
 };
 template <>
-struct LdsT<true> {
-  using T = __bf16;
-  static constexpr int CH = 32;  // 4 lane groups x 8
+struct Chunk<true> {
+  static constexpr int CH = 32;
   static constexpr int CPL = 8;
-  static constexpr int PAD = 8;
 };
 
-// acc += A(16 x K) . W(K x 16) over the chunks held in u (see
-// fetch_published), W rows from LDS row `wrow` (K contiguous).
+// A lane's weight fragments for its chunks, kept in registers for the whole
+// launch: element (k, column) of the 16-column weight block for
+// k = c*CH + koff + e.  fp32: 4 floats per chunk; bf16: 8 values per chunk.
+template <bool BF16>
+struct WFrag;
+template <>
+struct WFrag<false> {
+  using T = f4;
+};
+template <>
+struct WFrag<true> {
+  using T = bf8;
+};
+
+// acc += A(16 x K) . W(K x 16) over the chunks held in u (see fetch_published)
+// with the lane's weight fragments w (one per chunk slot).
 template <bool BF16, int MAXC>
-__device__ inline f4 mma_chunks(const unsigned (&u)[LdsT<BF16>::CPL * MAXC],
-                                const typename LdsT<BF16>::T* wrow, int first, int stride,
-                                int nchunks, int koff) {
-  constexpr int CH = LdsT<BF16>::CH;
-  constexpr int CPL = LdsT<BF16>::CPL;
+__device__ inline f4 mma_chunks(const unsigned (&u)[Chunk<BF16>::CPL * MAXC],
+                                const typename WFrag<BF16>::T (&w)[MAXC], int first, int stride,
+                                int nchunks) {
+  constexpr int CPL = Chunk<BF16>::CPL;
   f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
     const int c = first + i * stride;
     if (c >= nchunks) break;
-    const int kk = c * CH + koff;
     if constexpr (BF16) {
       bf8 av;
 #pragma unroll
       for (int e = 0; e < CPL; ++e) av[e] = (__bf16)__uint_as_float(u[i * CPL + e]);
-      const bf8 w = *reinterpret_cast<const bf8*>(wrow + kk);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, w, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, w[i], acc, 0, 0, 0);
     } else {
-      const f4 w = *reinterpret_cast<const f4*>(wrow + kk);
 #pragma unroll
       for (int e = 0; e < CPL; ++e)
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(u[i * CPL + e]), w[e], acc,
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(u[i * CPL + e]), w[i][e], acc,
                                                    0, 0, 0);
     }
   }
   return acc;
+}
+
+// Loads the lane's weight fragments: wk(k) returns the weight for reduction
+// index k of this lane's column (0 for padding columns).
+template <bool BF16, int MAXC, typename F>
+__device__ inline void load_wfrags(typename WFrag<BF16>::T (&w)[MAXC], int first, int stride,
+                                   int nchunks, int koff, F wk) {
+  constexpr int CH = Chunk<BF16>::CH;
+  constexpr int CPL = Chunk<BF16>::CPL;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = first + i * stride;
+#pragma unroll
+    for (int e = 0; e < CPL; ++e) {
+      const float v = c < nchunks ? wk(c * CH + koff + e) : 0.f;
+      if constexpr (BF16)
+        w[i][e] = (__bf16)v;
+      else
+        w[i][e] = v;
+    }
+  }
 }
 
 // Step indices of launch-relative step k for direction d.
@@ -184,15 +213,11 @@ __device__ inline StepIdx fwd_step(const int32_t* bs, const int32_t* off, int T,
 
 template <int G, bool BF16, int NW, int MAXC>
 __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
-  using T = typename LdsT<BF16>::T;
-  constexpr int CH = LdsT<BF16>::CH;
-  constexpr int CPL = LdsT<BF16>::CPL;
-  constexpr int NC = 16;
+  constexpr int CH = Chunk<BF16>::CH;
+  constexpr int CPL = Chunk<BF16>::CPL;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int H = a.H;
-  const int LDW = H + LdsT<BF16>::PAD;
-  T* Ws = reinterpret_cast<T*>(smem);
-  float* red = reinterpret_cast<float*>(smem + ((NC * LDW * sizeof(T) + 15) / 16) * 16);
+  float* red = reinterpret_cast<float*>(smem);
   int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
   int32_t* toff = tbs + a.T;                                  // offsets [T+1]
   for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
@@ -211,13 +236,15 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lq = lane >> 4;
 
-  // W slice: column c = g*4 + u holds row g*H + j0 + u of W_hh (zero for g >= G).
-  const float* whh = a.whh[d];
-  for (int i = threadIdx.x; i < NC * H; i += blockDim.x) {
-    const int c = i / H, k = i % H;
-    const int g = c >> 2, u = c & 3;
-    const float v = g < G ? whh[(int64_t)(g * H + j0 + u) * H + k] : 0.f;
-    Ws[c * LDW + k] = (T)v;
+  // Weight block: column c = g*4 + u is row g*H + j0 + u of W_hh (zero for
+  // g >= G); this lane feeds column lr.
+  const int nchunks = H / CH;
+  typename WFrag<BF16>::T wreg[MAXC];
+  {
+    const int g = lr >> 2, uu = lr & 3;
+    const float* wrow = a.whh[d] + (int64_t)(g * H + j0 + uu) * H;
+    load_wfrags<BF16, MAXC>(wreg, wave, NW, nchunks, lq * CPL,
+                            [&](int k) { return g < G ? wrow[k] : 0.f; });
   }
   // Epilogue lanes of wave 0: row r0 + (lane >> 2), unit j0 + (lane & 3).
   const int erow = r0 + (lane >> 2);
@@ -232,7 +259,6 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
   float* stash = a.stash[d];
   float* cst = a.cst[d];
   float* hout = a.hout + d * H;
-  const int nchunks = H / CH;
   const __amdgpu_buffer_rsrc_t hsrc = published_rsrc(a.hout, a.pub_bytes);
   __syncthreads();
 
@@ -263,7 +289,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
           r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + d * H) : kNoRow;
       unsigned u[CPL * MAXC];
       fetch_published<CPL, MAXC>(hsrc, row_off, wave, NW, nchunks, CH, lq * CPL, u);
-      const f4 acc = mma_chunks<BF16, MAXC>(u, Ws + lr * LDW, wave, NW, nchunks, lq * CPL);
+      const f4 acc = mma_chunks<BF16, MAXC>(u, wreg, wave, NW, nchunks);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
@@ -342,15 +368,12 @@ __device__ inline BwdIdx bwd_step(const int32_t* bs, const int32_t* off, int T, 
 
 template <int G, bool BF16, int NW, int MAXC>
 __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
-  using T = typename LdsT<BF16>::T;
-  constexpr int CH = LdsT<BF16>::CH;
-  constexpr int CPL = LdsT<BF16>::CPL;
+  constexpr int CH = Chunk<BF16>::CH;
+  constexpr int CPL = Chunk<BF16>::CPL;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int H = a.H;
   const int GH = G * H;
-  const int LDW = GH + LdsT<BF16>::PAD;
-  T* Ws = reinterpret_cast<T*>(smem);  // Ws[u][k] = W_hh[k][j0 + u]
-  float* red = reinterpret_cast<float*>(smem + ((kBwdUnits * LDW * sizeof(T) + 15) / 16) * 16);
+  float* red = reinterpret_cast<float*>(smem);
   int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
   int32_t* toff = tbs + a.T;                                  // offsets [T+1]
   for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
@@ -368,10 +391,14 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lq = lane >> 4;
 
-  const float* whh = a.whh[d];
-  for (int i = threadIdx.x; i < kBwdUnits * GH; i += blockDim.x) {
-    const int k = i / kBwdUnits, u = i % kBwdUnits;
-    Ws[u * LDW + k] = (T)whh[(int64_t)k * H + j0 + u];
+  // Weight block: column u is column j0 + u of W_hh (K = G*H rows); this
+  // lane feeds column lr.
+  const int nchunks = GH / CH;
+  typename WFrag<BF16>::T wreg[MAXC];
+  {
+    const float* wcol = a.whh[d] + j0 + lr;
+    load_wfrags<BF16, MAXC>(wreg, wave, NW, nchunks, lq * CPL,
+                            [&](int k) { return wcol[(int64_t)k * H]; });
   }
   // Epilogue: threads 0..255 -> row r0 + (tid >> 4), unit j0 + (tid & 15).
   const bool epi = threadIdx.x < 256;
@@ -385,7 +412,6 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
   float* da = a.da[d];
   float* dah = a.dah[d];
   const float* da_next = G == 3 ? dah : da;
-  const int nchunks = GH / CH;
   const __amdgpu_buffer_rsrc_t dsrc = published_rsrc(da_next, a.pub_bytes);
   __syncthreads();
 
@@ -426,7 +452,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
             r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
         unsigned u[CPL * MAXC];
         fetch_published<CPL, MAXC>(dsrc, row_off, wave, NW, nchunks, CH, lq * CPL, u);
-        acc = mma_chunks<BF16, MAXC>(u, Ws + lr * LDW, wave, NW, nchunks, lq * CPL);
+        acc = mma_chunks<BF16, MAXC>(u, wreg, wave, NW, nchunks);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
@@ -572,8 +598,7 @@ hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, i
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
   if (a.T > kMaxSteps) return hipSuccess;
-  const size_t w = 16 * (size_t)(a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
-  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  const size_t sh = sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
   const void* k = cell == RNNBKT_CELL_LSTM
                       ? (bf16 ? fwd_kernel<4, true>(nw, maxc) : fwd_kernel<4, false>(nw, maxc))
                       : (bf16 ? fwd_kernel<3, true>(nw, maxc) : fwd_kernel<3, false>(nw, maxc));
@@ -592,8 +617,7 @@ hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, i
   a.rgroups = (B + 15) / 16;
   const int blocks = dirs * a.slices * a.rgroups;
   if (a.T > kMaxSteps) return hipSuccess;
-  const size_t w = kBwdUnits * (size_t)(G * a.H + (bf16 ? 8 : 4)) * (bf16 ? 2 : 4);
-  const size_t sh = (w + 15) / 16 * 16 + sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  const size_t sh = sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
   const void* k = cell == RNNBKT_CELL_LSTM
                       ? (bf16 ? bwd_kernel<4, true>(nw, maxc) : bwd_kernel<4, false>(nw, maxc))
                       : (bf16 ? bwd_kernel<3, true>(nw, maxc) : bwd_kernel<3, false>(nw, maxc));
