@@ -399,47 +399,103 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   }
 
   const int GH = s.G * s.H;
-  const bool persistent = use_persistent();
+  const int ldh = s.dirs * s.H;
+  const uint64_t hout_bytes = sizeof(float) * (uint64_t)N * ldh;
+  // One recurrence unit (layer l, direction d) of a persistent launch.
+  auto make_unit = [&](int l, int d, bool in_published) {
+    FwdUnit u{};
+    const int ld = l * s.dirs + d;
+    u.in = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
+    u.ld_in = s.din(l);
+    u.kin = s.din(l);
+    const uint64_t ib = sizeof(float) * (uint64_t)N * u.ld_in;
+    u.in_bytes = ib < 0x7FFFFFF0u ? (uint32_t)ib : 0x7FFFFFF0u;
+    u.in_published = in_published ? 1 : 0;
+    u.wih = params + po.wih[ld];
+    u.whh = params + po.whh[ld];
+    u.b = params + po.b[ld];
+    u.bhh = s.cell == RNNBKT_CELL_GRU ? params + po.bhh[ld] : nullptr;
+    u.hout = at<float>(reserve, c.hout[l]);
+    u.out_bytes = hout_bytes < 0x7FFFFFF0u ? (uint32_t)hout_bytes : 0x7FFFFFF0u;
+    u.stash = at<float>(reserve, c.stash[ld]);
+    u.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+    u.dir = d;
+    u.hcol = d * s.H;
+    return u;
+  };
+  auto base_launch = [&]() {
+    FwdLaunch L{};
+    L.bs = d_bs;
+    L.off = d_off;
+    L.H = s.H;
+    L.ldh = ldh;
+    L.T = T;
+    return L;
+  };
+  // Algorithmic flops of the step products of one unit.
+  auto unit_flops = [&](int l) {
+    double fl = 0;
+    for (int t = 0; t < T; ++t) fl += 2.0 * bs[t] * GH * (s.din(l) + s.H);
+    return fl;
+  };
+  // Layers [l, l+n) of a unidirectional stack in one launch, each layer
+  // reading the one below as it is published.  Returns the largest n that
+  // the persistent kernel can keep resident (0 if none).
+  auto stack_fits = [&](int l0) {
+    int best = 0;
+    for (int n = 1; n <= kMaxUnits && l0 + n <= s.L; ++n) {
+      FwdLaunch L = base_launch();
+      for (int q = 0; q < n; ++q) L.u[q] = make_unit(l0 + q, 0, q > 0);
+      L.nunits = n;
+      if (fwd_persistent_blocks(L, s.cell, s.bf16, B) > 0) best = n;
+    }
+    return best;
+  };
+  std::vector<char> layer_done(s.L, 0);
+  if (use_persistent()) {
+    int l = 0;
+    while (l < s.L) {
+      FwdLaunch L = base_launch();
+      int n = 0;
+      if (s.dirs == 1) {
+        n = stack_fits(l);
+        for (int q = 0; q < n; ++q) L.u[q] = make_unit(l + q, 0, q > 0);
+      } else {
+        n = 1;
+        for (int d = 0; d < 2; ++d) L.u[d] = make_unit(l, d, false);
+      }
+      L.nunits = s.dirs == 1 ? n : 2;
+      bool fits = false;
+      if (n > 0) {
+        double fl = 0;
+        for (int q = 0; q < n; ++q) fl += s.dirs * unit_flops(l + q);
+        {
+          Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+          for (int q = 0; q < n; ++q)
+            RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l + q])),
+                                       N * ldh, kPublishSentinel, st));
+        }
+        Timed tm(RNNBKT_KERNEL_STEP_FWD, fl, 0.0, st);
+        RNNBKT_HIP(launch_fwd_persistent(L, s.cell, s.bf16, B, st, &fits));
+      }
+      if (!fits) break;  // this layer and the ones above take the per-step kernels
+      for (int q = 0; q < n; ++q) layer_done[l + q] = 1;
+      l += n;
+    }
+  }
+  // Per-step kernels for layers the persistent kernel does not take: input
+  // projection of all frames as one GEMM, then one launch per time step.
   for (int l = 0; l < s.L; ++l) {
+    if (layer_done[l]) continue;
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
     const int din = s.din(l);
     float* hout = at<float>(reserve, c.hout[l]);
-    // Input projection of every valid frame at once (bias folded in).
     for (int d = 0; d < s.dirs; ++d) {
       const int ld = l * s.dirs + d;
       RNNBKT_HIP(gemm(xin, din, true, params + po.wih[ld], din, true, at<float>(workspace, c.gx[d]),
                       GH, (int)N, GH, din, params + po.b[ld], 0, s.bf16, st));
     }
-    bool done = false;
-    if (persistent) {
-      PersistFwdArgs a{};
-      for (int d = 0; d < s.dirs; ++d) {
-        const int ld = l * s.dirs + d;
-        a.gx[d] = at<float>(workspace, c.gx[d]);
-        a.whh[d] = params + po.whh[ld];
-        a.bhh[d] = s.cell == RNNBKT_CELL_GRU ? params + po.bhh[ld] : nullptr;
-        a.stash[d] = at<float>(reserve, c.stash[ld]);
-        a.cst[d] = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
-      }
-      a.hout = hout;
-      a.bs = d_bs;
-      a.off = d_off;
-      const uint64_t pub = sizeof(float) * (uint64_t)N * s.dirs * s.H;
-      a.pub_bytes = pub < 0x7FFFFFF0u ? (uint32_t)pub : 0u;
-      a.H = s.H;
-      a.ldh = s.dirs * s.H;
-      a.T = T;
-      double fl = 0;
-      for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * GH * s.H;
-      {
-        Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-        RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(hout), N * s.dirs * s.H,
-                                   kPublishSentinel, st));
-      }
-      Timed tm(RNNBKT_KERNEL_STEP_FWD, fl, 0.0, st);
-      RNNBKT_HIP(launch_fwd_persistent(a, s.cell, s.bf16, B, s.dirs, st, &done));
-    }
-    for (int d = 0; d < s.dirs && !done; ++d) {
+    for (int d = 0; d < s.dirs; ++d) {
       const int ld = l * s.dirs + d;
       StepFwdArgs a{};
       a.gx = at<float>(workspace, c.gx[d]);
@@ -449,7 +505,7 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
       a.stash = at<float>(reserve, c.stash[ld]);
       a.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
       a.H = s.H;
-      a.ldh = s.dirs * s.H;
+      a.ldh = ldh;
       for (int k = 0; k < T; ++k) {
         const int t = d == 0 ? k : T - 1 - k;
         a.row0 = off[t];

@@ -125,16 +125,34 @@ hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_
 // sentinel 0xFFFFFFFF in every element when the launch starts.  *fits
 // reports whether the grid can be resident at once (and the shape is
 // supported); when it cannot, nothing is launched.
-struct PersistFwdArgs {
-  const float* gx[2];
-  const float* whh[2];
-  const float* bhh[2];
-  float* stash[2];
-  float* cst[2];
-  float* hout;  // layer output [N x ldh]; direction d at column d*H
+constexpr int kMaxUnits = 4;
+
+// One (layer, direction) recurrence inside a forward launch.  The input
+// projection is done per step inside the kernel: the reduction operand of
+// a step is [input row (kin floats, zero-padded to a chunk multiple) ;
+// previous state h (H floats)] against [W_ih ; W_hh].
+struct FwdUnit {
+  const float* in;     // input rows: frame f at in + f*ld_in (packed X or a layer output)
+  const float* wih;    // [G*H x kin]
+  const float* whh;    // [G*H x H]
+  const float* b;      // LSTM b / GRU b_ih [G*H]
+  const float* bhh;    // GRU b_hh [3H]; LSTM unused
+  float* hout;         // layer output base [N x ldh]; this unit writes columns hcol..hcol+H-1
+  float* stash;        // [N x 4H] (LSTM i,f,g,o; GRU r,z,n,W_hn h + b_hn)
+  float* cst;          // LSTM [N x H]; GRU unused
+  uint32_t in_bytes;   // bytes of the array `in` addresses (< 2^31 - 16)
+  uint32_t out_bytes;  // bytes of hout (< 2^31 - 16)
+  int32_t ld_in, kin;  // input row stride and length
+  int32_t in_published;  // 1: `in` is published by another unit of the same launch
+  int32_t dir, hcol;     // direction (0 forward in time, 1 reverse) and output column
+  int32_t wg_begin;      // first workgroup of this unit
+};
+
+struct FwdLaunch {
+  FwdUnit u[kMaxUnits];
+  int32_t nunits;
   const int32_t* bs;
   const int32_t* off;
-  uint32_t pub_bytes;  // bytes of hout (the published array); must be < 2^31 - 16
   int32_t H, ldh, T;
   int32_t slices, rgroups;  // set by the launcher
 };
@@ -154,8 +172,11 @@ struct PersistBwdArgs {
   int32_t slices, rgroups;
 };
 
-hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, int dirs,
-                                 hipStream_t stream, bool* fits);
+// Workgroups a forward launch of these units would need (0 = shape not
+// supported by the persistent kernel).
+int fwd_persistent_blocks(const FwdLaunch& a, int cell, bool bf16, int B);
+hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
+                                 bool* fits);
 hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
                                  hipStream_t stream, bool* fits);
 // Number of waits for published values that gave up (should stay 0).

@@ -24,6 +24,7 @@
 // rnnbkt_sync_check) and later waits return at once, so a launch always ends.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -110,7 +111,6 @@ __device__ inline void fetch_published(__amdgpu_buffer_rsrc_t rsrc, unsigned row
 }
 
 constexpr int kMaxSteps = 6144;  // batch tables kept in LDS: T_max above this is not handled here
-constexpr int kFwdUnits = 4;   // hidden units per forward workgroup (x G gates <= 16 columns)
 constexpr int kBwdUnits = 16;  // hidden units per backward workgroup
 constexpr int kMaxPerLane = 32;  // reduction-operand floats a lane holds per step
 
@@ -211,107 +211,190 @@ __device__ inline StepIdx fwd_step(const int32_t* bs, const int32_t* off, int T,
   return s;
 }
 
-template <int G, bool BF16, int NW, int MAXC>
-__global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
+// Reads the lane's operand slots of one step: slot i (chunk c = first +
+// i*stride) holds NV 128-bit pieces at byte offsets offs[i][v] in the input
+// array (from_in[i]) or in the output array; slots with chk[i] are published
+// values and are re-read until none holds the sentinel.  from_in / chk are
+// uniform across the wave.
+template <int NV, int MAXC>
+__device__ inline void fetch_slots(__amdgpu_buffer_rsrc_t rin, __amdgpu_buffer_rsrc_t rout,
+                                   const unsigned (&offs)[MAXC][NV], const bool (&from_in)[MAXC],
+                                   const bool (&chk)[MAXC], unsigned (&u)[MAXC * NV * 4]) {
+  unsigned spins = 0;
+  for (;;) {
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const u4 x = from_in[i]
+                         ? __builtin_amdgcn_raw_buffer_load_b128(rin, offs[i][v], 0, kDeviceScope)
+                         : __builtin_amdgcn_raw_buffer_load_b128(rout, offs[i][v], 0, kDeviceScope);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) u[(i * NV + v) * 4 + e] = x[e];
+      }
+    bool ready = true;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+      if (chk[i])
+#pragma unroll
+        for (int e = 0; e < NV * 4; ++e) ready &= u[i * NV * 4 + e] != kSentinel;
+    if (__all(ready)) return;
+    if (spins == 0 && __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) != 0u)
+      return;
+    if (++spins == (1u << 20)) {
+      if ((threadIdx.x & 63) == 0)
+        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Copies unit `ui` out of the kernel arguments without dynamic indexing.
+__device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
+  FwdUnit u = a.u[0];
+  if (ui == 1) u = a.u[1];
+  if (ui == 2) u = a.u[2];
+  if (ui == 3) u = a.u[3];
+  return u;
+}
+
+// Forward recurrence of the launch's units.  Workgroup = 16 rows x 4*NT
+// hidden units of one unit; column block nt holds, for its 4 units, the
+// LSTM gates (i, f, g, o) or the GRU groups (r, z, n from the input, n from
+// the state), so one MFMA tile per block yields every pre-activation a
+// unit's update needs.  NW waves split the reduction dimension; waves
+// 0..NT-1 then run the state update of one column block each.
+template <int G, bool BF16, int NW, int MAXC, int NT>
+__global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
+  constexpr int NV = CPL / 4;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int H = a.H;
-  float* red = reinterpret_cast<float*>(smem);
-  int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
-  int32_t* toff = tbs + a.T;                                  // offsets [T+1]
+  float* red = reinterpret_cast<float*>(smem);                     // [NW][NT][256]
+  int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * NT * 256);  // batch sizes [T]
+  int32_t* toff = tbs + a.T;                                       // offsets [T+1]
   for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
     if (i < a.T) tbs[i] = a.bs[i];
     toff[i] = a.off[i];
   }
-
-  const int per_dir = a.slices * a.rgroups;
-  const int d = blockIdx.x / per_dir;
-  const int rem = blockIdx.x % per_dir;
+  int ui = 0;
+  for (int q = 1; q < a.nunits; ++q)
+    if ((int)blockIdx.x >= a.u[q].wg_begin) ui = q;
+  const FwdUnit U = pick_unit(a, ui);
+  const int rem = blockIdx.x - U.wg_begin;
   const int slice = rem % a.slices;
   const int rg = rem / a.slices;
-  const int j0 = slice * kFwdUnits;
+  const int H = a.H;
+  const int j0 = slice * 4 * NT;
   const int r0 = rg * 16;
-  const int GH = G * H;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lq = lane >> 4;
+  const int kin_pad = (U.kin + CH - 1) / CH * CH;
+  const int nin = kin_pad / CH;
+  const int nch = nin + H / CH;
 
-  // Weight block: column c = g*4 + u is row g*H + j0 + u of W_hh (zero for
-  // g >= G); this lane feeds column lr.
-  const int nchunks = H / CH;
-  typename WFrag<BF16>::T wreg[MAXC];
+  // Weight fragments: this lane feeds column lr of every column block.
+  typename WFrag<BF16>::T w[NT][MAXC];
   {
-    const int g = lr >> 2, uu = lr & 3;
-    const float* wrow = a.whh[d] + (int64_t)(g * H + j0 + uu) * H;
-    load_wfrags<BF16, MAXC>(wreg, wave, NW, nchunks, lq * CPL,
-                            [&](int k) { return g < G ? wrow[k] : 0.f; });
+    const int grp = lr >> 2, uu = lr & 3;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int j = j0 + 4 * nt + uu;
+      // gate row of W_ih / W_hh feeding this column for the input part and
+      // the state part (-1 = none)
+      int gi, gh;
+      if (G == 4) {
+        gi = grp;
+        gh = grp;
+      } else {
+        gi = grp == 3 ? -1 : grp;
+        gh = grp == 2 ? -1 : (grp == 3 ? 2 : grp);
+      }
+      const float* wi = gi >= 0 ? U.wih + (int64_t)(gi * H + j) * U.kin : nullptr;
+      const float* wh = gh >= 0 ? U.whh + (int64_t)(gh * H + j) * H : nullptr;
+      load_wfrags<BF16, MAXC>(w[nt], wave, NW, nch, lq * CPL, [&](int k) {
+        if (k < kin_pad) return (wi && k < U.kin) ? wi[k] : 0.f;
+        return wh ? wh[k - kin_pad] : 0.f;
+      });
+    }
   }
-  // Epilogue lanes of wave 0: row r0 + (lane >> 2), unit j0 + (lane & 3).
+  // State-update lanes: wave nt < NT owns row r0 + (lane >> 2), unit
+  // j0 + 4*nt + (lane & 3) for the whole launch.
+  const bool epi = wave < NT;
   const int erow = r0 + (lane >> 2);
-  const int ej = j0 + (lane & 3);
-  float bhh[3] = {0.f, 0.f, 0.f};
-  if constexpr (G == 3) {
-    if (wave == 0)
-      for (int g = 0; g < 3; ++g) bhh[g] = a.bhh[d][g * H + ej];
+  const int ej = j0 + 4 * (epi ? wave : 0) + (lane & 3);
+  float bi[4] = {0.f, 0.f, 0.f, 0.f}, bh[3] = {0.f, 0.f, 0.f};
+  if (epi) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) bi[g] = U.b[g * H + ej];
+    if constexpr (G == 3) {
+#pragma unroll
+      for (int g = 0; g < 3; ++g) bh[g] = U.bhh[g * H + ej];
+    }
   }
   float c_state = 0.f, h_state = 0.f;
-  const float* gxd = a.gx[d];
-  float* stash = a.stash[d];
-  float* cst = a.cst[d];
-  float* hout = a.hout + d * H;
-  const __amdgpu_buffer_rsrc_t hsrc = published_rsrc(a.hout, a.pub_bytes);
+  const __amdgpu_buffer_rsrc_t rin = published_rsrc(U.in, U.in_bytes);
+  const __amdgpu_buffer_rsrc_t rout = published_rsrc(U.hout, U.out_bytes);
   __syncthreads();
 
-  // The input projection of a step's rows does not depend on other
-  // workgroups: wave 0 fetches it one step ahead.
-  // Loads are unconditional within wave 0 (rows past the active ones read
-  // frame 0 and are ignored) so no branch forces a wait on older loads.
-  float gxv[G];
-  auto load_gx = [&](const StepIdx& q) {
-    if (wave == 0) {
-      const int64_t fr = erow < q.rows ? q.row0 + erow : 0;
-      const float* gr = gxd + fr * GH;
-#pragma unroll
-      for (int g = 0; g < G; ++g) gxv[g] = gr[g * H + ej];
-    }
-  };
-  StepIdx s = fwd_step(tbs, toff, a.T, d, 0);
-  load_gx(s);
+  StepIdx s = fwd_step(tbs, toff, a.T, U.dir, 0);
   for (int k = 0; k < a.T; ++k) {
-    // Next step's table entries first, so no later wait has to cover them.
     StepIdx nx = s;
-    if (k + 1 < a.T) nx = fwd_step(tbs, toff, a.T, d, k + 1);
+    if (k + 1 < a.T) nx = fwd_step(tbs, toff, a.T, U.dir, k + 1);
     const bool active = r0 < s.rows;
-    const bool erow_on = active && wave == 0 && erow < s.rows;
     if (active) {
       const int r = r0 + lr;
-      const unsigned row_off =
-          r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + d * H) : kNoRow;
-      unsigned u[CPL * MAXC];
-      fetch_published<CPL, MAXC>(hsrc, row_off, wave, NW, nchunks, CH, lq * CPL, u);
-      const f4 acc = mma_chunks<BF16, MAXC>(u, wreg, wave, NW, nchunks);
+      unsigned offs[MAXC][NV];
+      bool from_in[MAXC], chk[MAXC];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
+      for (int i = 0; i < MAXC; ++i) {
+        const int c = wave + i * NW;
+        from_in[i] = c < nin;
+        chk[i] = c < nin ? U.in_published != 0 : c < nch;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int kk = c * CH + lq * CPL + 4 * v;
+          unsigned o = kNoRow;
+          if (c < nin) {
+            if (r < s.rows && kk < U.kin)
+              o = 4u * (unsigned)((int64_t)(s.row0 + r) * U.ld_in + kk);
+          } else if (c < nch) {
+            if (r < s.prev_rows)
+              o = 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + U.hcol + (kk - kin_pad));
+          }
+          offs[i][v] = o;
+        }
+      }
+      unsigned uu[MAXC * NV * 4];
+      fetch_slots<NV, MAXC>(rin, rout, offs, from_in, chk, uu);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const f4 acc = mma_chunks<BF16, MAXC>(uu, w[nt], wave, NW, nch);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red[(wave * NT + nt) * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
+      }
     }
     __syncthreads();
-    if (erow_on) {
-      const int rr = lane >> 2, uu = lane & 3;
-      float sg[G];
+    if (epi && active && erow < s.rows) {
+      const int rr = lane >> 2, u4_ = lane & 3;
+      float sg[4];
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
+      for (int g = 0; g < 4; ++g) {
         float v = 0.f;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) v += red[w * 256 + rr * 16 + g * 4 + uu];
+        for (int w_ = 0; w_ < NW; ++w_) v += red[(w_ * NT + wave) * 256 + rr * 16 + g * 4 + u4_];
         sg[g] = v;
       }
       const bool has_prev = erow < s.prev_rows;
       const int64_t f = s.row0 + erow;
-      float* st = stash + f * 4 * H;
+      float* st = U.stash + f * 4 * H;
       if constexpr (G == 4) {
-        const float ig = sigm(gxv[0] + sg[0]);
-        const float fg = sigm(gxv[1] + sg[1]);
-        const float gg = tanhf(gxv[2] + sg[2]);
-        const float og = sigm(gxv[3] + sg[3]);
+        const float ig = sigm(sg[0] + bi[0]);
+        const float fg = sigm(sg[1] + bi[1]);
+        const float gg = tanhf(sg[2] + bi[2]);
+        const float og = sigm(sg[3] + bi[3]);
         const float cp = has_prev ? c_state : 0.f;
         c_state = fg * cp + ig * gg;
         h_state = og * tanhf(c_state);
@@ -319,14 +402,12 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
         st[H + ej] = fg;
         st[2 * H + ej] = gg;
         st[3 * H + ej] = og;
-        cst[f * H + ej] = c_state;
+        U.cst[f * H + ej] = c_state;
       } else {
-        const float ahr = sg[0] + bhh[0];
-        const float ahz = sg[1] + bhh[1];
-        const float ahn = sg[2] + bhh[2];
-        const float rg_ = sigm(gxv[0] + ahr);
-        const float z = sigm(gxv[1] + ahz);
-        const float n = tanhf(gxv[2] + rg_ * ahn);
+        const float rg_ = sigm(sg[0] + bi[0] + bh[0]);
+        const float z = sigm(sg[1] + bi[1] + bh[1]);
+        const float ahn = sg[3] + bh[2];
+        const float n = tanhf(sg[2] + bi[2] + rg_ * ahn);
         const float hp = has_prev ? h_state : 0.f;
         h_state = (1.f - z) * n + z * hp;
         st[ej] = rg_;
@@ -334,10 +415,9 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(PersistFwdArgs a) {
         st[2 * H + ej] = n;
         st[3 * H + ej] = ahn;
       }
-      publish(hout + f * a.ldh + ej, h_state);
+      publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
     }
     s = nx;
-    if (k + 1 < a.T) load_gx(s);
     __syncthreads();  // red is rewritten by the next step
   }
 }
@@ -579,31 +659,90 @@ bool split_for(int K, bool bf16, int* nw, int* maxc) {
   return nullptr;
 
 template <int G, bool BF16>
-const void* fwd_kernel(int nw, int maxc) { RNNBKT_PICK(k_fwd_persistent, G, BF16) }
-
-template <int G, bool BF16>
 const void* bwd_kernel(int nw, int maxc) { RNNBKT_PICK(k_bwd_persistent, G, BF16) }
 
 #undef RNNBKT_PICK
 
 }  // namespace
 
-hipError_t launch_fwd_persistent(PersistFwdArgs a, int cell, bool bf16, int B, int dirs,
-                                 hipStream_t st, bool* fits) {
+namespace {
+
+// Chunks per wave (a power of two) for a reduction of nch chunks over 4
+// waves; 0 if above the per-lane budget.
+int fwd_maxc(int nch, bool bf16) {
+  const int per = (nch + 3) / 4;
+  int m = 1;
+  while (m < per) m *= 2;
+  return m <= (bf16 ? 8 : 16) ? m : 0;
+}
+
+template <int G, bool BF16, int NT>
+const void* fwd_kernel_nt(int maxc) {
+  switch (maxc) {
+    case 1: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 1, NT>);
+    case 2: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 2, NT>);
+    case 4: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 4, NT>);
+    case 8: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 8, NT>);
+  }
+  if constexpr (!BF16)
+    if (maxc == 16) return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 16, NT>);
+  return nullptr;
+}
+
+const void* fwd_kernel(int cell, bool bf16, int nt, int maxc) {
+  if (cell == RNNBKT_CELL_LSTM) {
+    if (bf16) return nt == 1 ? fwd_kernel_nt<4, true, 1>(maxc) : fwd_kernel_nt<4, true, 2>(maxc);
+    return nt == 1 ? fwd_kernel_nt<4, false, 1>(maxc) : fwd_kernel_nt<4, false, 2>(maxc);
+  }
+  if (bf16) return nt == 1 ? fwd_kernel_nt<3, true, 1>(maxc) : fwd_kernel_nt<3, true, 2>(maxc);
+  return nt == 1 ? fwd_kernel_nt<3, false, 1>(maxc) : fwd_kernel_nt<3, false, 2>(maxc);
+}
+
+struct FwdPlan {
+  const void* kernel;
+  int nt, maxc, blocks;
+  size_t shmem;
+};
+
+// Column blocks per workgroup: 2 (8 units) for wide layers, else 1 (4 units).
+FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
+  FwdPlan p{nullptr, 0, 0, 0, 0};
+  const int ch = bf16 ? 32 : 16;
+  if (a.T > kMaxSteps || a.nunits < 1 || a.nunits > kMaxUnits || a.H % ch != 0) return p;
+  int nch = 0;
+  for (int q = 0; q < a.nunits; ++q) {
+    const FwdUnit& u = a.u[q];
+    if (u.kin < 1 || u.kin % 4 != 0 || u.in_bytes >= kNoRow || u.out_bytes >= kNoRow) return p;
+    nch = std::max(nch, (u.kin + ch - 1) / ch + a.H / ch);
+  }
+  p.nt = a.H >= 256 && a.H % 8 == 0 ? 2 : 1;
+  p.maxc = fwd_maxc(nch, bf16);
+  if (p.maxc == 0) return p;
+  p.blocks = a.nunits * (a.H / (4 * p.nt)) * ((B + 15) / 16);
+  p.shmem = sizeof(float) * 4 * p.nt * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  p.kernel = fwd_kernel(cell, bf16, p.nt, p.maxc);
+  return p;
+}
+
+}  // namespace
+
+int fwd_persistent_blocks(const FwdLaunch& a, int cell, bool bf16, int B) {
+  const FwdPlan p = plan_fwd(a, cell, bf16, B);
+  if (!p.kernel) return 0;
+  if (p.blocks > max_coresident(p.kernel, 256, p.shmem)) return 0;
+  return p.blocks;
+}
+
+hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStream_t st,
+                                 bool* fits) {
   *fits = false;
-  int nw = 0, maxc = 0;
-  if (!split_for(a.H, bf16, &nw, &maxc) || a.H % kFwdUnits != 0) return hipSuccess;
-  if (a.pub_bytes == 0 || a.pub_bytes >= kNoRow) return hipSuccess;
-  a.slices = a.H / kFwdUnits;
+  const FwdPlan p = plan_fwd(a, cell, bf16, B);
+  if (!p.kernel) return hipSuccess;
+  a.slices = a.H / (4 * p.nt);
   a.rgroups = (B + 15) / 16;
-  const int blocks = dirs * a.slices * a.rgroups;
-  if (a.T > kMaxSteps) return hipSuccess;
-  const size_t sh = sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
-  const void* k = cell == RNNBKT_CELL_LSTM
-                      ? (bf16 ? fwd_kernel<4, true>(nw, maxc) : fwd_kernel<4, false>(nw, maxc))
-                      : (bf16 ? fwd_kernel<3, true>(nw, maxc) : fwd_kernel<3, false>(nw, maxc));
-  if (!k) return hipSuccess;
-  return coop_launch(k, blocks, 64 * nw, sh, &a, st, fits);
+  const int per_unit = a.slices * a.rgroups;
+  for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
+  return coop_launch(p.kernel, p.blocks, 256, p.shmem, &a, st, fits);
 }
 
 hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
