@@ -117,7 +117,8 @@ struct Carve {
   size_t gx[2], loss_part;
   size_t ws_fwd;
   // workspace (backward)
-  size_t dha, dhb, da[2], dah[2], carry, splitk, colsum;
+  size_t dha, dhb, carry, splitk, colsum;
+  std::vector<size_t> da, dah;  // per layer*dirs
 
   size_t ws_bwd;
   size_t workspace;
@@ -156,9 +157,10 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   pos = common;
   c.dha = take(sizeof(float) * N * s.Htop);
   c.dhb = take(sizeof(float) * N * s.Htop);
-  for (int d = 0; d < 2; ++d) c.da[d] = d < s.dirs ? take(sizeof(float) * N * GH) : c.da[0];
-  for (int d = 0; d < 2; ++d)
-    c.dah[d] = (s.cell == RNNBKT_CELL_GRU && d < s.dirs) ? take(sizeof(float) * N * GH) : c.dah[0];
+  for (int q = 0; q < s.L * s.dirs; ++q) {
+    c.da.push_back(take(sizeof(float) * N * GH));
+    c.dah.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0);
+  }
   c.carry = take(sizeof(float) * (size_t)B * s.H);
   size_t sk = 0;
   auto need = [&](int64_t M, int64_t Nn, int64_t K) {
@@ -578,7 +580,6 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   const int GH = s.G * s.H;
   const int n = (int)N;
   const bool gru = s.cell == RNNBKT_CELL_GRU;
-  const bool persistent = use_persistent();
 
   // Output layer: dH_top = dZ W_out, dW_out = dZ^T H_top, db_out = colsum dZ.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
@@ -591,83 +592,182 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, kColsumRows, cs, grads + po.bout, st));
   }
 
-  float* dh_in = dha;
-  float* dx = dhb;
-  for (int l = s.L - 1; l >= 0; --l) {
+  auto da_of = [&](int l, int d) { return at<float>(workspace, c.da[l * s.dirs + d]); };
+  auto dah_of = [&](int l, int d) {
+    return gru ? at<float>(workspace, c.dah[l * s.dirs + d]) : nullptr;
+  };
+  const uint64_t rec_b = sizeof(float) * (uint64_t)N * GH;
+  const uint32_t rec_bytes = rec_b < 0x7FFFFFF0u ? (uint32_t)rec_b : 0x7FFFFFF0u;
+  // Unit (layer l, direction d) of a persistent backward launch.
+  auto make_unit = [&](int l, int d, const float* dh, bool up_published, bool publish_dax) {
+    BwdUnit u{};
+    const int ld = l * s.dirs + d;
+    if (s.dirs == 1 && l + 1 < s.L) {
+      u.up = da_of(l + 1, 0);
+      u.wih_up = params + po.wih[l + 1];
+      u.k_up = GH;
+      u.din_up = s.din(l + 1);
+      u.up_bytes = rec_bytes;
+      u.up_published = up_published ? 1 : 0;
+    }
+    u.whh = params + po.whh[ld];
+    u.dh_in = dh;
+    u.ld_dh = s.Htop;
+    u.stash = at<float>(reserve, c.stash[ld]);
+    u.cst = gru ? nullptr : at<float>(reserve, c.cst[ld]);
+    u.hout = at<float>(reserve, c.hout[l]);
+    u.da = da_of(l, d);
+    u.dah = dah_of(l, d);
+    u.rec_bytes = rec_bytes;
+    u.publish_dax = publish_dax ? 1 : 0;
+    u.dir = d;
+    u.hcol = d * s.H;
+    return u;
+  };
+  auto base_launch = [&]() {
+    BwdLaunch Lc{};
+    Lc.bs = d_bs;
+    Lc.off = d_off;
+    Lc.H = s.H;
+    Lc.ldh = s.dirs * s.H;
+    Lc.T = T;
+    return Lc;
+  };
+  // Launch plan: unidirectional stacks run top-down, as many layers per
+  // launch as stay resident (each layer reads the one above as it is
+  // published); bidirectional layers run one layer (both directions) per
+  // launch with the gradient from above computed by a GEMM in between.
+  struct Group {
+    int hi, n;
+  };
+  std::vector<Group> groups;
+  bool persistent = use_persistent();
+  if (persistent) {
+    int hi = s.L - 1;
+    while (hi >= 0 && persistent) {
+      int best = 0;
+      const int maxn = s.dirs == 1 ? std::min(kMaxUnits, hi + 1) : 1;
+      for (int n = 1; n <= maxn; ++n) {
+        BwdLaunch Lc = base_launch();
+        for (int q = 0; q < n; ++q)
+          for (int d = 0; d < s.dirs; ++d)
+            Lc.u[q * s.dirs + d] = make_unit(hi - q, d, dha, q > 0, gru && q + 1 < n);
+        Lc.nunits = n * s.dirs;
+        if (bwd_persistent_blocks(Lc, s.cell, s.bf16, B) > 0) best = n;
+      }
+      if (best == 0) persistent = false;
+      groups.push_back({hi, best});
+      hi -= best;
+    }
+  }
+
+  if (persistent) {
+    float* dh_in = dha;  // gradient w.r.t. the output of the top layer of the next group
+    float* dx = dhb;
+    for (const Group& g : groups) {
+      BwdLaunch Lc = base_launch();
+      for (int q = 0; q < g.n; ++q) {
+        const int l = g.hi - q;
+        // Only the group's top layer reads a plain gradient from above: dH of
+        // the output layer, or (bidirectional) the dX GEMM of the layer above.
+        const float* dh = (q == 0 && (l == s.L - 1 || s.dirs == 2)) ? dh_in : nullptr;
+        for (int d = 0; d < s.dirs; ++d)
+          Lc.u[q * s.dirs + d] = make_unit(l, d, dh, q > 0, gru && q + 1 < g.n);
+      }
+      Lc.nunits = g.n * s.dirs;
+      double fl = 0;
+      for (int q = 0; q < g.n; ++q) {
+        const double kup = (s.dirs == 1 && g.hi - q + 1 < s.L) ? GH : 0;
+        for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * (kup + GH) * s.H;
+      }
+      {
+        Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+        for (int q = 0; q < Lc.nunits; ++q) {
+          const BwdUnit& u = Lc.u[q];
+          RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(gru ? u.dah : u.da), N * GH,
+                                     kPublishSentinel, st));
+          if (gru && u.publish_dax)
+            RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(u.da), N * GH, kPublishSentinel,
+                                       st));
+        }
+      }
+      bool fits = false;
+      {
+        Timed tm(RNNBKT_KERNEL_STEP_BWD, fl, 0.0, st);
+        RNNBKT_HIP(launch_bwd_persistent(Lc, s.cell, s.bf16, B, st, &fits));
+      }
+      RNNBKT_REQUIRE(fits, RNNBKT_EHIP, "lstm_bwd: persistent launch no longer fits");
+      // Bidirectional: gradient w.r.t. the layer below's output, both directions.
+      const int lo = g.hi - g.n + 1;
+      if (s.dirs == 2 && lo > 0) {
+        for (int d = 0; d < 2; ++d) {
+          const int ld = lo * 2 + d;
+          RNNBKT_HIP(gemm(da_of(lo, d), GH, true, params + po.wih[ld], s.din(lo), false, dx,
+                          s.din(lo), n, s.din(lo), GH, nullptr, d > 0 ? 1 : 0, s.bf16, st));
+        }
+        std::swap(dh_in, dx);
+      }
+    }
+  } else {
+    // One launch per time step: each layer needs the full gradient from above.
+    float* dh_in = dha;
+    float* dx = dhb;
+    for (int l = s.L - 1; l >= 0; --l) {
+      const float* hout = at<float>(reserve, c.hout[l]);
+      for (int d = 0; d < s.dirs; ++d) {
+        const int ld = l * s.dirs + d;
+        StepBwdArgs a{};
+        a.da_next = gru ? dah_of(l, d) : da_of(l, d);
+        a.whh = params + po.whh[ld];
+        a.dh_in = dh_in + d * s.H;
+        a.stash = at<float>(reserve, c.stash[ld]);
+        a.cst = gru ? nullptr : at<float>(reserve, c.cst[ld]);
+        a.hout = hout + d * s.H;
+        a.da = da_of(l, d);
+        a.dah = dah_of(l, d);
+        a.carry = carry;
+        a.H = s.H;
+        a.ldd = s.Htop;
+        a.ldh = s.dirs * s.H;
+        for (int k = 0; k < T; ++k) {
+          const int t = d == 0 ? T - 1 - k : k;
+          a.row0 = off[t];
+          a.rows = bs[t];
+          if (d == 0) {
+            a.next0 = t + 1 < T ? off[t + 1] : 0;
+            a.next_rows = t + 1 < T ? bs[t + 1] : 0;
+            a.prev0 = t > 0 ? off[t - 1] : 0;
+            a.prev_rows = t > 0 ? bs[t] : 0;
+          } else {
+            a.next0 = t > 0 ? off[t - 1] : 0;
+            a.next_rows = t > 0 ? bs[t] : 0;
+            a.prev0 = t + 1 < T ? off[t + 1] : 0;
+            a.prev_rows = t + 1 < T ? bs[t + 1] : 0;
+          }
+          Timed tm(RNNBKT_KERNEL_STEP_BWD, 2.0 * a.next_rows * GH * s.H, 0.0, st);
+          RNNBKT_HIP(launch_step_bwd(a, s.cell, s.bf16, st));
+        }
+      }
+      if (l > 0) {
+        for (int d = 0; d < s.dirs; ++d) {
+          const int ld = l * s.dirs + d;
+          RNNBKT_HIP(gemm(da_of(l, d), GH, true, params + po.wih[ld], s.din(l), false, dx,
+                          s.din(l), n, s.din(l), GH, nullptr, d > 0 ? 1 : 0, s.bf16, st));
+        }
+        std::swap(dh_in, dx);
+      }
+    }
+  }
+
+  // Weight gradients of every layer, reduced over every valid frame.
+  for (int l = 0; l < s.L; ++l) {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
     const int din = s.din(l);
     const float* hout = at<float>(reserve, c.hout[l]);
-    bool done = false;
-    if (persistent) {
-      PersistBwdArgs a{};
-      for (int d = 0; d < s.dirs; ++d) {
-        const int ld = l * s.dirs + d;
-        a.whh[d] = params + po.whh[ld];
-        a.stash[d] = at<float>(reserve, c.stash[ld]);
-        a.cst[d] = gru ? nullptr : at<float>(reserve, c.cst[ld]);
-        a.da[d] = at<float>(workspace, c.da[d]);
-        a.dah[d] = gru ? at<float>(workspace, c.dah[d]) : nullptr;
-      }
-      a.hout = hout;
-      a.dh_in = dh_in;
-      a.bs = d_bs;
-      a.off = d_off;
-      const uint64_t pub = sizeof(float) * (uint64_t)N * GH;
-      a.pub_bytes = pub < 0x7FFFFFF0u ? (uint32_t)pub : 0u;
-      a.H = s.H;
-      a.ldh = s.dirs * s.H;
-      a.ldd = s.Htop;
-      a.T = T;
-      double fl = 0;
-      for (int t = 1; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * GH * s.H;
-      {
-        Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-        for (int d = 0; d < s.dirs; ++d)
-          RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(gru ? a.dah[d] : a.da[d]),
-                                     N * GH, kPublishSentinel, st));
-      }
-      Timed tm(RNNBKT_KERNEL_STEP_BWD, fl, 0.0, st);
-      RNNBKT_HIP(launch_bwd_persistent(a, s.cell, s.bf16, B, s.dirs, st, &done));
-    }
-    for (int d = 0; d < s.dirs && !done; ++d) {
-      const int ld = l * s.dirs + d;
-      StepBwdArgs a{};
-      a.da_next = gru ? at<float>(workspace, c.dah[d]) : at<float>(workspace, c.da[d]);
-      a.whh = params + po.whh[ld];
-      a.dh_in = dh_in + d * s.H;
-      a.stash = at<float>(reserve, c.stash[ld]);
-      a.cst = gru ? nullptr : at<float>(reserve, c.cst[ld]);
-      a.hout = hout + d * s.H;
-      a.da = at<float>(workspace, c.da[d]);
-      a.dah = gru ? at<float>(workspace, c.dah[d]) : nullptr;
-      a.carry = carry;
-      a.H = s.H;
-      a.ldd = s.Htop;
-      a.ldh = s.dirs * s.H;
-      for (int k = 0; k < T; ++k) {
-        const int t = d == 0 ? T - 1 - k : k;
-        a.row0 = off[t];
-        a.rows = bs[t];
-        if (d == 0) {
-          a.next0 = t + 1 < T ? off[t + 1] : 0;
-          a.next_rows = t + 1 < T ? bs[t + 1] : 0;
-          a.prev0 = t > 0 ? off[t - 1] : 0;
-          a.prev_rows = t > 0 ? bs[t] : 0;
-        } else {
-          a.next0 = t > 0 ? off[t - 1] : 0;
-          a.next_rows = t > 0 ? bs[t] : 0;
-          a.prev0 = t + 1 < T ? off[t + 1] : 0;
-          a.prev_rows = t + 1 < T ? bs[t + 1] : 0;
-        }
-        Timed tm(RNNBKT_KERNEL_STEP_BWD, 2.0 * a.next_rows * GH * s.H, 0.0, st);
-        RNNBKT_HIP(launch_step_bwd(a, s.cell, s.bf16, st));
-      }
-    }
-    // Weight gradients reduced over every valid frame.
     for (int d = 0; d < s.dirs; ++d) {
       const int ld = l * s.dirs + d;
-      const float* dax = at<float>(workspace, c.da[d]);
-      const float* dahh = gru ? at<float>(workspace, c.dah[d]) : dax;
+      const float* dax = da_of(l, d);
+      const float* dahh = gru ? dah_of(l, d) : dax;
       RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
                       nullptr, 0, s.bf16, st, nullptr, sk));
       RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
@@ -678,11 +778,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         if (gru)
           RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, kColsumRows, cs, grads + po.bhh[ld], st));
       }
-      if (l > 0)
-        RNNBKT_HIP(gemm(dax, GH, true, params + po.wih[ld], din, false, dx, din, n, din, GH,
-                        nullptr, d > 0 ? 1 : 0, s.bf16, st));
     }
-    std::swap(dh_in, dx);
   }
   return RNNBKT_OK;
 }

@@ -119,12 +119,13 @@ hipError_t launch_step_fwd(const StepFwdArgs& a, int cell, bool bf16, hipStream_
 hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_t stream);
 
 // ---------------------------------------------------------------- persistent recurrence
-// All T steps of one layer (both directions) in one cooperative launch.
-// Tables bs/off are the device batch tables.  The buffer the steps exchange
-// (hout forward; da for the LSTM / dah for the GRU backward) must hold the
-// sentinel 0xFFFFFFFF in every element when the launch starts.  *fits
-// reports whether the grid can be resident at once (and the shape is
-// supported); when it cannot, nothing is launched.
+// All T steps of a set of recurrences (the layers of a unidirectional stack,
+// or the two directions of one layer) in one cooperative launch.  Tables
+// bs/off are the device batch tables.  Every array published during the
+// launch (hout of each unit forward; LSTM dA, GRU dAh and, when read by a
+// unit below, GRU dAx backward) must hold the sentinel 0xFFFFFFFF in every
+// element when the launch starts.  *fits reports whether the grid can be
+// resident at once and the shape is supported; if not, nothing is launched.
 constexpr int kMaxUnits = 4;
 
 // One (layer, direction) recurrence inside a forward launch.  The input
@@ -157,19 +158,37 @@ struct FwdLaunch {
   int32_t slices, rgroups;  // set by the launcher
 };
 
-struct PersistBwdArgs {
-  const float* whh[2];
-  const float* stash[2];
-  const float* cst[2];
-  const float* hout;   // layer output, direction d at column d*H
-  const float* dh_in;  // gradient w.r.t. the layer output, direction d at column d*H
-  float* da[2];
-  float* dah[2];
+// One (layer, direction) recurrence inside a backward launch.  The
+// reduction operand of a step is [gate gradient of the layer above at the
+// same frame (k_up floats; absent for the top layer) ; this layer's
+// recurrent gate gradient of the next step (G*H floats)] against
+// [W_ih of the layer above ; W_hh], restricted to this workgroup's units.
+struct BwdUnit {
+  const float* up;       // layer above: LSTM dA / GRU dAx rows [N x k_up]; nullptr = none
+  const float* wih_up;   // W_ih of the layer above [k_up x din_up]
+  const float* whh;      // [G*H x H]
+  const float* dh_in;    // plain gradient w.r.t. this unit's output (column hcol), or nullptr
+  const float* stash;    // [N x 4H]
+  const float* cst;      // LSTM [N x H]
+  const float* hout;     // layer output [N x ldh] (GRU previous state), column hcol
+  float* da;             // LSTM dA / GRU dAx [N x G*H]
+  float* dah;            // GRU dAh [N x 3H]
+  uint32_t up_bytes;     // bytes of `up`'s array (< 2^31 - 16)
+  uint32_t rec_bytes;    // bytes of the recurrent array (LSTM da, GRU dah; < 2^31 - 16)
+  int32_t k_up, din_up;  // columns of `up` and of W_ih above
+  int32_t up_published;  // 1: `up` is published by another unit of this launch
+  int32_t publish_dax;   // GRU: 1 if a unit below reads dAx during this launch
+  int32_t ld_dh, dir, hcol;
+  int32_t wg_begin;
+};
+
+struct BwdLaunch {
+  BwdUnit u[kMaxUnits];
+  int32_t nunits;
   const int32_t* bs;
   const int32_t* off;
-  uint32_t pub_bytes;  // bytes of each published da (LSTM) / dah (GRU); < 2^31 - 16
-  int32_t H, ldh, ldd, T;
-  int32_t slices, rgroups;
+  int32_t H, ldh, T;
+  int32_t slices, rgroups;  // set by the launcher
 };
 
 // Workgroups a forward launch of these units would need (0 = shape not
@@ -177,8 +196,9 @@ struct PersistBwdArgs {
 int fwd_persistent_blocks(const FwdLaunch& a, int cell, bool bf16, int B);
 hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
                                  bool* fits);
-hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
-                                 hipStream_t stream, bool* fits);
+int bwd_persistent_blocks(const BwdLaunch& a, int cell, bool bf16, int B);
+hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
+                                 bool* fits);
 // Number of waits for published values that gave up (should stay 0).
 hipError_t read_wait_timeouts(unsigned* count);
 constexpr unsigned kPublishSentinel = 0xFFFFFFFFu;

@@ -67,52 +67,8 @@ __device__ inline __amdgpu_buffer_rsrc_t published_rsrc(const float* base, unsig
 }
 constexpr unsigned kNoRow = 0x7FFFFFF0u;  // an offset past every published array
 constexpr int kDeviceScope = 16;           // sc1
-
-// A lane's share of the reduction operand of one step: for its row at byte
-// offset `row_off` (kNoRow = zero state) the chunks c = first + i*stride
-// (i < MAXC, c below nchunks), each contributing CPL consecutive floats at
-// float offset c*CH + koff.  Every round issues all loads back to back and
-// then checks them; the wave retries until no element holds the sentinel.
-// Raw bits in u[i*CPL + e].
-template <int CPL, int MAXC>
-__device__ inline void fetch_published(__amdgpu_buffer_rsrc_t rsrc, unsigned row_off, int first,
-                                       int stride, int nchunks, int CH, int koff,
-                                       unsigned (&u)[CPL * MAXC]) {
-  unsigned offs[MAXC];
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = first + i * stride;
-    offs[i] = (row_off != kNoRow && c < nchunks) ? row_off + 4u * (unsigned)(c * CH + koff) : kNoRow;
-  }
-  unsigned spins = 0;
-  for (;;) {
-#pragma unroll
-    for (int i = 0; i < MAXC; ++i)
-#pragma unroll
-      for (int v = 0; v < CPL / 4; ++v) {
-        const u4 x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, offs[i] + 16u * v, 0, kDeviceScope);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) u[i * CPL + 4 * v + e] = x[e];
-      }
-    bool ready = true;
-#pragma unroll
-    for (int j = 0; j < CPL * MAXC; ++j) ready &= u[j] != kSentinel;
-    if (__all(ready)) return;
-    if (spins == 0 && __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT) != 0u)
-      return;
-    if (++spins == (1u << 20)) {
-      if ((threadIdx.x & 63) == 0)
-        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
-}
-
 constexpr int kMaxSteps = 6144;  // batch tables kept in LDS: T_max above this is not handled here
-constexpr int kBwdUnits = 16;  // hidden units per backward workgroup
-constexpr int kMaxPerLane = 32;  // reduction-operand floats a lane holds per step
+constexpr int kBwdUnits = 16;    // hidden units per backward workgroup
 
 // Reduction-dimension chunking of one MFMA group: fp32 16x16x4 takes 4
 // k per lane group (4 groups), bf16 16x16x32 takes 8.
@@ -446,13 +402,31 @@ __device__ inline BwdIdx bwd_step(const int32_t* bs, const int32_t* off, int T, 
   return s;
 }
 
+__device__ inline BwdUnit pick_unit(const BwdLaunch& a, int ui) {
+  BwdUnit u = a.u[0];
+  if (ui == 1) u = a.u[1];
+  if (ui == 2) u = a.u[2];
+  if (ui == 3) u = a.u[3];
+  return u;
+}
+
+__device__ inline void store_or_publish(float* p, float v, bool pub) {
+  if (pub)
+    publish(p, v);
+  else
+    *p = v;
+}
+
+// Backpropagation through time of the launch's units.  Workgroup = 16 rows
+// x 16 hidden units of one unit; NW waves split the reduction dimension;
+// threads 0..255 then run the gate-gradient algebra of one (row, unit) each,
+// carrying dc*f (LSTM) or dh*z (GRU) of their row and unit in a register.
 template <int G, bool BF16, int NW, int MAXC>
-__global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
+__global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
+  constexpr int NV = CPL / 4;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  const int H = a.H;
-  const int GH = G * H;
   float* red = reinterpret_cast<float*>(smem);
   int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
   int32_t* toff = tbs + a.T;                                  // offsets [T+1]
@@ -460,102 +434,118 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
     if (i < a.T) tbs[i] = a.bs[i];
     toff[i] = a.off[i];
   }
-
-  const int per_dir = a.slices * a.rgroups;
-  const int d = blockIdx.x / per_dir;
-  const int rem = blockIdx.x % per_dir;
+  int ui = 0;
+  for (int q = 1; q < a.nunits; ++q)
+    if ((int)blockIdx.x >= a.u[q].wg_begin) ui = q;
+  const BwdUnit U = pick_unit(a, ui);
+  const int rem = blockIdx.x - U.wg_begin;
   const int slice = rem % a.slices;
   const int rg = rem / a.slices;
+  const int H = a.H;
+  const int GH = G * H;
   const int j0 = slice * kBwdUnits;
   const int r0 = rg * 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lq = lane >> 4;
+  const bool has_up = U.up != nullptr;
+  const int kup = has_up ? U.k_up : 0;
+  const int nup = kup / CH;
+  const int nch = nup + GH / CH;
 
-  // Weight block: column u is column j0 + u of W_hh (K = G*H rows); this
-  // lane feeds column lr.
-  const int nchunks = GH / CH;
-  typename WFrag<BF16>::T wreg[MAXC];
+  // Weight fragments: column lr is hidden unit j0 + lr.
+  typename WFrag<BF16>::T w[MAXC];
   {
-    const float* wcol = a.whh[d] + j0 + lr;
-    load_wfrags<BF16, MAXC>(wreg, wave, NW, nchunks, lq * CPL,
-                            [&](int k) { return wcol[(int64_t)k * H]; });
+    const int j = j0 + lr;
+    const float* wu = has_up ? U.wih_up + U.hcol + j : nullptr;
+    const float* wh = U.whh + j;
+    load_wfrags<BF16, MAXC>(w, wave, NW, nch, lq * CPL, [&](int k) {
+      return k < kup ? wu[(int64_t)k * U.din_up] : wh[(int64_t)(k - kup) * H];
+    });
   }
-  // Epilogue: threads 0..255 -> row r0 + (tid >> 4), unit j0 + (tid & 15).
+  // Gate-gradient threads: 0..255 -> row r0 + (tid >> 4), unit j0 + (tid & 15).
   const bool epi = threadIdx.x < 256;
   const int erow = r0 + ((threadIdx.x & 255) >> 4);
   const int ej = j0 + (threadIdx.x & 15);
   float carry = 0.f;
-  const float* stash = a.stash[d];
-  const float* cst = a.cst[d];
-  const float* hout = a.hout + d * H;
-  const float* dh_in = a.dh_in + d * H;
-  float* da = a.da[d];
-  float* dah = a.dah[d];
-  const float* da_next = G == 3 ? dah : da;
-  const __amdgpu_buffer_rsrc_t dsrc = published_rsrc(da_next, a.pub_bytes);
+  const float* rec = G == 3 ? U.dah : U.da;
+  const __amdgpu_buffer_rsrc_t rup = published_rsrc(has_up ? U.up : U.da, U.up_bytes);
+  const __amdgpu_buffer_rsrc_t rrec = published_rsrc(rec, U.rec_bytes);
+  const bool pub_dax = G == 4 || U.publish_dax != 0;
   __syncthreads();
 
-  BwdIdx s = bwd_step(tbs, toff, a.T, d, 0);
+  BwdIdx s = bwd_step(tbs, toff, a.T, U.dir, 0);
   for (int k = 0; k < a.T; ++k) {
-    // Next step's table entries first, so no later wait has to cover them.
     BwdIdx nx = s;
-    if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, d, k + 1);
+    if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
     const bool active = r0 < s.rows;
-    const bool erow_on = epi && active && erow < s.rows;
     // Operands that do not depend on other workgroups, loaded without
-    // branches inside the epilogue waves (inactive rows read frame 0 and are
-    // ignored) so no branch forces a wait on older loads.
-    float dhv, st0, st1, st2, st3, cc, cprev;
+    // branches inside the gate-gradient threads (inactive rows read frame
+    // 0 and are ignored).
+    float dhv = 0.f, st0, st1, st2, st3, cc, cprev;
     const int64_t f = erow < s.rows ? s.row0 + erow : 0;
     const bool has_prev = erow < s.prev_rows;
     if (epi) {
       const int64_t fp = has_prev ? s.prev0 + erow : 0;
-      dhv = dh_in[f * a.ldd + ej];
-      const float* st = stash + f * 4 * H;
+      if (U.dh_in) dhv = U.dh_in[f * U.ld_dh + U.hcol + ej];
+      const float* st = U.stash + f * 4 * H;
       st0 = st[ej];
       st1 = st[H + ej];
       st2 = st[2 * H + ej];
       st3 = st[3 * H + ej];
       if constexpr (G == 4) {
-        cc = cst[f * H + ej];
-        cprev = cst[fp * H + ej];
+        cc = U.cst[f * H + ej];
+        cprev = U.cst[fp * H + ej];
       } else {
         cc = 0.f;
-        cprev = hout[fp * a.ldh + ej];
+        cprev = U.hout[fp * a.ldh + U.hcol + ej];
       }
     }
     if (active) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
-      if (r0 < s.next_rows) {
-        const int r = r0 + lr;
-        const unsigned row_off =
-            r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
-        unsigned u[CPL * MAXC];
-        fetch_published<CPL, MAXC>(dsrc, row_off, wave, NW, nchunks, CH, lq * CPL, u);
-        acc = mma_chunks<BF16, MAXC>(u, wreg, wave, NW, nchunks);
+      const int r = r0 + lr;
+      unsigned offs[MAXC][NV];
+      bool from_up[MAXC], chk[MAXC];
+#pragma unroll
+      for (int i = 0; i < MAXC; ++i) {
+        const int c = wave + i * NW;
+        from_up[i] = c < nup;
+        chk[i] = c < nup ? U.up_published != 0 : c < nch;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int kk = c * CH + lq * CPL + 4 * v;
+          unsigned o = kNoRow;
+          if (c < nup) {
+            if (r < s.rows) o = 4u * (unsigned)((int64_t)(s.row0 + r) * kup + kk);
+          } else if (c < nch) {
+            if (r < s.next_rows) o = 4u * (unsigned)((int64_t)(s.next0 + r) * GH + (kk - kup));
+          }
+          offs[i][v] = o;
+        }
       }
+      unsigned uu[MAXC * NV * 4];
+      fetch_slots<NV, MAXC>(rup, rrec, offs, from_up, chk, uu);
+      const f4 acc = mma_chunks<BF16, MAXC>(uu, w, wave, NW, nch);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
     __syncthreads();
-    if (erow_on) {
+    if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
-      float dh_rec = 0.f;
+      float dh_red = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) dh_rec += red[w * 256 + threadIdx.x];
+      for (int w_ = 0; w_ < NW; ++w_) dh_red += red[w_ * 256 + threadIdx.x];
       if constexpr (G == 4) {
-        const float dh = dhv + (has_next ? dh_rec : 0.f);
+        const float dh = dhv + dh_red;
         const float tc = tanhf(cc);
         const float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
         const float cp = has_prev ? cprev : 0.f;
-        float* dar = da + f * GH;
+        float* dar = U.da + f * GH;
         publish(dar + ej, dc * st2 * st0 * (1.f - st0));
         publish(dar + H + ej, dc * cp * st1 * (1.f - st1));
         publish(dar + 2 * H + ej, dc * st0 * (1.f - st2 * st2));
         publish(dar + 3 * H + ej, dh * tc * st3 * (1.f - st3));
         carry = dc * st1;
       } else {
-        const float dh = dhv + (has_next ? dh_rec + carry : 0.f);
+        const float dh = dhv + dh_red + (has_next ? carry : 0.f);
         const float r = st0, z = st1, n = st2, ahn = st3;
         const float hp = has_prev ? cprev : 0.f;
         const float dn = dh * (1.f - z);
@@ -563,11 +553,11 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(PersistBwdArgs a) {
         const float dan = dn * (1.f - n * n);
         const float dar_ = dan * ahn * r * (1.f - r);
         const float daz = dz * z * (1.f - z);
-        float* dx = da + f * GH;
-        float* dhh = dah + f * GH;
-        dx[ej] = dar_;
-        dx[H + ej] = daz;
-        dx[2 * H + ej] = dan;
+        float* dx = U.da + f * GH;
+        float* dhh = U.dah + f * GH;
+        store_or_publish(dx + ej, dar_, pub_dax);
+        store_or_publish(dx + H + ej, daz, pub_dax);
+        store_or_publish(dx + 2 * H + ej, dan, pub_dax);
         publish(dhh + ej, dar_);
         publish(dhh + H + ej, daz);
         publish(dhh + 2 * H + ej, dan * r);
@@ -622,46 +612,6 @@ hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem
     return hipLaunchKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
   return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
 }
-
-// Waves per workgroup and chunks per wave for a K-long reduction: the
-// fewest waves (4 or 16) for which a wave's share fits a lane's budget of
-// kMaxPerLane floats; MAXC is the chunks a wave handles rounded up to a
-// power of two.  Returns false if K is too long for these kernels.
-bool split_for(int K, bool bf16, int* nw, int* maxc) {
-  const int ch = bf16 ? 32 : 16, cpl = bf16 ? 8 : 4;
-  const int nchunks = K / ch;
-  for (int w : {4, 16}) {
-    const int per = (nchunks + w - 1) / w;
-    int m = 1;
-    while (m < per) m *= 2;
-    if (m * cpl <= kMaxPerLane) {
-      *nw = w;
-      *maxc = m;
-      return true;
-    }
-  }
-  return false;
-}
-
-#define RNNBKT_PICK(KERN, G_, BF_)                                                   \
-  switch (nw * 100 + maxc) {                                                         \
-    case 401: return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 1>);             \
-    case 402: return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 2>);             \
-    case 404: return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 4>);             \
-    case 1601: return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 1>);           \
-    case 1602: return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 2>);           \
-    case 1604: return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 4>);           \
-  }                                                                                  \
-  if constexpr (!BF_) {                                                              \
-    if (nw * 100 + maxc == 408) return reinterpret_cast<const void*>(KERN<G_, BF_, 4, 8>);   \
-    if (nw * 100 + maxc == 1608) return reinterpret_cast<const void*>(KERN<G_, BF_, 16, 8>); \
-  }                                                                                  \
-  return nullptr;
-
-template <int G, bool BF16>
-const void* bwd_kernel(int nw, int maxc) { RNNBKT_PICK(k_bwd_persistent, G, BF16) }
-
-#undef RNNBKT_PICK
 
 }  // namespace
 
@@ -745,23 +695,87 @@ hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStr
   return coop_launch(p.kernel, p.blocks, 256, p.shmem, &a, st, fits);
 }
 
-hipError_t launch_bwd_persistent(PersistBwdArgs a, int cell, bool bf16, int B, int dirs,
-                                 hipStream_t st, bool* fits) {
-  *fits = false;
+namespace {
+
+template <int G, bool BF16, int NW>
+const void* bwd_kernel_nw(int maxc) {
+  switch (maxc) {
+    case 1: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 1>);
+    case 2: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 2>);
+    case 4: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 4>);
+    case 8: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 8>);
+  }
+  if constexpr (!BF16)
+    if (maxc == 16) return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 16>);
+  return nullptr;
+}
+
+const void* bwd_kernel(int cell, bool bf16, int nw, int maxc) {
+  if (cell == RNNBKT_CELL_LSTM) {
+    if (bf16) return nw == 4 ? bwd_kernel_nw<4, true, 4>(maxc) : bwd_kernel_nw<4, true, 16>(maxc);
+    return nw == 4 ? bwd_kernel_nw<4, false, 4>(maxc) : bwd_kernel_nw<4, false, 16>(maxc);
+  }
+  if (bf16) return nw == 4 ? bwd_kernel_nw<3, true, 4>(maxc) : bwd_kernel_nw<3, true, 16>(maxc);
+  return nw == 4 ? bwd_kernel_nw<3, false, 4>(maxc) : bwd_kernel_nw<3, false, 16>(maxc);
+}
+
+struct BwdPlan {
+  const void* kernel;
+  int nw, maxc, blocks;
+  size_t shmem;
+};
+
+// Waves: 4, or 16 when a wave's share of the reduction would exceed the
+// per-lane budget (16 chunks fp32, 8 chunks bf16).
+BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
+  BwdPlan p{nullptr, 0, 0, 0, 0};
+  const int ch = bf16 ? 32 : 16;
   const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
-  int nw = 0, maxc = 0;
-  if (!split_for(G * a.H, bf16, &nw, &maxc) || a.H % kBwdUnits != 0) return hipSuccess;
-  if (a.pub_bytes == 0 || a.pub_bytes >= kNoRow) return hipSuccess;
+  if (a.T > kMaxSteps || a.nunits < 1 || a.nunits > kMaxUnits || a.H % kBwdUnits != 0) return p;
+  if ((G * a.H) % ch != 0) return p;
+  int nch = 0;
+  for (int q = 0; q < a.nunits; ++q) {
+    const BwdUnit& u = a.u[q];
+    if (u.rec_bytes >= kNoRow || (u.up && (u.k_up % ch != 0 || u.up_bytes >= kNoRow))) return p;
+    nch = std::max(nch, (u.up ? u.k_up / ch : 0) + G * a.H / ch);
+  }
+  const int cap = bf16 ? 8 : 16;
+  for (int nw : {4, 16}) {
+    const int per = (nch + nw - 1) / nw;
+    int m = 1;
+    while (m < per) m *= 2;
+    if (m <= cap) {
+      p.nw = nw;
+      p.maxc = m;
+      break;
+    }
+  }
+  if (p.nw == 0) return p;
+  p.blocks = a.nunits * (a.H / kBwdUnits) * ((B + 15) / 16);
+  p.shmem = sizeof(float) * p.nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc);
+  return p;
+}
+
+}  // namespace
+
+int bwd_persistent_blocks(const BwdLaunch& a, int cell, bool bf16, int B) {
+  const BwdPlan p = plan_bwd(a, cell, bf16, B);
+  if (!p.kernel) return 0;
+  if (p.blocks > max_coresident(p.kernel, 64 * p.nw, p.shmem)) return 0;
+  return p.blocks;
+}
+
+hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStream_t st,
+                                 bool* fits) {
+  *fits = false;
+  const BwdPlan p = plan_bwd(a, cell, bf16, B);
+  if (!p.kernel) return hipSuccess;
   a.slices = a.H / kBwdUnits;
   a.rgroups = (B + 15) / 16;
-  const int blocks = dirs * a.slices * a.rgroups;
-  if (a.T > kMaxSteps) return hipSuccess;
-  const size_t sh = sizeof(float) * nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
-  const void* k = cell == RNNBKT_CELL_LSTM
-                      ? (bf16 ? bwd_kernel<4, true>(nw, maxc) : bwd_kernel<4, false>(nw, maxc))
-                      : (bf16 ? bwd_kernel<3, true>(nw, maxc) : bwd_kernel<3, false>(nw, maxc));
-  if (!k) return hipSuccess;
-  return coop_launch(k, blocks, 64 * nw, sh, &a, st, fits);
+  const int per_unit = a.slices * a.rgroups;
+  for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
+  return coop_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
 }
 
 hipError_t read_wait_timeouts(unsigned* count) {
