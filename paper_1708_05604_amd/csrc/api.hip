@@ -104,7 +104,9 @@ SplitK choose_splitk(int64_t M, int64_t N, int64_t K) {
   return SplitK{(int)S, (int)kps};
 }
 
-constexpr int64_t kColsumRows = 64;
+// Column sums: rows are cut into at most kColsumSplits slices.
+constexpr int64_t kColsumSplits = 64;
+int64_t colsum_rows(int64_t N) { return std::max<int64_t>(1, (N + kColsumSplits - 1) / kColsumSplits); }
 
 // Byte offsets of every buffer a batch uses.
 struct Carve {
@@ -119,6 +121,7 @@ struct Carve {
   // workspace (backward)
   size_t dha, dhb, carry, splitk, colsum;
   std::vector<size_t> da, dah;  // per layer*dirs
+  std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
 
   size_t ws_bwd;
   size_t workspace;
@@ -173,8 +176,13 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     need(GH, s.H, N);
   }
   c.splitk = take(sizeof(float) * std::max<size_t>(sk, 1));
-  const int64_t cs_splits = (N + kColsumRows - 1) / kColsumRows;
+  const int64_t cs_splits = (N + colsum_rows(N) - 1) / colsum_rows(N);
   c.colsum = take(sizeof(float) * cs_splits * std::max<int64_t>(GH, s.C));
+  const int rgroups = (B + 15) / 16;
+  for (int q = 0; q < s.L * s.dirs; ++q) {
+    c.bpart.push_back(take(sizeof(float) * rgroups * GH));
+    c.bpart_h.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * rgroups * GH) : 0);
+  }
   c.ws_bwd = pos;
   c.workspace = std::max(c.ws_fwd, c.ws_bwd);
   return c;
@@ -589,7 +597,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                   nullptr, 0, s.bf16, st, nullptr, sk));
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, kColsumRows, cs, grads + po.bout, st));
+    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), cs, grads + po.bout, st));
   }
 
   auto da_of = [&](int l, int d) { return at<float>(workspace, c.da[l * s.dirs + d]); };
@@ -618,6 +626,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     u.hout = at<float>(reserve, c.hout[l]);
     u.da = da_of(l, d);
     u.dah = dah_of(l, d);
+    u.bias_part = at<float>(workspace, c.bpart[ld]);
+    u.bias_part_h = gru ? at<float>(workspace, c.bpart_h[ld]) : nullptr;
     u.rec_bytes = rec_bytes;
     u.publish_dax = publish_dax ? 1 : 0;
     u.dir = d;
@@ -774,9 +784,19 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                       s.H, GH, s.H, n, nullptr, 0, s.bf16, st, d == 0 ? pf : pr, sk));
       {
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-        RNNBKT_HIP(launch_colsum(dax, N, GH, GH, kColsumRows, cs, grads + po.b[ld], st));
-        if (gru)
-          RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, kColsumRows, cs, grads + po.bhh[ld], st));
+        if (persistent) {
+          // The recurrence kernel left one partial per row group.
+          const int rgroups = (B + 15) / 16;
+          RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.bpart[ld]), rgroups, 1, GH,
+                                          grads + po.b[ld], GH, nullptr, 0, st));
+          if (gru)
+            RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.bpart_h[ld]), rgroups, 1, GH,
+                                            grads + po.bhh[ld], GH, nullptr, 0, st));
+        } else {
+          RNNBKT_HIP(launch_colsum(dax, N, GH, GH, colsum_rows(N), cs, grads + po.b[ld], st));
+          if (gru)
+            RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, colsum_rows(N), cs, grads + po.bhh[ld], st));
+        }
       }
     }
   }

@@ -203,10 +203,21 @@ __global__ void k_splitk_reduce(const float* __restrict__ partial, int S, int M,
                                 float* __restrict__ out, int64_t ldc,
                                 const float* __restrict__ bias, int accumulate) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)M * N) return;
+  const int64_t MN = (int64_t)M * N;
+  if (idx >= MN) return;
   const int m = (int)(idx / N), n = (int)(idx % N);
-  float v = 0.f;
-  for (int s = 0; s < S; ++s) v += partial[(int64_t)s * M * N + idx];
+  // Four independent partial sums keep several loads in flight; the folding
+  // order is fixed, so the result is deterministic.
+  float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
+  int s = 0;
+  for (; s + 4 <= S; s += 4) {
+    v0 += partial[(int64_t)s * MN + idx];
+    v1 += partial[(int64_t)(s + 1) * MN + idx];
+    v2 += partial[(int64_t)(s + 2) * MN + idx];
+    v3 += partial[(int64_t)(s + 3) * MN + idx];
+  }
+  for (; s < S; ++s) v0 += partial[(int64_t)s * MN + idx];
+  float v = (v0 + v1) + (v2 + v3);
   if (bias) v += bias[n];
   float* c = out + (int64_t)m * ldc + n;
   if (accumulate) v += *c;
@@ -221,9 +232,16 @@ __global__ void k_colsum_partial(const float* __restrict__ A, int64_t rows, int 
   if (c >= cols) return;
   const int64_t r0 = (int64_t)s * rows_per_split;
   const int64_t r1 = min(rows, r0 + rows_per_split);
-  float v = 0.f;
-  for (int64_t r = r0; r < r1; ++r) v += A[r * lda + c];
-  partial[(int64_t)s * cols + c] = v;
+  float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
+  int64_t r = r0;
+  for (; r + 4 <= r1; r += 4) {
+    v0 += A[r * lda + c];
+    v1 += A[(r + 1) * lda + c];
+    v2 += A[(r + 2) * lda + c];
+    v3 += A[(r + 3) * lda + c];
+  }
+  for (; r < r1; ++r) v0 += A[r * lda + c];
+  partial[(int64_t)s * cols + c] = (v0 + v1) + (v2 + v3);
 }
 
 }  // namespace

@@ -173,6 +173,8 @@ struct BwdUnit {
   const float* hout;     // layer output [N x ldh] (GRU previous state), column hcol
   float* da;             // LSTM dA / GRU dAx [N x G*H]
   float* dah;            // GRU dAh [N x 3H]
+  float* bias_part;      // [rgroups x G*H]: per row group, sum over frames of dA / dAx
+  float* bias_part_h;    // GRU: [rgroups x 3H] sums of dAh
   uint32_t up_bytes;     // bytes of `up`'s array (< 2^31 - 16)
   uint32_t rec_bytes;    // bytes of the recurrent array (LSTM da, GRU dah; < 2^31 - 16)
   int32_t k_up, din_up;  // columns of `up` and of W_ih above

@@ -1,5 +1,7 @@
-// Whole-sequence recurrence of one LSTM/GRU layer (both directions) in one
-// launch, forward and backward through time.
+// Whole-sequence recurrences of LSTM/GRU layers in one launch, forward and
+// backward through time: all layers of a unidirectional stack (each layer
+// consuming the one below as it is published), or both directions of one
+// bidirectional layer.
 //
 // A launch keeps every workgroup resident (cooperative launch) and walks
 // the T steps of the batch itself.  Each workgroup owns a fixed block of 16
@@ -11,13 +13,18 @@
 //   - per-step operands that do not depend on other workgroups (the input
 //     projection row, the saved gate activations) are fetched early.
 //
+// Each step reduces over two segments: first the input part (the layer
+// input row forward, the gate gradient of the layer above backward), which
+// does not depend on this recurrence and is fetched one step ahead, then the
+// recurrent part, which other workgroups publish during the previous step.
+//
 // Exchange between workgroups without a grid barrier: the buffer a step
 // publishes (h forward, the recurrent gate gradient backward) is filled
 // with a sentinel bit pattern before the launch; every element of it is
 // written exactly once during the launch with a relaxed device-scope atomic
 // store (a value equal to the sentinel is replaced by the canonical NaN), and
-// a reader polls its elements with relaxed device-scope atomic loads until
-// none holds the sentinel.  Single-location coherence of atomics is all this
+// a reader polls its elements with device-scope loads until none holds the
+// sentinel.  Single-location coherence of atomics is all this
 // needs: no fence, no cache write-back or invalidation, and a workgroup
 // waits only for the rows it reads (sequences are independent).  Polls are
 // bounded; after a timeout the wait gives up, counts it (reported by
@@ -99,18 +106,89 @@ struct WFrag<true> {
   using T = bf8;
 };
 
-// acc += A(16 x K) . W(K x 16) over the chunks held in u (see fetch_published)
-// with the lane's weight fragments w (one per chunk slot).
-template <bool BF16, int MAXC>
-__device__ inline f4 mma_chunks(const unsigned (&u)[Chunk<BF16>::CPL * MAXC],
-                                const typename WFrag<BF16>::T (&w)[MAXC], int first, int stride,
-                                int nchunks) {
+// The lane's slots of one segment: slot i is chunk c = first + i*stride of
+// the segment (used while c < nchunks).
+struct Slots {
+  int first, stride, nchunks, koff;
+};
+
+// Loads the lane's weight fragments of one segment: wk(k) returns the
+// weight for segment-local reduction index k of this lane's column.
+template <bool BF16, int MAXC, typename F>
+__device__ inline void load_wfrags(typename WFrag<BF16>::T (&w)[MAXC], const Slots& sl, F wk) {
+  constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
-  f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
-    const int c = first + i * stride;
-    if (c >= nchunks) break;
+    const int c = sl.first + i * sl.stride;
+#pragma unroll
+    for (int e = 0; e < CPL; ++e) {
+      const float v = c < sl.nchunks ? wk(c * CH + sl.koff + e) : 0.f;
+      if constexpr (BF16)
+        w[i][e] = (__bf16)v;
+      else
+        w[i][e] = v;
+    }
+  }
+}
+
+// Issues the lane's loads of one segment: piece v of slot i is read at byte
+// offset row_off + 4*(c*CH + koff + 4v) of the array behind `r` when the row
+// exists (row_off != kNoRow) and the piece starts below klim; other pieces
+// read zero.
+template <bool BF16, int MAXC>
+__device__ inline void issue_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
+                                     int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC]) {
+  constexpr int CH = Chunk<BF16>::CH;
+  constexpr int NV = Chunk<BF16>::CPL / 4;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = sl.first + i * sl.stride;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int kk = c * CH + sl.koff + 4 * v;
+      const unsigned o =
+          (row_off != kNoRow && c < sl.nchunks && kk < klim) ? row_off + 4u * (unsigned)kk : kNoRow;
+      const u4 x = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, kDeviceScope);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) u[(i * NV + v) * 4 + e] = x[e];
+    }
+  }
+}
+
+// Re-reads the segment until no element holds the sentinel (wave-uniform).
+template <bool BF16, int MAXC>
+__device__ inline void settle_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
+                                      int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC]) {
+  constexpr int NE = Chunk<BF16>::CPL * MAXC;
+  unsigned spins = 0;
+  for (;;) {
+    bool ready = true;
+#pragma unroll
+    for (int j = 0; j < NE; ++j) ready &= u[j] != kSentinel;
+    if (__all(ready)) return;
+    if (spins == 0 && __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT) != 0u)
+      return;
+    if (++spins == (1u << 20)) {
+      if ((threadIdx.x & 63) == 0)
+        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(1);
+    issue_segment<BF16, MAXC>(r, row_off, sl, klim, u);
+  }
+}
+
+// acc += (16 rows x segment) . (segment x 16 columns) over the lane's slots.
+template <bool BF16, int MAXC>
+__device__ inline void mma_segment(f4& acc, const unsigned (&u)[Chunk<BF16>::CPL * MAXC],
+                                   const typename WFrag<BF16>::T (&w)[MAXC], const Slots& sl) {
+  constexpr int CPL = Chunk<BF16>::CPL;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = sl.first + i * sl.stride;
+    if (c >= sl.nchunks) break;
     if constexpr (BF16) {
       bf8 av;
 #pragma unroll
@@ -121,28 +199,6 @@ __device__ inline f4 mma_chunks(const unsigned (&u)[Chunk<BF16>::CPL * MAXC],
       for (int e = 0; e < CPL; ++e)
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(u[i * CPL + e]), w[i][e], acc,
                                                    0, 0, 0);
-    }
-  }
-  return acc;
-}
-
-// Loads the lane's weight fragments: wk(k) returns the weight for reduction
-// index k of this lane's column (0 for padding columns).
-template <bool BF16, int MAXC, typename F>
-__device__ inline void load_wfrags(typename WFrag<BF16>::T (&w)[MAXC], int first, int stride,
-                                   int nchunks, int koff, F wk) {
-  constexpr int CH = Chunk<BF16>::CH;
-  constexpr int CPL = Chunk<BF16>::CPL;
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int c = first + i * stride;
-#pragma unroll
-    for (int e = 0; e < CPL; ++e) {
-      const float v = c < nchunks ? wk(c * CH + koff + e) : 0.f;
-      if constexpr (BF16)
-        w[i][e] = (__bf16)v;
-      else
-        w[i][e] = v;
     }
   }
 }
@@ -167,46 +223,6 @@ __device__ inline StepIdx fwd_step(const int32_t* bs, const int32_t* off, int T,
   return s;
 }
 
-// Reads the lane's operand slots of one step: slot i (chunk c = first +
-// i*stride) holds NV 128-bit pieces at byte offsets offs[i][v] in the input
-// array (from_in[i]) or in the output array; slots with chk[i] are published
-// values and are re-read until none holds the sentinel.  from_in / chk are
-// uniform across the wave.
-template <int NV, int MAXC>
-__device__ inline void fetch_slots(__amdgpu_buffer_rsrc_t rin, __amdgpu_buffer_rsrc_t rout,
-                                   const unsigned (&offs)[MAXC][NV], const bool (&from_in)[MAXC],
-                                   const bool (&chk)[MAXC], unsigned (&u)[MAXC * NV * 4]) {
-  unsigned spins = 0;
-  for (;;) {
-#pragma unroll
-    for (int i = 0; i < MAXC; ++i)
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const u4 x = from_in[i]
-                         ? __builtin_amdgcn_raw_buffer_load_b128(rin, offs[i][v], 0, kDeviceScope)
-                         : __builtin_amdgcn_raw_buffer_load_b128(rout, offs[i][v], 0, kDeviceScope);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) u[(i * NV + v) * 4 + e] = x[e];
-      }
-    bool ready = true;
-#pragma unroll
-    for (int i = 0; i < MAXC; ++i)
-      if (chk[i])
-#pragma unroll
-        for (int e = 0; e < NV * 4; ++e) ready &= u[i * NV * 4 + e] != kSentinel;
-    if (__all(ready)) return;
-    if (spins == 0 && __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT) != 0u)
-      return;
-    if (++spins == (1u << 20)) {
-      if ((threadIdx.x & 63) == 0)
-        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
-}
-
 // Copies unit `ui` out of the kernel arguments without dynamic indexing.
 __device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
   FwdUnit u = a.u[0];
@@ -216,25 +232,30 @@ __device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
   return u;
 }
 
+// Copies the batch tables into LDS.
+__device__ inline void load_tables(const int32_t* bs, const int32_t* off, int T, int32_t* tbs,
+                                   int32_t* toff) {
+  for (int i = threadIdx.x; i <= T; i += blockDim.x) {
+    if (i < T) tbs[i] = bs[i];
+    toff[i] = off[i];
+  }
+}
+
 // Forward recurrence of the launch's units.  Workgroup = 16 rows x 4*NT
 // hidden units of one unit; column block nt holds, for its 4 units, the
 // LSTM gates (i, f, g, o) or the GRU groups (r, z, n from the input, n from
 // the state), so one MFMA tile per block yields every pre-activation a
-// unit's update needs.  NW waves split the reduction dimension; waves
+// unit's update needs.  NW waves split each segment's reduction; waves
 // 0..NT-1 then run the state update of one column block each.
 template <int G, bool BF16, int NW, int MAXC, int NT>
 __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
-  constexpr int NV = CPL / 4;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   float* red = reinterpret_cast<float*>(smem);                     // [NW][NT][256]
   int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * NT * 256);  // batch sizes [T]
   int32_t* toff = tbs + a.T;                                       // offsets [T+1]
-  for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
-    if (i < a.T) tbs[i] = a.bs[i];
-    toff[i] = a.off[i];
-  }
+  load_tables(a.bs, a.off, a.T, tbs, toff);
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
     if ((int)blockIdx.x >= a.u[q].wg_begin) ui = q;
@@ -245,35 +266,29 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   const int H = a.H;
   const int j0 = slice * 4 * NT;
   const int r0 = rg * 16;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  // Wave-uniform: the per-slot tests below then become scalar branches.  An
+  // MFMA placed in a lane-masked region still reads every lane, so a slot
+  // must be skipped by the whole wave, never by masking.
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lr = lane & 15, lq = lane >> 4;
-  const int kin_pad = (U.kin + CH - 1) / CH * CH;
-  const int nin = kin_pad / CH;
-  const int nch = nin + H / CH;
+  const Slots sin{wave, NW, (U.kin + CH - 1) / CH, lq * CPL};
+  const Slots srec{wave, NW, H / CH, lq * CPL};
 
   // Weight fragments: this lane feeds column lr of every column block.
-  typename WFrag<BF16>::T w[NT][MAXC];
+  typename WFrag<BF16>::T win[NT][MAXC], wrec[NT][MAXC];
   {
     const int grp = lr >> 2, uu = lr & 3;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int j = j0 + 4 * nt + uu;
-      // gate row of W_ih / W_hh feeding this column for the input part and
-      // the state part (-1 = none)
-      int gi, gh;
-      if (G == 4) {
-        gi = grp;
-        gh = grp;
-      } else {
-        gi = grp == 3 ? -1 : grp;
-        gh = grp == 2 ? -1 : (grp == 3 ? 2 : grp);
-      }
+      // gate row of W_ih / W_hh feeding this column (-1 = none)
+      const int gi = G == 4 ? grp : (grp == 3 ? -1 : grp);
+      const int gh = G == 4 ? grp : (grp == 2 ? -1 : (grp == 3 ? 2 : grp));
       const float* wi = gi >= 0 ? U.wih + (int64_t)(gi * H + j) * U.kin : nullptr;
       const float* wh = gh >= 0 ? U.whh + (int64_t)(gh * H + j) * H : nullptr;
-      load_wfrags<BF16, MAXC>(w[nt], wave, NW, nch, lq * CPL, [&](int k) {
-        if (k < kin_pad) return (wi && k < U.kin) ? wi[k] : 0.f;
-        return wh ? wh[k - kin_pad] : 0.f;
-      });
+      load_wfrags<BF16, MAXC>(win[nt], sin, [&](int k) { return (wi && k < U.kin) ? wi[k] : 0.f; });
+      load_wfrags<BF16, MAXC>(wrec[nt], srec, [&](int k) { return wh ? wh[k] : 0.f; });
     }
   }
   // State-update lanes: wave nt < NT owns row r0 + (lane >> 2), unit
@@ -293,45 +308,43 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   float c_state = 0.f, h_state = 0.f;
   const __amdgpu_buffer_rsrc_t rin = published_rsrc(U.in, U.in_bytes);
   const __amdgpu_buffer_rsrc_t rout = published_rsrc(U.hout, U.out_bytes);
+  const int r = r0 + lr;
   __syncthreads();
 
+  auto in_off = [&](const StepIdx& q) {
+    return r < q.rows ? 4u * (unsigned)((int64_t)(q.row0 + r) * U.ld_in) : kNoRow;
+  };
   StepIdx s = fwd_step(tbs, toff, a.T, U.dir, 0);
+  unsigned uin[CPL * MAXC];
+  issue_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin);
   for (int k = 0; k < a.T; ++k) {
     StepIdx nx = s;
     if (k + 1 < a.T) nx = fwd_step(tbs, toff, a.T, U.dir, k + 1);
     const bool active = r0 < s.rows;
     if (active) {
-      const int r = r0 + lr;
-      unsigned offs[MAXC][NV];
-      bool from_in[MAXC], chk[MAXC];
+      f4 acc[NT];
 #pragma unroll
-      for (int i = 0; i < MAXC; ++i) {
-        const int c = wave + i * NW;
-        from_in[i] = c < nin;
-        chk[i] = c < nin ? U.in_published != 0 : c < nch;
+      for (int nt = 0; nt < NT; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
+      // Input part (fetched one step ahead; a published input may still be
+      // arriving).
+      if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin);
 #pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int kk = c * CH + lq * CPL + 4 * v;
-          unsigned o = kNoRow;
-          if (c < nin) {
-            if (r < s.rows && kk < U.kin)
-              o = 4u * (unsigned)((int64_t)(s.row0 + r) * U.ld_in + kk);
-          } else if (c < nch) {
-            if (r < s.prev_rows)
-              o = 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + U.hcol + (kk - kin_pad));
-          }
-          offs[i][v] = o;
-        }
-      }
-      unsigned uu[MAXC * NV * 4];
-      fetch_slots<NV, MAXC>(rin, rout, offs, from_in, chk, uu);
+      for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
+      // Recurrent part.
+      const unsigned roff =
+          r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + U.hcol) : kNoRow;
+      unsigned urec[CPL * MAXC];
+      issue_segment<BF16, MAXC>(rout, roff, srec, H, urec);
+      settle_segment<BF16, MAXC>(rout, roff, srec, H, urec);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const f4 acc = mma_chunks<BF16, MAXC>(uu, w[nt], wave, NW, nch);
+        mma_segment<BF16, MAXC>(acc[nt], urec, wrec[nt], srec);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) red[(wave * NT + nt) * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
+        for (int q = 0; q < 4; ++q)
+          red[(wave * NT + nt) * 256 + (lq * 4 + q) * 16 + lr] = acc[nt][q];
       }
     }
+    if (k + 1 < a.T) issue_segment<BF16, MAXC>(rin, in_off(nx), sin, U.kin, uin);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const int rr = lane >> 2, u4_ = lane & 3;
@@ -354,6 +367,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
         const float cp = has_prev ? c_state : 0.f;
         c_state = fg * cp + ig * gg;
         h_state = og * tanhf(c_state);
+        publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
         st[ej] = ig;
         st[H + ej] = fg;
         st[2 * H + ej] = gg;
@@ -366,12 +380,12 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
         const float n = tanhf(sg[2] + bi[2] + rg_ * ahn);
         const float hp = has_prev ? h_state : 0.f;
         h_state = (1.f - z) * n + z * hp;
+        publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
         st[ej] = rg_;
         st[H + ej] = z;
         st[2 * H + ej] = n;
         st[3 * H + ej] = ahn;
       }
-      publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
     }
     s = nx;
     __syncthreads();  // red is rewritten by the next step
@@ -418,22 +432,19 @@ __device__ inline void store_or_publish(float* p, float v, bool pub) {
 }
 
 // Backpropagation through time of the launch's units.  Workgroup = 16 rows
-// x 16 hidden units of one unit; NW waves split the reduction dimension;
+// x 16 hidden units of one unit; NW waves split each segment's reduction;
 // threads 0..255 then run the gate-gradient algebra of one (row, unit) each,
-// carrying dc*f (LSTM) or dh*z (GRU) of their row and unit in a register.
+// carrying dc*f (LSTM) or dh*z (GRU) of their row and unit in a register and
+// summing the unit's gate gradients over the steps for the bias gradients.
 template <int G, bool BF16, int NW, int MAXC>
 __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
-  constexpr int NV = CPL / 4;
   extern __shared__ __attribute__((aligned(16))) char smem[];
-  float* red = reinterpret_cast<float*>(smem);
-  int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * 256);  // batch sizes [T]
-  int32_t* toff = tbs + a.T;                                  // offsets [T+1]
-  for (int i = threadIdx.x; i <= a.T; i += blockDim.x) {
-    if (i < a.T) tbs[i] = a.bs[i];
-    toff[i] = a.off[i];
-  }
+  float* red = reinterpret_cast<float*>(smem);                // [max(NW, 8)][256]
+  int32_t* tbs = reinterpret_cast<int32_t*>(red + (NW < 8 ? 8 : NW) * 256);
+  int32_t* toff = tbs + a.T;
+  load_tables(a.bs, a.off, a.T, tbs, toff);
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
     if ((int)blockIdx.x >= a.u[q].wg_begin) ui = q;
@@ -445,35 +456,46 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   const int GH = G * H;
   const int j0 = slice * kBwdUnits;
   const int r0 = rg * 16;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  // Wave-uniform: the per-slot tests below then become scalar branches.  An
+  // MFMA placed in a lane-masked region still reads every lane, so a slot
+  // must be skipped by the whole wave, never by masking.
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lr = lane & 15, lq = lane >> 4;
   const bool has_up = U.up != nullptr;
   const int kup = has_up ? U.k_up : 0;
-  const int nup = kup / CH;
-  const int nch = nup + GH / CH;
+  const Slots sup{wave, NW, kup / CH, lq * CPL};
+  const Slots srec{wave, NW, GH / CH, lq * CPL};
 
   // Weight fragments: column lr is hidden unit j0 + lr.
-  typename WFrag<BF16>::T w[MAXC];
+  typename WFrag<BF16>::T wup[MAXC], wrec[MAXC];
   {
     const int j = j0 + lr;
     const float* wu = has_up ? U.wih_up + U.hcol + j : nullptr;
     const float* wh = U.whh + j;
-    load_wfrags<BF16, MAXC>(w, wave, NW, nch, lq * CPL, [&](int k) {
-      return k < kup ? wu[(int64_t)k * U.din_up] : wh[(int64_t)(k - kup) * H];
-    });
+    load_wfrags<BF16, MAXC>(wup, sup, [&](int k) { return wu ? wu[(int64_t)k * U.din_up] : 0.f; });
+    load_wfrags<BF16, MAXC>(wrec, srec, [&](int k) { return wh[(int64_t)k * H]; });
   }
   // Gate-gradient threads: 0..255 -> row r0 + (tid >> 4), unit j0 + (tid & 15).
   const bool epi = threadIdx.x < 256;
   const int erow = r0 + ((threadIdx.x & 255) >> 4);
   const int ej = j0 + (threadIdx.x & 15);
   float carry = 0.f;
+  float bsum[4] = {0.f, 0.f, 0.f, 0.f};  // sum over steps of this (row, unit)'s dA (LSTM) / dAx (GRU)
+  float bsumh[3] = {0.f, 0.f, 0.f};      // GRU: sum of dAh
   const float* rec = G == 3 ? U.dah : U.da;
-  const __amdgpu_buffer_rsrc_t rup = published_rsrc(has_up ? U.up : U.da, U.up_bytes);
+  const __amdgpu_buffer_rsrc_t rup = published_rsrc(has_up ? U.up : U.da, has_up ? U.up_bytes : 0u);
   const __amdgpu_buffer_rsrc_t rrec = published_rsrc(rec, U.rec_bytes);
   const bool pub_dax = G == 4 || U.publish_dax != 0;
+  const int r = r0 + lr;
   __syncthreads();
 
+  auto up_off = [&](const BwdIdx& q) {
+    return (has_up && r < q.rows) ? 4u * (unsigned)((int64_t)(q.row0 + r) * kup) : kNoRow;
+  };
   BwdIdx s = bwd_step(tbs, toff, a.T, U.dir, 0);
+  unsigned uup[CPL * MAXC];
+  issue_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
   for (int k = 0; k < a.T; ++k) {
     BwdIdx nx = s;
     if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
@@ -501,32 +523,21 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       }
     }
     if (active) {
-      const int r = r0 + lr;
-      unsigned offs[MAXC][NV];
-      bool from_up[MAXC], chk[MAXC];
-#pragma unroll
-      for (int i = 0; i < MAXC; ++i) {
-        const int c = wave + i * NW;
-        from_up[i] = c < nup;
-        chk[i] = c < nup ? U.up_published != 0 : c < nch;
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int kk = c * CH + lq * CPL + 4 * v;
-          unsigned o = kNoRow;
-          if (c < nup) {
-            if (r < s.rows) o = 4u * (unsigned)((int64_t)(s.row0 + r) * kup + kk);
-          } else if (c < nch) {
-            if (r < s.next_rows) o = 4u * (unsigned)((int64_t)(s.next0 + r) * GH + (kk - kup));
-          }
-          offs[i][v] = o;
-        }
-      }
-      unsigned uu[MAXC * NV * 4];
-      fetch_slots<NV, MAXC>(rup, rrec, offs, from_up, chk, uu);
-      const f4 acc = mma_chunks<BF16, MAXC>(uu, w, wave, NW, nch);
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+      // Gradient arriving from the layer above (fetched one step ahead).
+      if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
+      mma_segment<BF16, MAXC>(acc, uup, wup, sup);
+      // Recurrent part.
+      const unsigned roff =
+          r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
+      unsigned urec[CPL * MAXC];
+      issue_segment<BF16, MAXC>(rrec, roff, srec, GH, urec);
+      settle_segment<BF16, MAXC>(rrec, roff, srec, GH, urec);
+      mma_segment<BF16, MAXC>(acc, urec, wrec, srec);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
+    if (k + 1 < a.T) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
@@ -538,34 +549,70 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
         const float tc = tanhf(cc);
         const float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
         const float cp = has_prev ? cprev : 0.f;
+        const float di = dc * st2 * st0 * (1.f - st0);
+        const float df = dc * cp * st1 * (1.f - st1);
+        const float dg = dc * st0 * (1.f - st2 * st2);
+        const float dout = dh * tc * st3 * (1.f - st3);
         float* dar = U.da + f * GH;
-        publish(dar + ej, dc * st2 * st0 * (1.f - st0));
-        publish(dar + H + ej, dc * cp * st1 * (1.f - st1));
-        publish(dar + 2 * H + ej, dc * st0 * (1.f - st2 * st2));
-        publish(dar + 3 * H + ej, dh * tc * st3 * (1.f - st3));
+        publish(dar + ej, di);
+        publish(dar + H + ej, df);
+        publish(dar + 2 * H + ej, dg);
+        publish(dar + 3 * H + ej, dout);
         carry = dc * st1;
+        bsum[0] += di;
+        bsum[1] += df;
+        bsum[2] += dg;
+        bsum[3] += dout;
       } else {
         const float dh = dhv + dh_red + (has_next ? carry : 0.f);
-        const float r = st0, z = st1, n = st2, ahn = st3;
+        const float rr = st0, z = st1, n = st2, ahn = st3;
         const float hp = has_prev ? cprev : 0.f;
         const float dn = dh * (1.f - z);
         const float dz = dh * (hp - n);
         const float dan = dn * (1.f - n * n);
-        const float dar_ = dan * ahn * r * (1.f - r);
+        const float dar_ = dan * ahn * rr * (1.f - rr);
         const float daz = dz * z * (1.f - z);
-        float* dx = U.da + f * GH;
+        const float dhn = dan * rr;
         float* dhh = U.dah + f * GH;
+        publish(dhh + ej, dar_);
+        publish(dhh + H + ej, daz);
+        publish(dhh + 2 * H + ej, dhn);
+        float* dx = U.da + f * GH;
         store_or_publish(dx + ej, dar_, pub_dax);
         store_or_publish(dx + H + ej, daz, pub_dax);
         store_or_publish(dx + 2 * H + ej, dan, pub_dax);
-        publish(dhh + ej, dar_);
-        publish(dhh + H + ej, daz);
-        publish(dhh + 2 * H + ej, dan * r);
         carry = dh * z;
+        bsum[0] += dar_;
+        bsum[1] += daz;
+        bsum[2] += dan;
+        bsumh[0] += dar_;
+        bsumh[1] += daz;
+        bsumh[2] += dhn;
       }
     }
     s = nx;
     __syncthreads();  // red is rewritten by the next step
+  }
+  // Bias gradients of this workgroup: sum its 16 rows in a fixed order and
+  // write one partial per row group (folded over row groups afterwards).
+  if (epi) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) red[g * 256 + threadIdx.x] = bsum[g];
+    if constexpr (G == 3) {
+#pragma unroll
+      for (int g = 0; g < 3; ++g) red[(4 + g) * 256 + threadIdx.x] = bsumh[g];
+    }
+  }
+  __syncthreads();
+  const int nsum = G == 4 ? 4 : 6;
+  if ((int)threadIdx.x < nsum * 16) {
+    const int g = threadIdx.x >> 4, u = threadIdx.x & 15;
+    const int slot = G == 3 && g >= 3 ? 4 + (g - 3) : g;
+    float v = 0.f;
+    for (int row = 0; row < 16; ++row) v += red[slot * 256 + row * 16 + u];
+    const int gate = G == 3 && g >= 3 ? g - 3 : g;
+    float* dst = (G == 3 && g >= 3) ? U.bias_part_h : U.bias_part;
+    dst[(int64_t)rg * GH + gate * H + j0 + u] = v;
   }
 }
 
@@ -617,8 +664,8 @@ hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem
 
 namespace {
 
-// Chunks per wave (a power of two) for a reduction of nch chunks over 4
-// waves; 0 if above the per-lane budget.
+// Chunks per wave (a power of two) for the longer segment of nch chunks
+// split over 4 waves; 0 if above the per-lane budget.
 int fwd_maxc(int nch, bool bf16) {
   const int per = (nch + 3) / 4;
   int m = 1;
@@ -663,7 +710,7 @@ FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
   for (int q = 0; q < a.nunits; ++q) {
     const FwdUnit& u = a.u[q];
     if (u.kin < 1 || u.kin % 4 != 0 || u.in_bytes >= kNoRow || u.out_bytes >= kNoRow) return p;
-    nch = std::max(nch, (u.kin + ch - 1) / ch + a.H / ch);
+    nch = std::max(nch, std::max((u.kin + ch - 1) / ch, a.H / ch));
   }
   p.nt = a.H >= 256 && a.H % 8 == 0 ? 2 : 1;
   p.maxc = fwd_maxc(nch, bf16);
@@ -737,7 +784,7 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
   for (int q = 0; q < a.nunits; ++q) {
     const BwdUnit& u = a.u[q];
     if (u.rec_bytes >= kNoRow || (u.up && (u.k_up % ch != 0 || u.up_bytes >= kNoRow))) return p;
-    nch = std::max(nch, (u.up ? u.k_up / ch : 0) + G * a.H / ch);
+    nch = std::max(nch, std::max(u.up ? u.k_up / ch : 0, G * a.H / ch));
   }
   const int cap = bf16 ? 8 : 16;
   for (int nw : {4, 16}) {
@@ -752,7 +799,7 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
   }
   if (p.nw == 0) return p;
   p.blocks = a.nunits * (a.H / kBwdUnits) * ((B + 15) / 16);
-  p.shmem = sizeof(float) * p.nw * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  p.shmem = sizeof(float) * std::max(p.nw, 8) * 256 + sizeof(int32_t) * (2 * a.T + 1);
   p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc);
   return p;
 }
