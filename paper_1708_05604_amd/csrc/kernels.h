@@ -10,6 +10,15 @@
 
 namespace rnnbkt {
 
+// Cell nonlinearities of both recurrence implementations (device code):
+// the logistic function from the hardware exp and reciprocal (relative
+// error a few ulp), and tanh x = 2 sigma(2x) - 1 (absolute error a few
+// 1e-8 near 0).  Saturating inputs give exactly 0 / 1 (-1 / 1 for tanh).
+__device__ inline float act_sigmoid(float x) {
+  return __builtin_amdgcn_rcpf(1.f + __expf(-x));
+}
+__device__ inline float act_tanh(float x) { return 2.f * act_sigmoid(2.f * x) - 1.f; }
+
 // ---------------------------------------------------------------- GEMM
 // C[M x N] = op(A) . op(B) (+ bias[n]) (+ C if accumulate), fp32 in memory;
 // operands rounded to bf16 on the way to the matrix cores when bf16 != 0.

@@ -48,7 +48,6 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
-__device__ inline float sigm(float x) { return 1.f / (1.f + __expf(-x)); }
 
 
 constexpr unsigned kSentinel = 0xFFFFFFFFu;
@@ -156,27 +155,49 @@ __device__ inline void issue_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off,
   }
 }
 
+template <int NE>
+__device__ inline bool segment_clear(const unsigned (&u)[NE]) {
+  bool ready = true;
+#pragma unroll
+  for (int j = 0; j < NE; ++j) ready &= u[j] != kSentinel;
+  return __all(ready);
+}
+
+// True once some wait of any launch has given up: later waits return at
+// once, so the launch still ends.
+__device__ inline bool waits_abandoned() {
+  return __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+}
+
+__device__ inline void report_timeout() {
+  if ((threadIdx.x & 63) == 0)
+    __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The buffer loads are pure reads to the compiler: between two polls of the
+// same addresses it must be told that memory may have changed, or it merges
+// the polls into one (no code is emitted for this).
+__device__ inline void poll_fence() { __asm__ __volatile__("" ::: "memory"); }
+
+constexpr unsigned kMaxPolls = 1u << 20;
+
 // Re-reads the segment until no element holds the sentinel (wave-uniform).
+// One poll at a time: keeping a second poll in flight detects arrivals
+// sooner, but its load is still pending when the next step issues, which
+// costs more than it saves.
 template <bool BF16, int MAXC>
 __device__ inline void settle_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
                                       int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC]) {
-  constexpr int NE = Chunk<BF16>::CPL * MAXC;
-  unsigned spins = 0;
-  for (;;) {
-    bool ready = true;
-#pragma unroll
-    for (int j = 0; j < NE; ++j) ready &= u[j] != kSentinel;
-    if (__all(ready)) return;
-    if (spins == 0 && __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT) != 0u)
-      return;
-    if (++spins == (1u << 20)) {
-      if ((threadIdx.x & 63) == 0)
-        __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (segment_clear(u) || waits_abandoned()) return;
+  for (unsigned polls = 1;; ++polls) {
+    __builtin_amdgcn_s_sleep(1);
+    poll_fence();
+    issue_segment<BF16, MAXC>(r, row_off, sl, klim, u);
+    if (segment_clear(u)) return;
+    if (polls >= kMaxPolls) {
+      report_timeout();
       return;
     }
-    __builtin_amdgcn_s_sleep(1);
-    issue_segment<BF16, MAXC>(r, row_off, sl, klim, u);
   }
 }
 
@@ -360,13 +381,13 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
       const int64_t f = s.row0 + erow;
       float* st = U.stash + f * 4 * H;
       if constexpr (G == 4) {
-        const float ig = sigm(sg[0] + bi[0]);
-        const float fg = sigm(sg[1] + bi[1]);
-        const float gg = tanhf(sg[2] + bi[2]);
-        const float og = sigm(sg[3] + bi[3]);
+        const float ig = act_sigmoid(sg[0] + bi[0]);
+        const float fg = act_sigmoid(sg[1] + bi[1]);
+        const float gg = act_tanh(sg[2] + bi[2]);
+        const float og = act_sigmoid(sg[3] + bi[3]);
         const float cp = has_prev ? c_state : 0.f;
         c_state = fg * cp + ig * gg;
-        h_state = og * tanhf(c_state);
+        h_state = og * act_tanh(c_state);
         publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
         st[ej] = ig;
         st[H + ej] = fg;
@@ -374,10 +395,10 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
         st[3 * H + ej] = og;
         U.cst[f * H + ej] = c_state;
       } else {
-        const float rg_ = sigm(sg[0] + bi[0] + bh[0]);
-        const float z = sigm(sg[1] + bi[1] + bh[1]);
+        const float rg_ = act_sigmoid(sg[0] + bi[0] + bh[0]);
+        const float z = act_sigmoid(sg[1] + bi[1] + bh[1]);
         const float ahn = sg[3] + bh[2];
-        const float n = tanhf(sg[2] + bi[2] + rg_ * ahn);
+        const float n = act_tanh(sg[2] + bi[2] + rg_ * ahn);
         const float hp = has_prev ? h_state : 0.f;
         h_state = (1.f - z) * n + z * hp;
         publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
@@ -546,7 +567,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       for (int w_ = 0; w_ < NW; ++w_) dh_red += red[w_ * 256 + threadIdx.x];
       if constexpr (G == 4) {
         const float dh = dhv + dh_red;
-        const float tc = tanhf(cc);
+        const float tc = act_tanh(cc);
         const float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
         const float cp = has_prev ? cprev : 0.f;
         const float di = dc * st2 * st0 * (1.f - st0);
@@ -744,26 +765,48 @@ hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStr
 
 namespace {
 
+// Chunks per wave a workgroup of nw waves holds in registers without
+// spilling (512, 256 and 128 VGPRs per lane at 1, 2 and 4 waves per SIMD),
+// and the largest instantiated (16 waves may spill for very wide layers).
+constexpr int bwd_maxc_fit(int nw, bool bf16) {
+  return (nw == 4 ? 16 : nw == 8 ? 8 : 4) / (bf16 ? 2 : 1);
+}
+constexpr int bwd_maxc_cap(int nw, bool bf16) {
+  return nw == 16 ? (bf16 ? 8 : 16) : bwd_maxc_fit(nw, bf16);
+}
+
+template <int G, bool BF16, int NW, int M>
+const void* bwd_kernel_m() {
+  if constexpr (M <= bwd_maxc_cap(NW, BF16))
+    return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, M>);
+  return nullptr;
+}
+
 template <int G, bool BF16, int NW>
 const void* bwd_kernel_nw(int maxc) {
   switch (maxc) {
-    case 1: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 1>);
-    case 2: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 2>);
-    case 4: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 4>);
-    case 8: return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 8>);
+    case 1: return bwd_kernel_m<G, BF16, NW, 1>();
+    case 2: return bwd_kernel_m<G, BF16, NW, 2>();
+    case 4: return bwd_kernel_m<G, BF16, NW, 4>();
+    case 8: return bwd_kernel_m<G, BF16, NW, 8>();
+    case 16: return bwd_kernel_m<G, BF16, NW, 16>();
   }
-  if constexpr (!BF16)
-    if (maxc == 16) return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, 16>);
+  return nullptr;
+}
+
+template <int G, bool BF16>
+const void* bwd_kernel_g(int nw, int maxc) {
+  switch (nw) {
+    case 4: return bwd_kernel_nw<G, BF16, 4>(maxc);
+    case 8: return bwd_kernel_nw<G, BF16, 8>(maxc);
+    case 16: return bwd_kernel_nw<G, BF16, 16>(maxc);
+  }
   return nullptr;
 }
 
 const void* bwd_kernel(int cell, bool bf16, int nw, int maxc) {
-  if (cell == RNNBKT_CELL_LSTM) {
-    if (bf16) return nw == 4 ? bwd_kernel_nw<4, true, 4>(maxc) : bwd_kernel_nw<4, true, 16>(maxc);
-    return nw == 4 ? bwd_kernel_nw<4, false, 4>(maxc) : bwd_kernel_nw<4, false, 16>(maxc);
-  }
-  if (bf16) return nw == 4 ? bwd_kernel_nw<3, true, 4>(maxc) : bwd_kernel_nw<3, true, 16>(maxc);
-  return nw == 4 ? bwd_kernel_nw<3, false, 4>(maxc) : bwd_kernel_nw<3, false, 16>(maxc);
+  if (cell == RNNBKT_CELL_LSTM) return bf16 ? bwd_kernel_g<4, true>(nw, maxc) : bwd_kernel_g<4, false>(nw, maxc);
+  return bf16 ? bwd_kernel_g<3, true>(nw, maxc) : bwd_kernel_g<3, false>(nw, maxc);
 }
 
 struct BwdPlan {
@@ -772,8 +815,11 @@ struct BwdPlan {
   size_t shmem;
 };
 
-// Waves: 4, or 16 when a wave's share of the reduction would exceed the
-// per-lane budget (16 chunks fp32, 8 chunks bf16).
+// Waves per workgroup: the fewest that bring a wave's share of the longer
+// segment down to kBwdChain chunks (each chunk is a serial MFMA group on
+// the step's critical path), else the most that fit in registers.
+constexpr int kBwdChain = 2;
+
 BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
   BwdPlan p{nullptr, 0, 0, 0, 0};
   const int ch = bf16 ? 32 : 16;
@@ -786,15 +832,22 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     if (u.rec_bytes >= kNoRow || (u.up && (u.k_up % ch != 0 || u.up_bytes >= kNoRow))) return p;
     nch = std::max(nch, std::max(u.up ? u.k_up / ch : 0, G * a.H / ch));
   }
-  const int cap = bf16 ? 8 : 16;
-  for (int nw : {4, 16}) {
+  for (int nw : {4, 8, 16}) {
     const int per = (nch + nw - 1) / nw;
     int m = 1;
     while (m < per) m *= 2;
-    if (m <= cap) {
-      p.nw = nw;
+    if (m > bwd_maxc_fit(nw, bf16)) continue;
+    p.nw = nw;
+    p.maxc = m;
+    if (m <= kBwdChain) break;
+  }
+  if (p.nw == 0) {
+    // Very wide layers: 16 waves with spilled registers.
+    int m = 1;
+    while (m < (nch + 15) / 16) m *= 2;
+    if (m <= bwd_maxc_cap(16, bf16)) {
+      p.nw = 16;
       p.maxc = m;
-      break;
     }
   }
   if (p.nw == 0) return p;

@@ -22,7 +22,6 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 
-__device__ inline float sigm(float x) { return 1.f / (1.f + __expf(-x)); }
 
 __device__ inline bf8 to_bf8(f4 lo, f4 hi) {
   bf8 r;
@@ -119,13 +118,13 @@ __global__ __launch_bounds__(256) void k_step_fwd(StepFwdArgs a) {
   const float* gx = a.gx + f * GH;
   const bool has_prev = row < a.prev_rows;
   if constexpr (G == 4) {
-    const float ig = sigm(gx[j] + s[0]);
-    const float fg = sigm(gx[H + j] + s[1]);
-    const float gg = tanhf(gx[2 * H + j] + s[2]);
-    const float og = sigm(gx[3 * H + j] + s[3]);
+    const float ig = act_sigmoid(gx[j] + s[0]);
+    const float fg = act_sigmoid(gx[H + j] + s[1]);
+    const float gg = act_tanh(gx[2 * H + j] + s[2]);
+    const float og = act_sigmoid(gx[3 * H + j] + s[3]);
     const float cp = has_prev ? a.cst[(int64_t)(a.prev0 + row) * H + j] : 0.f;
     const float c = fg * cp + ig * gg;
-    const float h = og * tanhf(c);
+    const float h = og * act_tanh(c);
     float* st = a.stash + f * 4 * H;
     st[j] = ig;
     st[H + j] = fg;
@@ -137,9 +136,9 @@ __global__ __launch_bounds__(256) void k_step_fwd(StepFwdArgs a) {
     const float ahr = s[0] + a.bhh[j];
     const float ahz = s[1] + a.bhh[H + j];
     const float ahn = s[2] + a.bhh[2 * H + j];
-    const float r = sigm(gx[j] + ahr);
-    const float z = sigm(gx[H + j] + ahz);
-    const float n = tanhf(gx[2 * H + j] + r * ahn);
+    const float r = act_sigmoid(gx[j] + ahr);
+    const float z = act_sigmoid(gx[H + j] + ahz);
+    const float n = act_tanh(gx[2 * H + j] + r * ahn);
     const float hp = has_prev ? a.hout[(int64_t)(a.prev0 + row) * a.ldh + j] : 0.f;
     const float h = (1.f - z) * n + z * hp;
     float* st = a.stash + f * 4 * H;
@@ -217,7 +216,7 @@ __global__ __launch_bounds__(256) void k_step_bwd(StepBwdArgs a) {
     const float dh = a.dh_in[f * a.ldd + j] + (has_next ? dh_rec : 0.f);
     const float ig = st[j], fg = st[H + j], gg = st[2 * H + j], og = st[3 * H + j];
     const float c = a.cst[f * H + j];
-    const float tc = tanhf(c);
+    const float tc = act_tanh(c);
     const float dc = dh * og * (1.f - tc * tc) + (has_next ? *carry : 0.f);
     const float cp = has_prev ? a.cst[(int64_t)(a.prev0 + row) * H + j] : 0.f;
     float* da = a.da + f * GH;
