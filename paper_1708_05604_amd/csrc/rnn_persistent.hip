@@ -253,6 +253,17 @@ __device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
   return u;
 }
 
+// Workgroups are dispatched to the 8 XCDs in turn (block b on XCD b mod 8),
+// each XCD with its own L2.  Renumbering so that consecutive logical ids
+// share an XCD keeps each unit's row groups, which exchange values every
+// step, on one XCD.
+constexpr int kXcds = 8;
+__device__ inline int logical_block() {
+  const int b = blockIdx.x, n = gridDim.x;
+  if (n % kXcds != 0) return b;
+  return (b % kXcds) * (n / kXcds) + b / kXcds;
+}
+
 // Copies the batch tables into LDS.
 __device__ inline void load_tables(const int32_t* bs, const int32_t* off, int T, int32_t* tbs,
                                    int32_t* toff) {
@@ -277,11 +288,12 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * NT * 256);  // batch sizes [T]
   int32_t* toff = tbs + a.T;                                       // offsets [T+1]
   load_tables(a.bs, a.off, a.T, tbs, toff);
+  const int bid = logical_block();
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
-    if ((int)blockIdx.x >= a.u[q].wg_begin) ui = q;
+    if (bid >= a.u[q].wg_begin) ui = q;
   const FwdUnit U = pick_unit(a, ui);
-  const int rem = blockIdx.x - U.wg_begin;
+  const int rem = bid - U.wg_begin;
   const int slice = rem % a.slices;
   const int rg = rem / a.slices;
   const int H = a.H;
@@ -466,11 +478,12 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   int32_t* tbs = reinterpret_cast<int32_t*>(red + (NW < 8 ? 8 : NW) * 256);
   int32_t* toff = tbs + a.T;
   load_tables(a.bs, a.off, a.T, tbs, toff);
+  const int bid = logical_block();
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
-    if ((int)blockIdx.x >= a.u[q].wg_begin) ui = q;
+    if (bid >= a.u[q].wg_begin) ui = q;
   const BwdUnit U = pick_unit(a, ui);
-  const int rem = blockIdx.x - U.wg_begin;
+  const int rem = bid - U.wg_begin;
   const int slice = rem % a.slices;
   const int rg = rem / a.slices;
   const int H = a.H;
