@@ -37,6 +37,32 @@ from paper_1708_05604_amd import lib, synth  # noqa: E402
 METRIC = "useful (non-pad) LSTM timesteps/sec fwd+bwd on 1 GPU; MFMA util %; pad waste %"
 PEAK_TFLOPS = {synth.FP32: 157.3, synth.BF16: 2500.0}
 PEAK_HBM_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+# Kernel sources whose hash keys the recorded byte counters: after any change
+# to them the counters no longer describe the kernel and traffic is null.
+TRAFFIC_SOURCES = ("paper_1708_05604_amd/csrc/rnn_persistent.hip", "paper_1708_05604_amd/csrc/kernels.h")
+
+
+def recorded_traffic(workload, K, kind):
+    """HBM bytes per launch of the dominant kernel from the rocprofv3 FETCH_SIZE /
+    WRITE_SIZE runs summarised under profiles/, or None when no record matches
+    this workload, kernel and the current kernel sources."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{workload}_k{K}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            rec[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for src in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if rec.get("kernel_kind") != kind or rec.get("sources_sha256_16") != h.hexdigest()[:16]:
+        return None
+    return float(rec["fetch_bytes_per_launch"]) + float(rec["write_bytes_per_launch"])
 TILE_M = 16
 
 
@@ -255,6 +281,7 @@ def main(argv=None):
             ach = d["bytes"] / max(d["launches"], 1) / avg_s / 1e9
             roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": ach / PEAK_HBM_GBS, "traffic": None}
+        roof["traffic"] = recorded_traffic(args.workload, K, dom)
         roof.update({"kernel": dom, "avg_launch_us": avg_s * 1e6, "launches": d["launches"]})
         out["roofline"] = roof
         out["kernels"] = {k: {"ms": v["ms"], "launches": v["launches"],
