@@ -13,6 +13,8 @@ Modules
              shuffled inside each bucket (Sec. III), cut into mini-batches
   rnn        LSTM / GRU forward and backpropagation-through-time in float64,
              per-frame softmax cross-entropy, SGD
+  optim      ADADELTA, the update rule of the paper's training processes
+             (Sec. III.B, step 4)
 
 Every function is written to be checked by eye against the paper or against
 textbook definitions, not to be fast.  Pins (brute force, closed forms, finite
