@@ -121,14 +121,17 @@ class Epoch:
 
 
 def run_steps(ep, state, first, count, torch):
-    desc, params, grads, reserve, workspace, loss, lr = state
+    desc, params, grads, reserve, workspace, loss, lr, opt = state
     useful = 0
     nb = len(ep.batches)
     for k in range(count):
         i = (first + k) % nb
         lib.lstm_fwd(desc, params, ep.x[i], ep.y[i], ep.lens[i], reserve, workspace, loss)
         lib.lstm_bwd(desc, params, ep.lens[i], reserve, workspace, grads)
-        lib.sgd_apply(params, grads, lr)
+        if opt is None:
+            lib.sgd_apply(params, grads, lr)
+        else:
+            lib.adadelta_apply(params, grads, opt[0], opt[1])
         useful += ep.useful[i]
     return useful
 
@@ -186,7 +189,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--workload", default="lstm2", choices=list(synth.WORKLOADS))
     ap.add_argument("--K", type=int, default=0, help="buckets (0 = largest of the workload)")
-    ap.add_argument("--lr", type=float, default=0.1)
+    ap.add_argument("--lr", type=float, default=0.1, help="SGD step size")
+    ap.add_argument("--optimizer", default="sgd", choices=("sgd", "adadelta"),
+                    help="parameter update of each step (adadelta: rho 0.95, eps 1e-6)")
     ap.add_argument("--no-k1", action="store_true", help="skip the K=1 epoch")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--no-timer", action="store_true", help="skip the per-kernel pass")
@@ -230,7 +235,10 @@ def main(argv=None):
     params = torch.from_numpy(data.params).to(dev)
     grads = torch.zeros_like(params)
     loss = torch.zeros(1, dtype=torch.float32, device=dev)
-    state = (desc, params, grads, reserve, workspace, loss, args.lr)
+    opt = None
+    if args.optimizer == "adadelta":
+        opt = (torch.zeros_like(params), torch.zeros_like(params))
+    state = (desc, params, grads, reserve, workspace, loss, args.lr, opt)
 
     nb = len(ep.batches)
     steps = args.steps or nb
@@ -245,7 +253,7 @@ def main(argv=None):
         "warmup": warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.gemm_dtype == synth.BF16 else "f32", "data": "synthetic",
-        "config": {"workload": describe(w, K), "batches_per_epoch": nb,
+        "config": {"workload": describe(w, K), "optimizer": args.optimizer, "batches_per_epoch": nb,
                    "useful_timesteps_per_epoch": ep.U, "parallelism": "single GPU"},
         "mfma_util_pct": 100.0 * flops * value / (peak * 1e12),
         "achieved_tflops": flops * value / 1e12,

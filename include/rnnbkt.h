@@ -198,6 +198,24 @@ int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
 int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,
                          void* stream);
 
+/* rnnbkt_adadelta_apply -- one ADADELTA step, the update rule of the paper's
+ * training processes (Sec. III.B, step 4; Zeiler's method, its ref. [21]),
+ * elementwise over n device fp32 values, in this order:
+ *   acc_g2[i]  <- rho * acc_g2[i] + (1 - rho) * g^2            (g = grads[i])
+ *   dx          = -sqrt(acc_dx2[i] + eps) / sqrt(acc_g2[i] + eps) * g
+ *                 (acc_g2 already updated, acc_dx2 not yet)
+ *   acc_dx2[i] <- rho * acc_dx2[i] + (1 - rho) * dx^2
+ *   params[i]  <- params[i] + lr * dx
+ *   acc_g2, acc_dx2  caller-owned optimiser state of n floats each, zero
+ *                    before the first step, kept between steps
+ *   rho in [0, 1) (0.95 in the published method), eps > 0 (1e-6), lr > 0
+ *   (1 = the method as published; it has no learning rate of its own).
+ * All four arrays 16-byte aligned; params, acc_g2, acc_dx2 updated in place.
+ * Errors: RNNBKT_EINVAL (null pointer, n < 0, misalignment, constants out of
+ * range), before any launch. */
+int32_t rnnbkt_adadelta_apply(float* params, const float* grads, float* acc_g2, float* acc_dx2,
+                              int64_t n, float rho, float eps, float lr, void* stream);
+
 /*
  * rnnbkt_top_hidden -- copies the top layer's per-frame output of the batch
  * held in `reserve` (after rnnbkt_lstm_fwd) into the padded layout
@@ -212,9 +230,11 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
  * Kernel timer -- measurement support for the benchmark (not part of the
  * method).  While enabled, the model calls and rnnbkt_sgd_apply bracket every
  * kernel launch with a pair of HIP events recorded on the call's stream and
- * note the launch's algorithmic work: recurrent steps count the flops of
- * their h.W_hh (forward) or dA.W_hh (backward) product, GEMMs 2*M*N*K,
- * the loss kernel 8*C+4 bytes per frame, SGD 12 bytes per parameter.
+ * note the launch's algorithmic work: recurrent launches count the flops of
+ * their products (forward x.W_ih and h.W_hh, backward dA.W_hh and, where a
+ * launch takes a stack of layers, the upper layer's dA.W_ih), GEMMs 2*M*N*K,
+ * the loss kernel 8*C+4 bytes per frame, SGD 12 and ADADELTA 28 bytes per
+ * parameter.
  * Kinds: see RNNBKT_KERNEL_*.  The events add a small gap between launches,
  * so time a run with the timer off and use the timer in a separate pass.
  *   rnnbkt_kernel_timer(1) clears the records and starts recording,
@@ -227,7 +247,7 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
 #define RNNBKT_KERNEL_STEP_BWD 1 /* recurrent step, backward through time */
 #define RNNBKT_KERNEL_GEMM 2     /* dense contractions incl. split-K folds */
 #define RNNBKT_KERNEL_XENT 3     /* softmax cross-entropy and its gradient */
-#define RNNBKT_KERNEL_SGD 4      /* parameter update */
+#define RNNBKT_KERNEL_SGD 4      /* parameter update (SGD or ADADELTA) */
 #define RNNBKT_KERNEL_OTHER 5    /* batch tables, packing, column sums, loss sum */
 #define RNNBKT_KERNEL_KINDS 6
 

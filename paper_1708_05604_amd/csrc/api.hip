@@ -817,6 +817,25 @@ extern "C" int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n
   return RNNBKT_OK;
 }
 
+extern "C" int32_t rnnbkt_adadelta_apply(float* params, const float* grads, float* acc_g2,
+                                         float* acc_dx2, int64_t n, float rho, float eps,
+                                         float lr, void* stream) {
+  clear_error();
+  RNNBKT_REQUIRE(params && grads && acc_g2 && acc_dx2, RNNBKT_EINVAL,
+                 "adadelta_apply: null pointer");
+  RNNBKT_REQUIRE(n >= 0, RNNBKT_EINVAL, "adadelta_apply: n < 0");
+  RNNBKT_REQUIRE(aligned16(params) && aligned16(grads) && aligned16(acc_g2) && aligned16(acc_dx2),
+                 RNNBKT_EINVAL, "adadelta_apply: all four arrays must be 16-byte aligned");
+  RNNBKT_REQUIRE(rho >= 0.f && rho < 1.f, RNNBKT_EINVAL, "adadelta_apply: rho must be in [0, 1)");
+  RNNBKT_REQUIRE(eps > 0.f, RNNBKT_EINVAL, "adadelta_apply: eps must be > 0");
+  RNNBKT_REQUIRE(lr > 0.f, RNNBKT_EINVAL, "adadelta_apply: lr must be > 0");
+  if (n == 0) return RNNBKT_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Timed tm(RNNBKT_KERNEL_SGD, 0.0, 28.0 * n, st);
+  RNNBKT_HIP(launch_adadelta(params, grads, acc_g2, acc_dx2, n, rho, eps, lr, st));
+  return RNNBKT_OK;
+}
+
 extern "C" int32_t rnnbkt_kernel_timer(int32_t enable) {
   clear_error();
   std::lock_guard<std::mutex> lk(g_tmu);

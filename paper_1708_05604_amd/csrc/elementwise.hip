@@ -1,6 +1,7 @@
 // Memory-bound kernels of the training step: batch tables and packing of the
 // padded batch into valid frames, the per-frame softmax cross-entropy with
-// its gradient, deterministic reductions, and the SGD update.
+// its gradient, deterministic reductions, and the parameter updates (SGD and
+// ADADELTA).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -175,6 +176,39 @@ __global__ void k_sgd(float* __restrict__ p, const float* __restrict__ g, int64_
   }
 }
 
+// One ADADELTA step on element i (Zeiler's method, the update rule of the
+// paper's training processes): the squared-gradient average first, the step
+// from the previous squared-update average, then that average.
+__device__ inline void adadelta1(float& p, float g, float& eg2, float& edx2, float rho, float eps,
+                                 float lr) {
+  const float e = rho * eg2 + (1.f - rho) * g * g;
+  const float dx = -(sqrtf(edx2 + eps) / sqrtf(e + eps)) * g;
+  edx2 = rho * edx2 + (1.f - rho) * dx * dx;
+  eg2 = e;
+  p += lr * dx;
+}
+
+__global__ void k_adadelta(float* __restrict__ p, const float* __restrict__ g,
+                           float* __restrict__ eg2, float* __restrict__ edx2, int64_t n, float rho,
+                           float eps, float lr) {
+  const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i4 + 3 < n) {
+    float4 pv = *reinterpret_cast<float4*>(p + i4);
+    const float4 gv = *reinterpret_cast<const float4*>(g + i4);
+    float4 a = *reinterpret_cast<float4*>(eg2 + i4);
+    float4 b = *reinterpret_cast<float4*>(edx2 + i4);
+    adadelta1(pv.x, gv.x, a.x, b.x, rho, eps, lr);
+    adadelta1(pv.y, gv.y, a.y, b.y, rho, eps, lr);
+    adadelta1(pv.z, gv.z, a.z, b.z, rho, eps, lr);
+    adadelta1(pv.w, gv.w, a.w, b.w, rho, eps, lr);
+    *reinterpret_cast<float4*>(p + i4) = pv;
+    *reinterpret_cast<float4*>(eg2 + i4) = a;
+    *reinterpret_cast<float4*>(edx2 + i4) = b;
+  } else {
+    for (int64_t i = i4; i < n; ++i) adadelta1(p[i], g[i], eg2[i], edx2[i], rho, eps, lr);
+  }
+}
+
 __global__ void k_fill_u32(unsigned* __restrict__ p, int64_t n, unsigned v) {
   const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i4 + 3 < n) {
@@ -250,6 +284,15 @@ hipError_t launch_sgd(float* p, const float* g, int64_t n, float lr, hipStream_t
   const int64_t quads = (n + 3) / 4;
   hipLaunchKernelGGL(k_sgd, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads), 0,
                      st, p, g, n, lr);
+  return hipGetLastError();
+}
+
+hipError_t launch_adadelta(float* p, const float* g, float* eg2, float* edx2, int64_t n,
+                           float rho, float eps, float lr, hipStream_t st) {
+  const int threads = 256;
+  const int64_t quads = (n + 3) / 4;
+  hipLaunchKernelGGL(k_adadelta, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads),
+                     0, st, p, g, eg2, edx2, n, rho, eps, lr);
   return hipGetLastError();
 }
 

@@ -89,6 +89,9 @@ hipError_t launch_sum(const float* partial, int32_t n, float scale, float* out,
 
 hipError_t launch_sgd(float* params, const float* grads, int64_t n, float lr,
                       hipStream_t stream);
+// One ADADELTA step over n elements (p, eg2, edx2 updated in place).
+hipError_t launch_adadelta(float* p, const float* g, float* eg2, float* edx2, int64_t n,
+                           float rho, float eps, float lr, hipStream_t st);
 
 // ---------------------------------------------------------------- recurrent steps
 // One time step of one layer/direction over the active rows [0, rows) of the

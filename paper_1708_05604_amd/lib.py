@@ -76,6 +76,8 @@ _SIGNATURES = {
     "rnnbkt_lstm_bwd": (ctypes.c_int32, [_descp, _vp, _i32p, ctypes.c_int32, ctypes.c_int32,
                                          _vp, ctypes.c_size_t, _vp, ctypes.c_size_t, _vp, _vp]),
     "rnnbkt_sgd_apply": (ctypes.c_int32, [_vp, _vp, ctypes.c_int64, ctypes.c_float, _vp]),
+    "rnnbkt_adadelta_apply": (ctypes.c_int32, [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_float,
+                                               ctypes.c_float, ctypes.c_float, _vp]),
     "rnnbkt_top_hidden": (ctypes.c_int32, [_descp, _i32p, ctypes.c_int32, ctypes.c_int32, _vp,
                                            ctypes.c_size_t, _vp, _vp]),
     "rnnbkt_kernel_timer": (ctypes.c_int32, [ctypes.c_int32]),
@@ -253,6 +255,19 @@ def sgd_apply(params, grads, lr: float, stream=None, n: Optional[int] = None):
         raise ValueError("n exceeds the tensors' sizes")
     _check(load().rnnbkt_sgd_apply(_dev(params, "float32"), _dev(grads, "float32"), count,
                                    float(lr), _stream(stream)))
+
+
+def adadelta_apply(params, grads, acc_g2, acc_dx2, rho: float = 0.95, eps: float = 1e-6,
+                   lr: float = 1.0, stream=None, n: Optional[int] = None):
+    """One ADADELTA step in place (params, acc_g2, acc_dx2); the state tensors
+    start at zero and are kept between steps."""
+    count = params.numel() if n is None else int(n)
+    if not isinstance(params, int) and count > min(params.numel(), grads.numel(),
+                                                   acc_g2.numel(), acc_dx2.numel()):
+        raise ValueError("n exceeds the tensors' sizes")
+    _check(load().rnnbkt_adadelta_apply(_dev(params, "float32"), _dev(grads, "float32"),
+                                        _dev(acc_g2, "float32"), _dev(acc_dx2, "float32"), count,
+                                        float(rho), float(eps), float(lr), _stream(stream)))
 
 
 def top_hidden(desc, lengths, reserve, out, stream=None):

@@ -121,6 +121,57 @@ def test_sgd_apply_exact():
         np.testing.assert_allclose(tp.cpu().numpy(), ref, rtol=1e-6, atol=1e-7)
 
 
+def test_adadelta_apply_matches_oracle():
+    """Three consecutive ADADELTA steps on ragged sizes, gradients spanning
+    eight decades, against the float64 oracle (state carried on both sides)."""
+    import torch
+    from oracle import optim
+    rng = np.random.default_rng(11)
+    for n in (1, 5, 1027, 4099):
+        p = rng.standard_normal(n).astype(np.float32)
+        tp = torch.from_numpy(p).cuda()
+        ta = torch.zeros(n, dtype=torch.float32, device="cuda")
+        tb = torch.zeros(n, dtype=torch.float32, device="cuda")
+        x, e1, e2 = p.astype(np.float64), np.zeros(n), np.zeros(n)
+        for step in range(3):
+            g = (rng.standard_normal(n) * 10.0 ** rng.integers(-4, 4, n)).astype(np.float32)
+            lib.adadelta_apply(tp, torch.from_numpy(g).cuda(), ta, tb)
+            x, e1, e2 = optim.adadelta(x, g, e1, e2)
+            torch.cuda.synchronize()
+            for name, got, ref in (("params", tp, x), ("E[g^2]", ta, e1), ("E[dx^2]", tb, e2)):
+                got = got.cpu().numpy().astype(np.float64)
+                np.testing.assert_allclose(got, ref, rtol=1e-5, atol=1e-12 * np.max(np.abs(ref)),
+                                           err_msg=f"n={n} step={step} {name}")
+
+
+def test_adadelta_trajectory_tiny():
+    """Three training steps (forward, backward, ADADELTA) on one batch: the
+    parameters follow the oracle's trajectory."""
+    import torch
+    from oracle import optim
+    spec = H.Spec(0, 1, 0, 4, 32, 20)
+    data = H.data_from_lengths(spec, [30, 22, 22, 9, 3], seed=6, scale=0.3)
+    order = H.batch_order(data, range(5))
+    gb = H.GpuBatch(spec, data.params, data, order)
+    ta = torch.zeros_like(gb.params)
+    tb = torch.zeros_like(gb.params)
+    theta = data.params.astype(np.float64)
+    e1 = np.zeros_like(theta)
+    e2 = np.zeros_like(theta)
+    for step in range(3):
+        gb.forward()
+        gb.backward()
+        lib.adadelta_apply(gb.params, gb.grads, ta, tb)
+        torch.cuda.synchronize()
+        lib.sync_check()
+        _, grad, _ = H.oracle_batch(spec, theta, data, order)
+        theta, e1, e2 = optim.adadelta(theta, grad, e1, e2)
+        got = gb.params.cpu().numpy().astype(np.float64)
+        err = H.normwise_err(got - data.params, theta - data.params)
+        print(f"[case] adadelta step {step} update err {err:.2e}", flush=True)
+        assert err < 1e-4
+
+
 def test_nan_padding_and_determinism():
     """Pad frames filled with NaN change nothing, and two runs are bitwise equal."""
     spec = H.Spec(0, 2, 1, 8, 64, 12)

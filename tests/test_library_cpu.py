@@ -162,6 +162,15 @@ def test_validation_errors_before_launch():
     assert rc == lib.EINVAL
     rc = L.rnnbkt_sgd_apply(18, 16, 10, 0.1, None)
     assert rc == lib.EINVAL and "aligned" in lib.last_error()
+    rc = L.rnnbkt_adadelta_apply(16, 16, None, 16, 10, 0.95, 1e-6, 1.0, None)
+    assert rc == lib.EINVAL and "null" in lib.last_error()
+    rc = L.rnnbkt_adadelta_apply(16, 16, 16, 20, 10, 0.95, 1e-6, 1.0, None)
+    assert rc == lib.EINVAL and "aligned" in lib.last_error()
+    for rho, eps, lr in ((1.0, 1e-6, 1.0), (-0.1, 1e-6, 1.0), (0.95, 0.0, 1.0), (0.95, 1e-6, 0.0)):
+        rc = L.rnnbkt_adadelta_apply(16, 16, 16, 16, 10, rho, eps, lr, None)
+        assert rc == lib.EINVAL, (rho, eps, lr)
+    assert L.rnnbkt_adadelta_apply(16, 16, 16, 16, -1, 0.95, 1e-6, 1.0, None) == lib.EINVAL
+    assert L.rnnbkt_adadelta_apply(16, 16, 16, 16, 0, 0.95, 1e-6, 1.0, None) == lib.OK
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
