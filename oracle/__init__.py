@@ -15,6 +15,8 @@ Modules
              per-frame softmax cross-entropy, SGD
   optim      ADADELTA, the update rule of the paper's training processes
              (Sec. III.B, step 4)
+  ctc        the CTC loss of the paper's experiments (Sec. IV.A) and its
+             gradient, log-space forward-backward over the blank-extended target
 
 Every function is written to be checked by eye against the paper or against
 textbook definitions, not to be fast.  Pins (brute force, closed forms, finite

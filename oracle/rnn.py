@@ -220,11 +220,18 @@ def log_softmax(z):
     return z - (m + np.log(np.exp(z - m).sum(axis=-1, keepdims=True)))
 
 
-def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True):
+def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True, ctc_targets=None):
     """Loss and flat gradient for one mini-batch given as lists of per-sequence
     features [L_s, D] and labels [L_s].  Returns (loss, grad or None, outputs)
-    where outputs holds the per-sequence top-layer activations."""
+    where outputs holds the per-sequence top-layer activations.
+
+    Per-frame loss: the mean over the batch's valid frames of the softmax
+    cross-entropy of the frame's label.  With ctc_targets (one label string
+    per sequence, classes 1..C-1; seqs_y is then not used): the mean over
+    the batch's sequences of the CTC loss (oracle/ctc.py)."""
+    from oracle import ctc
     p = unpack(m, theta)
+    n_seq = len(seqs_x)
     G, H, dirs = m.gates, m.hidden, m.dirs
     n_valid = sum(int(len(y)) for y in seqs_y)
     grads = {k: np.zeros_like(v) for k, v in p.items()}
@@ -251,13 +258,20 @@ def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True):
         top = inputs[-1]
         tops.append(top)
         z = top @ p[("W_out", 0, 0)].T + p[("b_out", 0, 0)]
-        logp = log_softmax(z)
-        loss -= logp[np.arange(L), Y].sum() / n_valid
-        if not need_grad:
-            continue
-        dz = np.exp(logp)
-        dz[np.arange(L), Y] -= 1.0
-        dz /= n_valid
+        if ctc_targets is not None:
+            lc, gc = ctc.ctc_loss_grad(z, ctc_targets[len(tops) - 1])
+            loss += lc / n_seq
+            if not need_grad:
+                continue
+            dz = gc / n_seq
+        else:
+            logp = log_softmax(z)
+            loss -= logp[np.arange(L), Y].sum() / n_valid
+            if not need_grad:
+                continue
+            dz = np.exp(logp)
+            dz[np.arange(L), Y] -= 1.0
+            dz /= n_valid
         grads[("W_out", 0, 0)] += dz.T @ top
         grads[("b_out", 0, 0)] += dz.sum(axis=0)
         dIn = dz @ p[("W_out", 0, 0)]

@@ -22,6 +22,13 @@ no recurrence).  Draw order for ``make_workload``:
   4. parameters (when a count is given) = uniform(-0.1, 0.1, count) as float32.
 Shuffle keys for an epoch come from a separate generator seeded by
 (seed, epoch) so that any epoch can be regenerated on its own.
+
+Label strings for the CTC loss (``ctc_targets``) come from their own generator
+seeded by (seed, 0xC7C), so the per-frame draws above do not change: sequence
+s, in index order, gets max(1, L_s // FRAMES_PER_LABEL) labels uniform over
+classes 1..C-1 (class 0 is the blank).  Eight frames per label keeps every
+string alignable (L_s >= 2 U_s covers a blank between every pair of equal
+neighbours).
 """
 from __future__ import annotations
 
@@ -108,6 +115,16 @@ def make_workload(w: Workload, seed: int = 0, param_count: Optional[int] = None,
     if param_count is not None:
         params = rng.uniform(-0.1, 0.1, param_count).astype(np.float32)
     return Data(lengths, offsets, X, Y, params)
+
+
+FRAMES_PER_LABEL = 8
+
+
+def ctc_targets(lengths, C: int, seed: int = 0):
+    """One label string per sequence (int32 arrays, classes 1..C-1)."""
+    rng = np.random.default_rng([seed, 0xC7C])
+    return [rng.integers(1, C, max(1, int(L) // FRAMES_PER_LABEL)).astype(np.int32)
+            for L in lengths]
 
 
 def shuffle_keys(seed: int, epoch: int, n: int) -> np.ndarray:

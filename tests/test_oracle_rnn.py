@@ -45,7 +45,7 @@ def _torch_model(m, theta):
     return net, lin
 
 
-def _torch_loss_grad(m, theta, xs, ys):
+def _torch_loss_grad(m, theta, xs, ys, ctc_targets=None):
     net, lin = _torch_model(m, theta)
     lengths = torch.tensor([len(y) for y in ys])
     padded = torch.nn.utils.rnn.pad_sequence([torch.tensor(x) for x in xs])
@@ -54,8 +54,16 @@ def _torch_loss_grad(m, theta, xs, ys):
     out, _ = torch.nn.utils.rnn.pad_packed_sequence(out)
     tops = [out[:L, b] for b, L in enumerate(lengths.tolist())]
     top = torch.cat(tops)
-    y = torch.cat([torch.tensor(np.asarray(v)) for v in ys])
-    loss = torch.nn.functional.cross_entropy(lin(top), y, reduction="mean")
+    if ctc_targets is None:
+        y = torch.cat([torch.tensor(np.asarray(v)) for v in ys])
+        loss = torch.nn.functional.cross_entropy(lin(top), y, reduction="mean")
+    else:
+        # CTC, mean over sequences: torch's ctc_loss summed, divided by the count
+        lp = torch.nn.utils.rnn.pad_sequence([torch.log_softmax(lin(t), dim=1) for t in tops])
+        tg = torch.cat([torch.tensor(np.asarray(t), dtype=torch.long) for t in ctc_targets])
+        tl = torch.tensor([len(t) for t in ctc_targets])
+        loss = torch.nn.functional.ctc_loss(lp, tg, lengths, tl, blank=0, reduction="sum",
+                                            zero_infinity=False) / len(xs)
     loss.backward()
     grads = {}
     for l in range(m.num_layers):
@@ -95,6 +103,45 @@ def test_matches_torch_float64(mi):
         np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
     assert abs(loss - tloss) < 1e-12
     np.testing.assert_allclose(grad, tgrad, rtol=0, atol=1e-10)
+
+
+def _rand_targets(rng, lengths, C):
+    return [rng.integers(1, C, max(1, L // 3)) for L in lengths]
+
+
+@pytest.mark.parametrize("mi", range(len(MODELS)))
+def test_ctc_matches_torch_float64(mi):
+    """The model with the CTC loss against PyTorch's LSTM/GRU + ctc_loss."""
+    m = MODELS[mi]
+    rng = np.random.default_rng(40 + mi)
+    theta = rng.uniform(-0.5, 0.5, rnn.param_count(m))
+    lengths = [9, 7, 7, 3, 1]
+    xs, ys = _rand_batch(rng, lengths, m.input_dim, m.num_classes)
+    tg = _rand_targets(rng, lengths, m.num_classes)
+    loss, grad, _ = rnn.forward_backward(m, theta, xs, ys, ctc_targets=tg)
+    tloss, tgrad, _ = _torch_loss_grad(m, theta, xs, ys, ctc_targets=tg)
+    assert abs(loss - tloss) < 1e-11 * abs(tloss)
+    np.testing.assert_allclose(grad, tgrad, rtol=0, atol=1e-10)
+
+
+@pytest.mark.parametrize("mi", [0, 3])
+def test_ctc_finite_differences(mi):
+    m = MODELS[mi]
+    rng = np.random.default_rng(50 + mi)
+    theta = rng.uniform(-0.5, 0.5, rnn.param_count(m))
+    lengths = [6, 4, 2]
+    xs, ys = _rand_batch(rng, lengths, m.input_dim, m.num_classes)
+    tg = _rand_targets(rng, lengths, m.num_classes)
+    _, grad, _ = rnn.forward_backward(m, theta, xs, ys, ctc_targets=tg)
+    h = 1e-6
+    fd = np.zeros_like(theta)
+    for k in range(theta.size):
+        tp = theta.copy(); tp[k] += h
+        tm = theta.copy(); tm[k] -= h
+        fd[k] = (rnn.forward_backward(m, tp, xs, ys, False, tg)[0]
+                 - rnn.forward_backward(m, tm, xs, ys, False, tg)[0]) / (2 * h)
+    err = np.abs(fd - grad) / np.maximum(np.abs(grad), 1e-3)
+    assert err.max() < 1e-6, err.max()
 
 
 @pytest.mark.parametrize("mi", range(len(MODELS)))
