@@ -58,36 +58,35 @@ def ctc_loss_grad(z, target):
     # the skip transition s-2 -> s is allowed into a label differing from l'_{s-2}
     skip = np.zeros(S, bool)
     skip[2:] = (ext[2:] != BLANK) & (ext[2:] != ext[:-2])
+    emit = lp[:, ext]                                 # ln y_t(l'_s)  [T, S]
     la = np.full((T, S), NEG)
-    la[0, 0] = lp[0, ext[0]]
+    la[0, 0] = emit[0, 0]
     if S > 1:
-        la[0, 1] = lp[0, ext[1]]
+        la[0, 1] = emit[0, 1]
     for t in range(1, T):
-        for s in range(S):
-            terms = [la[t - 1, s]]
-            if s >= 1:
-                terms.append(la[t - 1, s - 1])
-            if skip[s]:
-                terms.append(la[t - 1, s - 2])
-            la[t, s] = _logsumexp(np.array(terms)) + lp[t, ext[s]]
+        prev = la[t - 1]
+        stay = prev                                                  # s -> s
+        step = np.concatenate(([NEG], prev[:-1]))                    # s-1 -> s
+        jump = np.where(skip, np.concatenate(([NEG, NEG], prev[:-2])), NEG)  # s-2 -> s
+        la[t] = np.logaddexp(np.logaddexp(stay, step), jump) + emit[t]
+    # the transition s -> s+2 exists where the skip into s+2 does
+    skip_from = np.concatenate((skip[2:], [False, False]))
     lb = np.full((T, S), NEG)
-    lb[T - 1, S - 1] = lp[T - 1, ext[S - 1]]
+    lb[T - 1, S - 1] = emit[T - 1, S - 1]
     if S > 1:
-        lb[T - 1, S - 2] = lp[T - 1, ext[S - 2]]
+        lb[T - 1, S - 2] = emit[T - 1, S - 2]
     for t in range(T - 2, -1, -1):
-        for s in range(S):
-            terms = [lb[t + 1, s]]
-            if s + 1 < S:
-                terms.append(lb[t + 1, s + 1])
-            if s + 2 < S and skip[s + 2]:
-                terms.append(lb[t + 1, s + 2])
-            lb[t, s] = _logsumexp(np.array(terms)) + lp[t, ext[s]]
+        nxt = lb[t + 1]
+        stay = nxt                                                   # s <- s
+        step = np.concatenate((nxt[1:], [NEG]))                      # s <- s+1
+        jump = np.where(skip_from, np.concatenate((nxt[2:], [NEG, NEG])), NEG)  # s <- s+2
+        lb[t] = np.logaddexp(np.logaddexp(stay, step), jump) + emit[t]
     ends = [la[T - 1, S - 1]] + ([la[T - 1, S - 2]] if S > 1 else [])
     lnp = _logsumexp(np.array(ends))
     if not np.isfinite(lnp):
         return np.inf, np.zeros_like(z)
     # occupancy of each extended state: alpha beta / y, normalised by p
-    occ = np.exp(la + lb - lp[:, ext] - lnp)
+    occ = np.exp(la + lb - emit - lnp)
     grad = np.exp(lp)
     for s in range(S):
         grad[:, ext[s]] -= occ[:, s]
