@@ -182,6 +182,48 @@ int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* params,
                         size_t workspace_bytes, float* loss, void* stream);
 
 /*
+ * rnnbkt_ctc_workspace_bytes -- bytes of the extra caller-owned device
+ * workspace rnnbkt_lstm_fwd_ctc needs for batches of up to T_max frames,
+ * B sequences and U_max labels per target (scratch; nothing carried between
+ * calls).  Errors: EINVAL (non-positive sizes), EUNSUPPORTED (U_max > 1023).
+ */
+int32_t rnnbkt_ctc_workspace_bytes(int32_t T_max, int32_t B, int32_t U_max, size_t* bytes);
+
+/*
+ * rnnbkt_lstm_fwd_ctc -- rnnbkt_lstm_fwd with the connectionist temporal
+ * classification loss, the cost the paper trains with (Sec. IV.A), in place
+ * of the per-frame loss.  Class 0 of the output layer is the blank; each
+ * sequence has an unaligned target string over classes 1..num_classes-1.
+ *
+ *   targets         device int32[B][U_max]: row b holds sequence b's labels
+ *                   in its first target_lengths[b] entries (the rest are
+ *                   never read); a label outside 1..num_classes-1 is clamped
+ *                   into that range (device data is not checked)
+ *   target_lengths  host int32[B], 1 <= target_lengths[b] <= min(U_max,
+ *                   lengths[b])
+ *   ctc_ws          device buffer of at least
+ *                   rnnbkt_ctc_workspace_bytes(T_max, B, U_max) bytes,
+ *                   16-byte aligned
+ *   loss            device fp32[1] out: mean over the B sequences of
+ *                   -ln p(target | x), p summing over every frame path that
+ *                   collapses to the target (repeats merged, blanks dropped)
+ * Other arguments as in rnnbkt_lstm_fwd (no per-frame labels).  The loss
+ * gradient w.r.t. the logits is kept in reserve, so rnnbkt_lstm_bwd follows
+ * unchanged.  A target no path of its sequence's length can produce (equal
+ * neighbours need a blank between them) gives an infinite loss and zero
+ * gradient rows for that sequence.  Probabilities are renormalised every
+ * frame in fp32; the per-sequence log-likelihood is summed in fp64.
+ * Errors: as rnnbkt_lstm_fwd, plus EINVAL (bad target lengths, ctc_ws too
+ * small) and EUNSUPPORTED (U_max > 1023).
+ */
+int32_t rnnbkt_lstm_fwd_ctc(const rnnbkt_model_desc* desc, const float* params, const float* x,
+                            const int32_t* targets, const int32_t* target_lengths,
+                            int32_t U_max, const int32_t* lengths, int32_t T_max, int32_t B,
+                            void* reserve, size_t reserve_bytes, void* workspace,
+                            size_t workspace_bytes, void* ctc_ws, size_t ctc_ws_bytes,
+                            float* loss, void* stream);
+
+/*
  * rnnbkt_lstm_bwd -- backpropagation through time of the batch last run
  * through rnnbkt_lstm_fwd with the same (desc, params, x, lengths, reserve).
  *   grads   device fp32[param_count] out: d loss / d params (overwritten
@@ -246,7 +288,7 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
 #define RNNBKT_KERNEL_STEP_FWD 0 /* recurrent step, forward */
 #define RNNBKT_KERNEL_STEP_BWD 1 /* recurrent step, backward through time */
 #define RNNBKT_KERNEL_GEMM 2     /* dense contractions incl. split-K folds */
-#define RNNBKT_KERNEL_XENT 3     /* softmax cross-entropy and its gradient */
+#define RNNBKT_KERNEL_XENT 3     /* output loss and its gradient (cross-entropy or CTC) */
 #define RNNBKT_KERNEL_SGD 4      /* parameter update (SGD or ADADELTA) */
 #define RNNBKT_KERNEL_OTHER 5    /* batch tables, packing, column sums, loss sum */
 #define RNNBKT_KERNEL_KINDS 6

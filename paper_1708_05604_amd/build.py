@@ -20,7 +20,8 @@ LIB = os.path.join(PKG, "librnnbkt.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["gemm.hip", "rnn_step.hip", "rnn_persistent.hip", "elementwise.hip", "api.hip"]
+HIP_SOURCES = ["gemm.hip", "rnn_step.hip", "rnn_persistent.hip", "elementwise.hip", "ctc.hip",
+               "api.hip"]
 CXX_SOURCES = ["plan.cpp"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-I", os.path.join(ROOT, "include"), "-I", CSRC]

@@ -367,11 +367,47 @@ extern "C" int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_
   return RNNBKT_OK;
 }
 
-extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* params,
-                                   const float* x, const int32_t* labels,
-                                   const int32_t* lengths, int32_t T, int32_t B, void* reserve,
-                                   size_t reserve_bytes, void* workspace,
-                                   size_t workspace_bytes, float* loss, void* stream) {
+namespace {
+
+// CTC scratch of a batch: per-sequence table (target and sequence lengths),
+// emission probabilities / occupancy sums and forward variables
+// [B][T][S_stride], per-frame log-sum-exp, per-sequence losses.
+struct CtcCarve {
+  size_t tab, e, alpha, lse, loss_part, total;
+  int S_stride;
+};
+
+CtcCarve ctc_carve(int T, int B, int U_max) {
+  CtcCarve c{};
+  c.S_stride = 64 * ctc_states_per_lane(U_max);
+  size_t pos = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = pos;
+    pos = align_up(pos + bytes);
+    return at;
+  };
+  const size_t rows = (size_t)B * T * c.S_stride;
+  c.tab = take(sizeof(int32_t) * 2 * B);
+  c.e = take(sizeof(float) * rows);
+  c.alpha = take(sizeof(float) * rows);
+  c.lse = take(sizeof(float) * (size_t)B * T);
+  c.loss_part = take(sizeof(float) * B);
+  c.total = pos;
+  return c;
+}
+
+struct CtcInputs {
+  const int32_t* targets;
+  const int32_t* target_lengths;
+  int32_t U_max;
+  void* ws;
+  size_t ws_bytes;
+};
+
+int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float* x,
+                const int32_t* labels, const CtcInputs* ctc, const int32_t* lengths, int32_t T,
+                int32_t B, void* reserve, size_t reserve_bytes, void* workspace,
+                size_t workspace_bytes, float* loss, void* stream) {
   clear_error();
   Shape s;
   int32_t rc = check_desc(desc, &s);
@@ -379,8 +415,26 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   int64_t N = 0;
   rc = check_lengths(lengths, T, B, &N);
   if (rc != RNNBKT_OK) return rc;
-  RNNBKT_REQUIRE(params && x && labels && reserve && workspace && loss, RNNBKT_EINVAL,
+  RNNBKT_REQUIRE(params && x && (labels || ctc) && reserve && workspace && loss, RNNBKT_EINVAL,
                  "lstm_fwd: null pointer");
+  CtcCarve cc{};
+  if (ctc) {
+    RNNBKT_REQUIRE(ctc->targets && ctc->target_lengths && ctc->ws, RNNBKT_EINVAL,
+                   "lstm_fwd_ctc: null pointer");
+    RNNBKT_REQUIRE(ctc->U_max >= 1, RNNBKT_EINVAL, "lstm_fwd_ctc: U_max must be >= 1");
+    RNNBKT_REQUIRE(ctc_states_per_lane(ctc->U_max) > 0, RNNBKT_EUNSUPPORTED,
+                   "lstm_fwd_ctc: targets longer than 1023 labels are not supported");
+    RNNBKT_REQUIRE(aligned16(ctc->ws), RNNBKT_EINVAL, "lstm_fwd_ctc: ctc_ws must be 16-byte aligned");
+    for (int b = 0; b < B; ++b)
+      RNNBKT_REQUIRE(ctc->target_lengths[b] >= 1 && ctc->target_lengths[b] <= ctc->U_max &&
+                         ctc->target_lengths[b] <= lengths[b],
+                     RNNBKT_EINVAL,
+                     "lstm_fwd_ctc: target_lengths[%d] = %d outside [1, min(U_max %d, length %d)]",
+                     b, ctc->target_lengths[b], ctc->U_max, lengths[b]);
+    cc = ctc_carve(T, B, ctc->U_max);
+    RNNBKT_REQUIRE(ctc->ws_bytes >= cc.total, RNNBKT_EINVAL,
+                   "lstm_fwd_ctc: ctc_ws too small (%zu < %zu)", ctc->ws_bytes, cc.total);
+  }
   RNNBKT_REQUIRE(aligned16(params) && aligned16(x) && aligned16(reserve) && aligned16(workspace),
                  RNNBKT_EINVAL, "lstm_fwd: params, x, reserve and workspace must be 16-byte aligned");
   const Carve c = carve(s, T, B, N);
@@ -405,7 +459,10 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
     RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
-    RNNBKT_HIP(launch_pack(x, labels, d_bs, d_off, T, B, s.D, Xp, Yp, pf, pr, st));
+    // The CTC loss has no per-frame labels: nothing to pack (k_pack reads
+    // labels only when given somewhere to put them).
+    RNNBKT_HIP(launch_pack(x, ctc ? nullptr : labels, d_bs, d_off, T, B, s.D, Xp,
+                           ctc ? nullptr : Yp, pf, pr, st));
   }
 
   const int GH = s.G * s.H;
@@ -536,6 +593,37 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
   RNNBKT_HIP(gemm(top, s.Htop, true, params + po.wout, s.Htop, true, dz, s.C, (int)N, s.C,
                   s.Htop, params + po.bout, 0, s.bf16, st));
+  if (ctc) {
+    CtcArgs a{};
+    a.z = dz;
+    a.C = s.C;
+    a.bs = d_bs;
+    a.off = d_off;
+    a.T = T;
+    a.B = B;
+    a.targets = ctc->targets;
+    a.U_max = ctc->U_max;
+    int32_t* tab = at<int32_t>(ctc->ws, cc.tab);
+    a.tab = tab;
+    a.S_stride = cc.S_stride;
+    a.e = at<float>(ctc->ws, cc.e);
+    a.alpha = at<float>(ctc->ws, cc.alpha);
+    a.lse = at<float>(ctc->ws, cc.lse);
+    a.loss_part = at<float>(ctc->ws, cc.loss_part);
+    a.scale = 1.0f / (float)B;
+    {
+      Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+      RNNBKT_HIP(launch_store_ints(ctc->target_lengths, B, tab, st));
+      RNNBKT_HIP(launch_store_ints(lengths, B, tab + B, st));
+    }
+    {
+      Timed tm(RNNBKT_KERNEL_XENT, 0.0, (8.0 * s.C + 4.0) * N, st);
+      RNNBKT_HIP(launch_ctc(a, st));
+    }
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    RNNBKT_HIP(launch_sum(a.loss_part, B, 1.0f / (float)B, loss, st));
+    return RNNBKT_OK;
+  }
   int32_t nparts = 0;
   {
     Timed tm(RNNBKT_KERNEL_XENT, 0.0, (8.0 * s.C + 4.0) * N, st);
@@ -546,6 +634,43 @@ extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* p
     RNNBKT_HIP(launch_sum(lp, nparts, 1.0f / (float)N, loss, st));
   }
   return RNNBKT_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t rnnbkt_lstm_fwd(const rnnbkt_model_desc* desc, const float* params,
+                                   const float* x, const int32_t* labels,
+                                   const int32_t* lengths, int32_t T, int32_t B, void* reserve,
+                                   size_t reserve_bytes, void* workspace,
+                                   size_t workspace_bytes, float* loss, void* stream) {
+  return forward(desc, params, x, labels, nullptr, lengths, T, B, reserve, reserve_bytes,
+                 workspace, workspace_bytes, loss, stream);
+}
+
+extern "C" int32_t rnnbkt_ctc_workspace_bytes(int32_t T_max, int32_t B, int32_t U_max,
+                                              size_t* bytes) {
+  clear_error();
+  RNNBKT_REQUIRE(bytes, RNNBKT_EINVAL, "ctc_workspace_bytes: null pointer");
+  RNNBKT_REQUIRE(T_max >= 1 && B >= 1 && U_max >= 1, RNNBKT_EINVAL,
+                 "ctc_workspace_bytes: T_max, B and U_max must be >= 1");
+  RNNBKT_REQUIRE(ctc_states_per_lane(U_max) > 0, RNNBKT_EUNSUPPORTED,
+                 "ctc_workspace_bytes: targets longer than 1023 labels are not supported");
+  *bytes = ctc_carve(T_max, B, U_max).total;
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_lstm_fwd_ctc(const rnnbkt_model_desc* desc, const float* params,
+                                       const float* x, const int32_t* targets,
+                                       const int32_t* target_lengths, int32_t U_max,
+                                       const int32_t* lengths, int32_t T, int32_t B,
+                                       void* reserve, size_t reserve_bytes, void* workspace,
+                                       size_t workspace_bytes, void* ctc_ws, size_t ctc_ws_bytes,
+                                       float* loss, void* stream) {
+  clear_error();
+  RNNBKT_REQUIRE(target_lengths, RNNBKT_EINVAL, "lstm_fwd_ctc: null pointer");
+  const CtcInputs ctc{targets, target_lengths, U_max, ctc_ws, ctc_ws_bytes};
+  return forward(desc, params, x, nullptr, &ctc, lengths, T, B, reserve, reserve_bytes, workspace,
+                 workspace_bytes, loss, stream);
 }
 
 extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,

@@ -17,6 +17,11 @@ struct LenChunk {
   int32_t len[kLenChunk];
 };
 
+__global__ void k_store_ints(LenChunk c, int count, int32_t* dst) {
+  const int i = threadIdx.x;
+  if (i < count) dst[i] = c.len[i];
+}
+
 // batch_sizes[t] (+)= #{b in chunk : len[b] > t}
 __global__ void k_batch_sizes(LenChunk c, int count, int T, int32_t* bs, int first) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
@@ -227,6 +232,18 @@ hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned v, hipStream_t st) {
   hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads),
                      0, st, p, n, v);
   return hipGetLastError();
+}
+
+hipError_t launch_store_ints(const int32_t* values, int n, int32_t* dst, hipStream_t st) {
+  for (int c0 = 0; c0 < n; c0 += kLenChunk) {
+    LenChunk c{};
+    const int cnt = std::min(kLenChunk, n - c0);
+    for (int i = 0; i < cnt; ++i) c.len[i] = values[c0 + i];
+    hipLaunchKernelGGL(k_store_ints, dim3(1), dim3(kLenChunk), 0, st, c, cnt, dst + c0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_batch_tables(const int32_t* lengths, int32_t B, int32_t T, int32_t* bs,

@@ -89,6 +89,37 @@ hipError_t launch_sum(const float* partial, int32_t n, float scale, float* out,
 
 hipError_t launch_sgd(float* params, const float* grads, int64_t n, float lr,
                       hipStream_t stream);
+// ---------------------------------------------------------------- CTC
+// Loss and logit gradient of a batch (packed frames, class 0 = blank).
+//   z        [N x C] logits in, gradient d loss / d logits out (x scale)
+//   targets  device int32 [B][U_max] label strings
+//   tab      device int32 [2B]: target lengths, then sequence lengths
+//   e, alpha device [B][T][S_stride] scratch (S_stride = 64 * states per
+//            lane, see ctc_states_per_lane); lse [N]; loss_part [B] out
+//            (per-sequence -ln p, +inf when no path exists)
+struct CtcArgs {
+  float* z;
+  int C;
+  const int32_t* bs;
+  const int32_t* off;
+  int T, B;
+  const int32_t* targets;
+  int U_max;
+  const int32_t* tab;
+  int S_stride;
+  float* e;
+  float* alpha;
+  float* lse;
+  float* loss_part;
+  float scale;
+};
+// States per lane of the sequential kernel for targets of up to U_max
+// labels (a power of two, 0 if above 32).
+int ctc_states_per_lane(int U_max);
+hipError_t launch_ctc(const CtcArgs& a, hipStream_t st);
+// dst[i] = values[i] for i < n, from host memory through kernel arguments.
+hipError_t launch_store_ints(const int32_t* values, int n, int32_t* dst, hipStream_t st);
+
 // One ADADELTA step over n elements (p, eg2, edx2 updated in place).
 hipError_t launch_adadelta(float* p, const float* g, float* eg2, float* edx2, int64_t n,
                            float rho, float eps, float lr, hipStream_t st);

@@ -73,6 +73,12 @@ _SIGNATURES = {
     "rnnbkt_lstm_fwd": (ctypes.c_int32, [_descp, _vp, _vp, _vp, _i32p, ctypes.c_int32,
                                          ctypes.c_int32, _vp, ctypes.c_size_t, _vp,
                                          ctypes.c_size_t, _vp, _vp]),
+    "rnnbkt_ctc_workspace_bytes": (ctypes.c_int32, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                    _szp]),
+    "rnnbkt_lstm_fwd_ctc": (ctypes.c_int32, [_descp, _vp, _vp, _vp, _i32p, ctypes.c_int32, _i32p,
+                                             ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_size_t,
+                                             _vp, ctypes.c_size_t, _vp, ctypes.c_size_t, _vp,
+                                             _vp]),
     "rnnbkt_lstm_bwd": (ctypes.c_int32, [_descp, _vp, _i32p, ctypes.c_int32, ctypes.c_int32,
                                          _vp, ctypes.c_size_t, _vp, ctypes.c_size_t, _vp, _vp]),
     "rnnbkt_sgd_apply": (ctypes.c_int32, [_vp, _vp, ctypes.c_int64, ctypes.c_float, _vp]),
@@ -237,6 +243,34 @@ def lstm_fwd(desc, params, x, labels, lengths, reserve, workspace, loss, stream=
                                   int(L[0]), int(L.size), _dev(reserve), _nbytes(reserve),
                                   _dev(workspace), _nbytes(workspace), _dev(loss, "float32"),
                                   _stream(stream)))
+
+
+def ctc_workspace_bytes(T_max: int, B: int, U_max: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().rnnbkt_ctc_workspace_bytes(int(T_max), int(B), int(U_max), ctypes.byref(n)))
+    return n.value
+
+
+def lstm_fwd_ctc(desc, params, x, targets, target_lengths, lengths, reserve, workspace, ctc_ws,
+                 loss, stream=None):
+    """Forward pass with the CTC loss.  targets: device int32 [B, U_max]
+    (row b's first target_lengths[b] entries hold its labels)."""
+    L = _i32(lengths)
+    TL = _i32(target_lengths)
+    T, B = int(L[0]), int(L.size)
+    if TL.size != B:
+        raise ValueError("target_lengths must have one entry per sequence")
+    if targets.dim() != 2 or targets.shape[0] != B:
+        raise ValueError("targets must be [B, U_max]")
+    U_max = int(targets.shape[1])
+    _need(params, param_count(desc), "params")
+    _need(x, T * B * desc.input_dim, "x")
+    _need(loss, 1, "loss")
+    _check(load().rnnbkt_lstm_fwd_ctc(ctypes.byref(desc), _dev(params, "float32"),
+                                      _dev(x, "float32"), _dev(targets, "int32"), _ptr(TL, _i32p),
+                                      U_max, _ptr(L, _i32p), T, B, _dev(reserve), _nbytes(reserve),
+                                      _dev(workspace), _nbytes(workspace), _dev(ctc_ws),
+                                      _nbytes(ctc_ws), _dev(loss, "float32"), _stream(stream)))
 
 
 def lstm_bwd(desc, params, lengths, reserve, workspace, grads, stream=None):

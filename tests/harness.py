@@ -61,10 +61,14 @@ def batch_order(data: synth.Data, idx):
     return np.asarray(idx, np.int64)
 
 
-def oracle_batch(spec: Spec, params, data: synth.Data, order):
+def oracle_batch(spec: Spec, params, data: synth.Data, order, targets=None):
+    """targets: per-sequence CTC label strings (indexed like the data), or
+    None for the per-frame loss."""
     xs = [data.X[data.offsets[s]:data.offsets[s + 1]] for s in order]
     ys = [data.Y[data.offsets[s]:data.offsets[s + 1]] for s in order]
-    loss, grad, tops = orn.forward_backward(spec.model(), np.asarray(params, np.float64), xs, ys)
+    tg = None if targets is None else [targets[s] for s in order]
+    loss, grad, tops = orn.forward_backward(spec.model(), np.asarray(params, np.float64), xs, ys,
+                                            ctc_targets=tg)
     lens = data.lengths[order]
     top = np.zeros((int(lens.max()), len(order), spec.htop))
     for b, t in enumerate(tops):
@@ -76,7 +80,7 @@ class GpuBatch:
     """Device buffers of one batch and the library calls on them."""
 
     def __init__(self, spec: Spec, params, data: synth.Data, order, pad_fill=0.0,
-                 device="cuda"):
+                 device="cuda", targets=None):
         import torch
         self.torch = torch
         self.spec = spec
@@ -98,10 +102,25 @@ class GpuBatch:
         self.loss = torch.full((1,), float("nan"), dtype=torch.float32, device=device)
         self.top = torch.full((T, B, spec.htop), float("nan"), dtype=torch.float32,
                               device=device)
+        self.ctc = targets is not None
+        if self.ctc:
+            tg = [np.asarray(targets[s], np.int32) for s in order]
+            self.target_lengths = np.array([len(t) for t in tg], np.int32)
+            U_max = int(self.target_lengths.max())
+            tmat = np.full((B, U_max), -5, np.int32)  # entries past a target are never read
+            for b, t in enumerate(tg):
+                tmat[b, :len(t)] = t
+            self.targets = torch.from_numpy(tmat).to(device)
+            nb = lib.ctc_workspace_bytes(T, B, U_max)
+            self.ctc_ws = torch.empty(nb, dtype=torch.uint8, device=device)
 
     def forward(self):
-        lib.lstm_fwd(self.desc, self.params, self.x, self.y, self.lens, self.reserve,
-                     self.workspace, self.loss)
+        if self.ctc:
+            lib.lstm_fwd_ctc(self.desc, self.params, self.x, self.targets, self.target_lengths,
+                             self.lens, self.reserve, self.workspace, self.ctc_ws, self.loss)
+        else:
+            lib.lstm_fwd(self.desc, self.params, self.x, self.y, self.lens, self.reserve,
+                         self.workspace, self.loss)
         lib.top_hidden(self.desc, self.lens, self.reserve, self.top)
 
     def backward(self):
@@ -140,14 +159,14 @@ def block_errors(spec: Spec, g_gpu, g_ref):
     return out
 
 
-def assert_batch_close(spec: Spec, params, data, order, rtol=None, label=""):
+def assert_batch_close(spec: Spec, params, data, order, rtol=None, label="", targets=None):
     rtol = RTOL[spec.gemm_dtype] if rtol is None else rtol
-    print(f"[case] {label} spec={spec} B={len(order)} T={int(data.lengths[order].max())}",
-          flush=True)
-    gb = GpuBatch(spec, params, data, order)
+    print(f"[case] {label} spec={spec} B={len(order)} T={int(data.lengths[order].max())}"
+          + (" ctc" if targets is not None else ""), flush=True)
+    gb = GpuBatch(spec, params, data, order, targets=targets)
     loss_g, grad_g, top_g = gb.run()
     assert np.all(np.isfinite(grad_g)), "non-finite gradient (unwritten entries?)"
-    loss_r, grad_r, top_r = oracle_batch(spec, params, data, order)
+    loss_r, grad_r, top_r = oracle_batch(spec, params, data, order, targets=targets)
     lens = data.lengths[order]
     for b, L in enumerate(lens):
         bad = np.nonzero(np.any(top_g[L:, b] != 0.0, axis=-1))[0]
