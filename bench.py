@@ -94,7 +94,7 @@ def describe(w: synth.Workload, K: int) -> str:
 class Epoch:
     """One epoch's batches staged on the GPU."""
 
-    def __init__(self, w, data, K, epoch, torch, dev):
+    def __init__(self, w, data, K, epoch, torch, dev, targets=None):
         t0 = time.perf_counter()
         self.upper, bof, self.keff, self.p_bucket = lib.bucket_plan(data.lengths, K)
         self.plan_ms = (time.perf_counter() - t0) * 1e3
@@ -114,6 +114,17 @@ class Epoch:
             self.p_batch += len(L) * int(L[0])
             bt = np.bincount(L, minlength=int(L[0]) + 1)[::-1].cumsum()[::-1][1:]
             self.p_exec += int(np.sum((bt + TILE_M - 1) // TILE_M * TILE_M))
+        # CTC label strings per batch ([B, U_max] device tensor, host lengths)
+        self.tg, self.tl = [], []
+        if targets is not None:
+            for order in self.batches:
+                tl = np.array([len(targets[s]) for s in order], np.int32)
+                tm = np.zeros((len(order), int(tl.max())), np.int32)
+                for b, s in enumerate(order):
+                    tm[b, :tl[b]] = targets[s]
+                self.tg.append(torch.from_numpy(tm).to(dev))
+                self.tl.append(tl)
+        self.max_U = max((int(t.max()) for t in self.tl), default=0)
         self.U = int(sum(self.useful))
         self.max_T = max(int(L[0]) for L in self.lens)
         self.max_B = max(len(L) for L in self.lens)
@@ -121,12 +132,16 @@ class Epoch:
 
 
 def run_steps(ep, state, first, count, torch):
-    desc, params, grads, reserve, workspace, loss, lr, opt = state
+    desc, params, grads, reserve, workspace, loss, lr, opt, ctc_ws = state
     useful = 0
     nb = len(ep.batches)
     for k in range(count):
         i = (first + k) % nb
-        lib.lstm_fwd(desc, params, ep.x[i], ep.y[i], ep.lens[i], reserve, workspace, loss)
+        if ctc_ws is None:
+            lib.lstm_fwd(desc, params, ep.x[i], ep.y[i], ep.lens[i], reserve, workspace, loss)
+        else:
+            lib.lstm_fwd_ctc(desc, params, ep.x[i], ep.tg[i], ep.tl[i], ep.lens[i], reserve,
+                             workspace, ctc_ws, loss)
         lib.lstm_bwd(desc, params, ep.lens[i], reserve, workspace, grads)
         if opt is None:
             lib.sgd_apply(params, grads, lr)
@@ -149,7 +164,7 @@ def timed(ep, state, warmup, steps, torch):
     return useful, a.elapsed_time(b) / 1e3
 
 
-def cpu_baseline(w, data, ep, budget_s=15.0):
+def cpu_baseline(w, data, ep, budget_s=15.0, targets=None):
     """The float64 oracle on the host: first batch of each bucket in turn
     until about `budget_s` seconds of work, BLAS pinned to one thread."""
     from threadpoolctl import threadpool_limits
@@ -170,7 +185,8 @@ def cpu_baseline(w, data, ep, budget_s=15.0):
             xs = [data.X[data.offsets[s]:data.offsets[s + 1]] for s in order]
             ys = [data.Y[data.offsets[s]:data.offsets[s + 1]] for s in order]
             t0 = time.perf_counter()
-            _, g, _ = orn.forward_backward(m, theta, xs, ys)
+            tg = None if targets is None else [targets[s] for s in order]
+            _, g, _ = orn.forward_backward(m, theta, xs, ys, ctc_targets=tg)
             orn.sgd(theta, g, 0.1)
             t_total += time.perf_counter() - t0
             useful += int(sum(len(y) for y in ys))
@@ -190,6 +206,9 @@ def main(argv=None):
     ap.add_argument("--workload", default="lstm2", choices=list(synth.WORKLOADS))
     ap.add_argument("--K", type=int, default=0, help="buckets (0 = largest of the workload)")
     ap.add_argument("--lr", type=float, default=0.1, help="SGD step size")
+    ap.add_argument("--loss", default="frame", choices=("frame", "ctc"),
+                    help="per-frame cross-entropy, or CTC over synthetic label strings "
+                         "(one label per 8 frames)")
     ap.add_argument("--optimizer", default="sgd", choices=("sgd", "adadelta"),
                     help="parameter update of each step (adadelta: rho 0.95, eps 1e-6)")
     ap.add_argument("--no-k1", action="store_true", help="skip the K=1 epoch")
@@ -225,8 +244,9 @@ def main(argv=None):
         torch.cuda.synchronize()
         del cp, cg
 
-    ep = Epoch(w, data, K, 0, torch, dev)
-    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev)
+    targets = synth.ctc_targets(data.lengths, w.num_classes, 0) if args.loss == "ctc" else None
+    ep = Epoch(w, data, K, 0, torch, dev, targets)
+    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev, targets)
     eps = [e for e in (ep, ep1) if e is not None]
     rb, wb = lib.buffer_sizes(desc, max(e.max_T for e in eps), max(e.max_B for e in eps),
                               max(e.max_N for e in eps))
@@ -238,7 +258,12 @@ def main(argv=None):
     opt = None
     if args.optimizer == "adadelta":
         opt = (torch.zeros_like(params), torch.zeros_like(params))
-    state = (desc, params, grads, reserve, workspace, loss, args.lr, opt)
+    ctc_ws = None
+    if targets is not None:
+        nbytes = lib.ctc_workspace_bytes(max(e.max_T for e in eps), max(e.max_B for e in eps),
+                                         max(e.max_U for e in eps))
+        ctc_ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    state = (desc, params, grads, reserve, workspace, loss, args.lr, opt, ctc_ws)
 
     nb = len(ep.batches)
     steps = args.steps or nb
@@ -253,7 +278,8 @@ def main(argv=None):
         "warmup": warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.gemm_dtype == synth.BF16 else "f32", "data": "synthetic",
-        "config": {"workload": describe(w, K), "optimizer": args.optimizer, "batches_per_epoch": nb,
+        "config": {"workload": describe(w, K), "loss": args.loss, "optimizer": args.optimizer,
+                   "batches_per_epoch": nb,
                    "useful_timesteps_per_epoch": ep.U, "parallelism": "single GPU"},
         "mfma_util_pct": 100.0 * flops * value / (peak * 1e12),
         "achieved_tflops": flops * value / 1e12,
@@ -296,7 +322,7 @@ def main(argv=None):
                               "avg_us": 1e3 * v["ms"] / max(v["launches"], 1)}
                           for k, v in kinds.items()}
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(w, data, ep)
+        out["cpu_baseline"] = cpu_baseline(w, data, ep, targets=targets)
     print(json.dumps(out), flush=True)
     return 0
 

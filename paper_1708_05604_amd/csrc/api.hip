@@ -370,10 +370,10 @@ extern "C" int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_
 namespace {
 
 // CTC scratch of a batch: per-sequence table (target and sequence lengths),
-// emission probabilities / occupancy sums and forward variables
-// [B][T][S_stride], per-frame log-sum-exp, per-sequence losses.
+// log emissions and the two log recursions [B][T][S_stride], label chains,
+// per-frame log-sum-exp, per-sequence losses.
 struct CtcCarve {
-  size_t tab, e, alpha, lse, loss_part, total;
+  size_t tab, e, alpha, beta, chain, lse, loss_part, total;
   int S_stride;
 };
 
@@ -390,6 +390,8 @@ CtcCarve ctc_carve(int T, int B, int U_max) {
   c.tab = take(sizeof(int32_t) * 2 * B);
   c.e = take(sizeof(float) * rows);
   c.alpha = take(sizeof(float) * rows);
+  c.beta = take(sizeof(float) * rows);
+  c.chain = take(sizeof(int32_t) * 2 * (size_t)B * U_max);
   c.lse = take(sizeof(float) * (size_t)B * T);
   c.loss_part = take(sizeof(float) * B);
   c.total = pos;
@@ -608,6 +610,8 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     a.S_stride = cc.S_stride;
     a.e = at<float>(ctc->ws, cc.e);
     a.alpha = at<float>(ctc->ws, cc.alpha);
+    a.beta = at<float>(ctc->ws, cc.beta);
+    a.chain = at<int32_t>(ctc->ws, cc.chain);
     a.lse = at<float>(ctc->ws, cc.lse);
     a.loss_part = at<float>(ctc->ws, cc.loss_part);
     a.scale = 1.0f / (float)B;

@@ -43,6 +43,44 @@ __device__ inline float wave_max(float v) {
   return v;
 }
 
+// Cross-lane steps of the sequential kernel as DPP moves (no LDS round trip).
+// dpp<CTRL, ROWS>(fill, v): v from the lane CTRL names; lanes in rows not in
+// ROWS, or with no source lane, get fill.
+template <int CTRL, int ROWS = 0xf>
+__device__ inline float dpp(float fill, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(v), CTRL,
+                                                    ROWS, 0xf, false));
+}
+constexpr int kQuadSwap1 = 0xB1;     // quad_perm (1, 0, 3, 2)
+constexpr int kQuadSwap2 = 0x4E;     // quad_perm (2, 3, 0, 1)
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowMirror = 0x140;
+constexpr int kRowBcast15 = 0x142;
+constexpr int kRowBcast31 = 0x143;
+constexpr int kWaveShl1 = 0x130;     // lane i <- lane i+1
+constexpr int kWaveShr1 = 0x138;     // lane i <- lane i-1
+
+// Sum / maximum over the wave, returned in every lane (the total forms in
+// lane 63 and is read back as a scalar).
+__device__ inline float dpp_wave_sum(float v) {
+  v += dpp<kQuadSwap1>(0.f, v);
+  v += dpp<kQuadSwap2>(0.f, v);
+  v += dpp<kRowHalfMirror>(0.f, v);
+  v += dpp<kRowMirror>(0.f, v);
+  v += dpp<kRowBcast15, 0xa>(0.f, v);
+  v += dpp<kRowBcast31, 0xc>(0.f, v);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ inline float dpp_wave_max(float v) {
+  v = fmaxf(v, dpp<kQuadSwap1>(-INFINITY, v));
+  v = fmaxf(v, dpp<kQuadSwap2>(-INFINITY, v));
+  v = fmaxf(v, dpp<kRowHalfMirror>(-INFINITY, v));
+  v = fmaxf(v, dpp<kRowMirror>(-INFINITY, v));
+  v = fmaxf(v, dpp<kRowBcast15, 0xa>(-INFINITY, v));
+  v = fmaxf(v, dpp<kRowBcast31, 0xc>(-INFINITY, v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
 // Target classes are read from device memory the host cannot check: a value
 // outside 1..C-1 is clamped into that range (wrong numbers, never an access
 // outside the logits).
@@ -115,7 +153,13 @@ __device__ inline void store_row(float* base, int64_t stride, int t, int s0, con
   }
 }
 
-constexpr int kAhead = 4;  // steps between a row's load and its use
+// Steps between a row's load and its use: deep enough to cover a load from
+// HBM at a fraction of a microsecond per step, within the register budget
+// (two queues of D rows of NS floats in the backward pass).
+template <int NS>
+constexpr int ahead() {
+  return NS <= 4 ? 16 : 64 / NS;
+}
 
 // ln(e^x + e^y + e^z) with -inf terms allowed (all -inf gives -inf).
 __device__ inline float log_add3(float x, float y, float z) {
@@ -125,263 +169,200 @@ __device__ inline float log_add3(float x, float y, float z) {
 }
 
 
-// One wave per sequence; lane owns states s0 = lane*NS .. s0+NS-1.
+// Label chains of a target, one entry per label position u: nxt[u] = the
+// next position with the same class (-1: none), head[u] = 1 at the first
+// position of each class.  Written by the forward block of each sequence.
+__device__ inline void build_chains(const CtcArgs& a, int b, const int32_t* tg, int U) {
+  int32_t* nxt = a.chain + (int64_t)b * 2 * a.U_max;
+  int32_t* head = nxt + a.U_max;
+  for (int u = threadIdx.x; u < U; u += 64) {
+    const int k = label_at(a, tg, u);
+    int h = 1;
+    for (int v = 0; v < u; ++v)
+      if (label_at(a, tg, v) == k) {
+        h = 0;
+        break;
+      }
+    int n = -1;
+    for (int v = u + 1; v < U; ++v)
+      if (label_at(a, tg, v) == k) {
+        n = v;
+        break;
+      }
+    nxt[u] = n;
+    head[u] = h;
+  }
+}
+
+// The two recursions of one sequence, one wave each: block b < B runs the
+// forward variables of sequence b over t = 0..L-1, block B + b the backward
+// variables over t = L-1..0.  Both are kept in log space and shifted every
+// step so that their maximum is 0; each stores its rows for the gradient
+// kernel.  Lane owns states s0 = lane*NS .. s0+NS-1.
 template <int NS>
 __global__ __launch_bounds__(64) void k_ctc_seq(CtcArgs a) {
-  constexpr int SP = 64 * NS;
-  __shared__ int lab[SP];     // l'_s (0 past S)
-  __shared__ int nx[SP];      // next state with the same label (-1: none)
-  __shared__ float occ[SP];   // normalised occupancies of the current frame
-  const int b = blockIdx.x;
+  const bool backward = (int)blockIdx.x >= a.B;
+  const int b = backward ? blockIdx.x - a.B : blockIdx.x;
   const int lane = threadIdx.x;
   const int U = a.tab[b], L = a.tab[a.B + b];
   const int S = 2 * U + 1;
   const int s0 = lane * NS;
   const int32_t* tg = a.targets + (int64_t)b * a.U_max;
   const int64_t stride = a.S_stride;
-  float* eb = a.e + (int64_t)b * a.T * stride;
-  float* ab = a.alpha + (int64_t)b * a.T * stride;
+  const float* eb = a.e + (int64_t)b * a.T * stride;
+  float* out = (backward ? a.beta : a.alpha) + (int64_t)b * a.T * stride;
+  if (!backward) build_chains(a, b, tg, U);
 
-  int ext[NS];
+  // skip[i]: the transition between s and s-2 (forward) / s+2 (backward)
+  // exists: the farther state is a label different from the nearer one.
+  // (labels are read only at positions inside the target)
+  bool skip[NS];
 #pragma unroll
   for (int i = 0; i < NS; ++i) {
     const int s = s0 + i;
-    ext[i] = (s < S && (s & 1)) ? label_at(a, tg, s >> 1) : 0;
-    lab[s] = ext[i];
-  }
-  __syncthreads();
-  // into[i]: the transition s-2 -> s exists; from[i]: s -> s+2 exists;
-  // head[i]: s is the first state carrying its label (its lane sums the
-  // class's occupancies along the nx chain, in state order).
-  bool into[NS], from[NS], head[NS];
-#pragma unroll
-  for (int i = 0; i < NS; ++i) {
-    const int s = s0 + i;
+    const int far = backward ? s + 2 : s - 2;
     const bool lbl = s < S && (s & 1);
-    into[i] = lbl && s >= 3 && ext[i] != lab[s - 2];
-    from[i] = s + 2 < S && ((s + 2) & 1) && lab[s + 2] != ext[i];
-    head[i] = lbl;
-    int next = -1;
-    if (lbl) {
-      for (int q = s - 2; q >= 1; q -= 2)
-        if (lab[q] == ext[i]) {
-          head[i] = false;
-          break;
-        }
-      for (int q = s + 2; q < S; q += 2)
-        if (lab[q] == ext[i]) {
-          next = q;
-          break;
-        }
-    }
-    nx[s] = next;
+    skip[i] = lbl && far >= 1 && far < S && label_at(a, tg, far >> 1) != label_at(a, tg, s >> 1);
   }
 
-  // ---- forward variables
-  float al[NS];
+  constexpr int D = ahead<NS>();
+  float q[D][NS];
+  // row of step k (t = k forward, L-1-k backward), clamped inside the sequence
+  auto fetch = [&](int k, float (&v)[NS]) {
+    const int kk = k < L ? k : L - 1;
+    load_row<NS>(eb, stride, backward ? L - 1 - kk : kk, s0, v);
+  };
+#pragma unroll
+  for (int j = 0; j < D; ++j) fetch(j, q[j]);
+  float cur[NS];
   double logc = 0.0;
   bool dead = false;
-  float q0[NS], q1[NS], q2[NS], q3[NS];
-  auto fetch_e = [&](int t, float (&q)[NS]) { load_row<NS>(eb, stride, t < L ? t : L - 1, s0, q); };
-  fetch_e(0, q0);
-  fetch_e(1, q1);
-  fetch_e(2, q2);
-  fetch_e(3, q3);
-  auto fwd_step = [&](int t, const float (&ev)[NS]) {
-    float an[NS];
-    if (t == 0) {
-#pragma unroll
-      for (int i = 0; i < NS; ++i) an[i] = (s0 + i) < 2 ? ev[i] : -INFINITY;
-    } else {
-      // states s0-1 and s0-2 live in the lanes below
-      float m1 = __shfl_up(al[NS - 1], 1, 64);
-      float m2 = NS >= 2 ? __shfl_up(al[NS >= 2 ? NS - 2 : 0], 1, 64) : __shfl_up(al[0], 2, 64);
-      if (lane < 1) m1 = -INFINITY;
-      if (lane < (NS >= 2 ? 1 : 2)) m2 = -INFINITY;
+  auto step = [&](int k, const float (&ev)[NS]) {
+    float nx[NS];
+    if (k == 0) {
 #pragma unroll
       for (int i = 0; i < NS; ++i) {
-        const float a1 = i >= 1 ? al[i - 1] : m1;
-        const float a2 = i >= 2 ? al[i - 2] : (i == 1 ? m1 : m2);
-        an[i] = log_add3(al[i], a1, into[i] ? a2 : -INFINITY) + ev[i];
+        const int s = s0 + i;
+        const bool start = backward ? (s == S - 1 || s == S - 2) : s < 2;
+        nx[i] = start ? ev[i] : -INFINITY;
+      }
+    } else if (!backward) {
+      // states s0-1 and s0-2 live in the lanes below (-inf below lane 0)
+      const float m1 = dpp<kWaveShr1>(-INFINITY, cur[NS - 1]);
+      const float m2 = NS >= 2 ? dpp<kWaveShr1>(-INFINITY, cur[NS >= 2 ? NS - 2 : 0])
+                               : dpp<kWaveShr1>(-INFINITY, m1);
+#pragma unroll
+      for (int i = 0; i < NS; ++i) {
+        const float n1 = i >= 1 ? cur[i - 1] : m1;
+        const float n2 = i >= 2 ? cur[i - 2] : (i == 1 ? m1 : m2);
+        nx[i] = log_add3(cur[i], n1, skip[i] ? n2 : -INFINITY) + ev[i];
+      }
+    } else {
+      // states s0+NS and s0+NS+1 live in the lanes above (-inf past lane 63)
+      const float p1 = dpp<kWaveShl1>(-INFINITY, cur[0]);
+      const float p2 = NS >= 2 ? dpp<kWaveShl1>(-INFINITY, cur[NS >= 2 ? 1 : 0])
+                               : dpp<kWaveShl1>(-INFINITY, p1);
+#pragma unroll
+      for (int i = 0; i < NS; ++i) {
+        const float n1 = i + 1 < NS ? cur[i + 1] : p1;
+        const float n2 = i + 2 < NS ? cur[i + 2] : (i + 1 == NS ? p2 : p1);
+        nx[i] = log_add3(cur[i], n1, skip[i] ? n2 : -INFINITY) + ev[i];
       }
     }
     float part = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < NS; ++i) part = fmaxf(part, an[i]);
-    const float mx = wave_max(part);
+    for (int i = 0; i < NS; ++i) part = fmaxf(part, nx[i]);
+    const float mx = dpp_wave_max(part);
     if (mx == -INFINITY) dead = true;
     const float sh = mx == -INFINITY ? 0.f : mx;
     logc += (double)sh;
 #pragma unroll
-    for (int i = 0; i < NS; ++i) al[i] = an[i] - sh;
-    store_row<NS>(ab, stride, t, s0, al);
+    for (int i = 0; i < NS; ++i) cur[i] = nx[i] - sh;
+    store_row<NS>(out, stride, backward ? L - 1 - k : k, s0, cur);
   };
-  for (int t = 0; t < L; t += kAhead) {
-    fwd_step(t, q0);
-    fetch_e(t + 4, q0);
-    if (t + 1 < L) {
-      fwd_step(t + 1, q1);
-      fetch_e(t + 5, q1);
-    }
-    if (t + 2 < L) {
-      fwd_step(t + 2, q2);
-      fetch_e(t + 6, q2);
-    }
-    if (t + 3 < L) {
-      fwd_step(t + 3, q3);
-      fetch_e(t + 7, q3);
+  for (int k0 = 0; k0 < L; k0 += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      if (k0 + j < L) {
+        step(k0 + j, q[j]);
+        fetch(k0 + j + D, q[j]);
+      }
     }
   }
+  if (backward) return;
   // ln p = sum of the shifts + ln(alpha(S-1) + alpha(S-2)) at the last frame
   float endp = 0.f;
 #pragma unroll
   for (int i = 0; i < NS; ++i)
-    if (s0 + i == S - 1 || s0 + i == S - 2) endp += __expf(al[i]);
-  endp = wave_sum(endp);
+    if (s0 + i == S - 1 || s0 + i == S - 2) endp += __expf(cur[i]);
+  endp = dpp_wave_sum(endp);
   dead = dead || !(endp > 0.f);
   if (lane == 0) a.loss_part[b] = dead ? INFINITY : (float)(-(logc + (double)__logf(endp)));
-
-  // ---- backward variables and occupancies
-  float be[NS];
-  float r0[NS], r1[NS], r2[NS], r3[NS];  // alpha rows, read ahead like the e rows
-  auto fetch_a = [&](int t, float (&q)[NS]) { load_row<NS>(ab, stride, t >= 0 ? t : 0, s0, q); };
-  auto fetch_eb = [&](int t, float (&q)[NS]) { load_row<NS>(eb, stride, t >= 0 ? t : 0, s0, q); };
-  // The backward pass reads back the forward pass's alpha rows: wait for
-  // every store of this wave first.
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  fetch_eb(L - 1, q0);
-  fetch_eb(L - 2, q1);
-  fetch_eb(L - 3, q2);
-  fetch_eb(L - 4, q3);
-  fetch_a(L - 1, r0);
-  fetch_a(L - 2, r1);
-  fetch_a(L - 3, r2);
-  fetch_a(L - 4, r3);
-  float* csum = eb;  // occupancy sums overwrite e row t once it has been used
-  auto bwd_step = [&](int t, const float (&ev)[NS], const float (&av)[NS]) {
-    float bn[NS];
-    if (t == L - 1) {
-#pragma unroll
-      for (int i = 0; i < NS; ++i)
-        bn[i] = (s0 + i == S - 1 || s0 + i == S - 2) ? ev[i] : -INFINITY;
-    } else {
-      float p1 = __shfl_down(be[0], 1, 64);
-      float p2 = NS >= 2 ? __shfl_down(be[NS >= 2 ? 1 : 0], 1, 64) : __shfl_down(be[0], 2, 64);
-      if (lane >= 63) p1 = -INFINITY;
-      if (lane >= (NS >= 2 ? 63 : 62)) p2 = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < NS; ++i) {
-        const float b1 = i + 1 < NS ? be[i + 1] : p1;
-        const float b2 = i + 2 < NS ? be[i + 2] : (i + 1 == NS ? p2 : p1);
-        bn[i] = log_add3(be[i], b1, from[i] ? b2 : -INFINITY) + ev[i];
-      }
-    }
-    float part = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) part = fmaxf(part, bn[i]);
-    const float mb = wave_max(part);
-    const float shb = mb == -INFINITY ? 0.f : mb;
-    // ln of alpha beta / y per state, then occupancies relative to their
-    // maximum (which is therefore 1: the normaliser cannot underflow)
-    float lg[NS];
-    float lpart = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      be[i] = bn[i] - shb;
-      lg[i] = (av[i] == -INFINITY || be[i] == -INFINITY) ? -INFINITY : av[i] + be[i] - ev[i];
-      lpart = fmaxf(lpart, lg[i]);
-    }
-    const float mg = wave_max(lpart);
-    float g[NS];
-    float gpart = 0.f;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      g[i] = mg == -INFINITY ? 0.f : __expf(lg[i] - mg);
-      gpart += g[i];
-    }
-    const float z = wave_sum(gpart);
-    const float zinv = (z > 0.f && !dead) ? 1.f / z : 0.f;
-    float blank = 0.f;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      g[i] *= zinv;
-      occ[s0 + i] = g[i];
-      if (!((s0 + i) & 1)) blank += g[i];
-    }
-    blank = wave_sum(blank);
-    __syncthreads();
-    // Entry 1+u of the row: the class sum at the first position u of each
-    // label, -1 at later positions of a repeated label; entry 0: blank.
-    float* cs = csum + (int64_t)t * stride;
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      const int s = s0 + i;
-      if (!(s < S && (s & 1))) continue;
-      float v = -1.f;
-      if (head[i]) {
-        v = g[i];
-        for (int q = nx[s]; q >= 0; q = nx[q]) v += occ[q];
-      }
-      cs[1 + (s >> 1)] = v;
-    }
-    if (lane == 0) cs[0] = blank;
-    __syncthreads();
-  };
-  for (int t = L - 1; t >= 0; t -= kAhead) {
-    bwd_step(t, q0, r0);
-    fetch_eb(t - 4, q0);
-    fetch_a(t - 4, r0);
-    if (t - 1 >= 0) {
-      bwd_step(t - 1, q1, r1);
-      fetch_eb(t - 5, q1);
-      fetch_a(t - 5, r1);
-    }
-    if (t - 2 >= 0) {
-      bwd_step(t - 2, q2, r2);
-      fetch_eb(t - 6, q2);
-      fetch_a(t - 6, r2);
-    }
-    if (t - 3 >= 0) {
-      bwd_step(t - 3, q3, r3);
-      fetch_eb(t - 7, q3);
-      fetch_a(t - 7, r3);
-    }
-  }
 }
 
-// Gradient rows: y_t(k) - (class k's occupancy), times the loss scale.
+// Gradient rows, one wave per valid frame: the state occupancies
+// alpha beta / y of the frame (from the two stored recursions, normalised
+// by their maximum, then their sum), their per-class sums (blank: all even
+// states; a label class: its positions along the chain, in order), and
+// y_t(k) minus those sums, times the loss scale, over the logits.
+constexpr int kMaxStates = 2048;
 __global__ __launch_bounds__(64 * kEmitWaves) void k_ctc_grad(CtcArgs a) {
   __shared__ float row_s[kEmitWaves][1024];
+  __shared__ float occ_s[kEmitWaves][kMaxStates / 2];  // odd states: label positions
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t id = (int64_t)blockIdx.x * kEmitWaves + w;
-  const bool live = id < (int64_t)a.T * a.B;
-  const int t = live ? (int)(id / a.B) : 0, b = live ? (int)(id % a.B) : 0;
-  const int64_t f = live ? frame_of(a, t, b) : -1;
-  float* row = f >= 0 ? a.z + f * a.C : nullptr;
+  if (id >= (int64_t)a.T * a.B) return;
+  const int t = (int)(id / a.B), b = (int)(id % a.B);
+  const int64_t f = frame_of(a, t, b);
+  if (f < 0) return;
+  float* row = a.z + f * a.C;
   float* rs = row_s[w];
-  if (f >= 0) {
-    const float lse = a.lse[f];
-    for (int k = lane; k < a.C; k += 64) rs[k] = __expf(row[k] - lse);
+  float* oc = occ_s[w];
+  const int U = a.tab[b];
+  const int S = 2 * U + 1;
+  const bool dead = !(a.loss_part[b] < INFINITY);
+  const int64_t ro = ((int64_t)b * a.T + t) * a.S_stride;
+  const float* al = a.alpha + ro;
+  const float* be = a.beta + ro;
+  const float* ee = a.e + ro;
+  // ln(alpha beta / y) per state; its maximum; occupancies; their sum
+  float mx = -INFINITY;
+  for (int s = lane; s < S; s += 64) {
+    const float x = al[s], y = be[s];
+    const float lg = (x == -INFINITY || y == -INFINITY) ? -INFINITY : x + y - ee[s];
+    mx = fmaxf(mx, lg);
   }
-  __syncthreads();
-  if (f >= 0) {
-    const int U = a.tab[b];
-    const int32_t* tg = a.targets + (int64_t)b * a.U_max;
-    const float* cs = a.e + ((int64_t)b * a.T + t) * a.S_stride;
-    // Class sums sit at the first position of each label (distinct classes,
-    // so lanes never meet on a class); later positions hold -1.
-    if (lane == 0) rs[0] -= cs[0];
-    for (int u = lane; u < U; u += 64) {
-      const float v = cs[1 + u];
-      if (v >= 0.f) rs[label_at(a, tg, u)] -= v;
-    }
+  mx = wave_max(mx);
+  float z = 0.f, blank = 0.f;
+  for (int s = lane; s < S; s += 64) {
+    const float x = al[s], y = be[s];
+    const float o = (x == -INFINITY || y == -INFINITY || mx == -INFINITY)
+                        ? 0.f : __expf(x + y - ee[s] - mx);
+    z += o;
+    if (s & 1)
+      oc[s >> 1] = o;
+    else
+      blank += o;
   }
-  __syncthreads();
-  if (f >= 0) {
-    const bool dead = !(a.loss_part[b] < INFINITY);
-    for (int k = lane; k < a.C; k += 64) row[k] = dead ? 0.f : rs[k] * a.scale;
+  z = wave_sum(z);
+  blank = wave_sum(blank);
+  const float zinv = (z > 0.f && !dead) ? 1.f / z : 0.f;
+  const float lse = a.lse[f];
+  for (int k = lane; k < a.C; k += 64) rs[k] = __expf(row[k] - lse);
+  __builtin_amdgcn_wave_barrier();
+  if (lane == 0) rs[0] -= blank * zinv;
+  // one lane per class (the first position of each class), in position order
+  const int32_t* tg = a.targets + (int64_t)b * a.U_max;
+  const int32_t* nxt = a.chain + (int64_t)b * 2 * a.U_max;
+  const int32_t* head = nxt + a.U_max;
+  for (int u = lane; u < U; u += 64) {
+    if (!head[u]) continue;
+    float v = 0.f;
+    for (int q = u; q >= 0; q = nxt[q]) v += oc[q];
+    rs[label_at(a, tg, u)] -= v * zinv;
   }
+  __builtin_amdgcn_wave_barrier();
+  for (int k = lane; k < a.C; k += 64) row[k] = dead ? 0.f : rs[k] * a.scale;
 }
 
 }  // namespace
@@ -400,12 +381,12 @@ hipError_t launch_ctc(const CtcArgs& a, hipStream_t st) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   switch (a.S_stride / 64) {
-    case 1: hipLaunchKernelGGL(k_ctc_seq<1>, dim3(a.B), dim3(64), 0, st, a); break;
-    case 2: hipLaunchKernelGGL(k_ctc_seq<2>, dim3(a.B), dim3(64), 0, st, a); break;
-    case 4: hipLaunchKernelGGL(k_ctc_seq<4>, dim3(a.B), dim3(64), 0, st, a); break;
-    case 8: hipLaunchKernelGGL(k_ctc_seq<8>, dim3(a.B), dim3(64), 0, st, a); break;
-    case 16: hipLaunchKernelGGL(k_ctc_seq<16>, dim3(a.B), dim3(64), 0, st, a); break;
-    case 32: hipLaunchKernelGGL(k_ctc_seq<32>, dim3(a.B), dim3(64), 0, st, a); break;
+    case 1: hipLaunchKernelGGL(k_ctc_seq<1>, dim3(2 * a.B), dim3(64), 0, st, a); break;
+    case 2: hipLaunchKernelGGL(k_ctc_seq<2>, dim3(2 * a.B), dim3(64), 0, st, a); break;
+    case 4: hipLaunchKernelGGL(k_ctc_seq<4>, dim3(2 * a.B), dim3(64), 0, st, a); break;
+    case 8: hipLaunchKernelGGL(k_ctc_seq<8>, dim3(2 * a.B), dim3(64), 0, st, a); break;
+    case 16: hipLaunchKernelGGL(k_ctc_seq<16>, dim3(2 * a.B), dim3(64), 0, st, a); break;
+    case 32: hipLaunchKernelGGL(k_ctc_seq<32>, dim3(2 * a.B), dim3(64), 0, st, a); break;
     default: return hipErrorInvalidValue;
   }
   e = hipGetLastError();

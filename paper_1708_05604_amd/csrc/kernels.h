@@ -94,9 +94,11 @@ hipError_t launch_sgd(float* params, const float* grads, int64_t n, float lr,
 //   z        [N x C] logits in, gradient d loss / d logits out (x scale)
 //   targets  device int32 [B][U_max] label strings
 //   tab      device int32 [2B]: target lengths, then sequence lengths
-//   e, alpha device [B][T][S_stride] scratch (S_stride = 64 * states per
-//            lane, see ctc_states_per_lane); lse [N]; loss_part [B] out
-//            (per-sequence -ln p, +inf when no path exists)
+//   e, alpha, beta  device [B][T][S_stride] scratch (S_stride = 64 * states
+//            per lane, see ctc_states_per_lane): log emissions and the two
+//            shifted log recursions; chain [B][2*U_max] scratch (label
+//            chains); lse [N]; loss_part [B] out (per-sequence -ln p, +inf
+//            when no path exists)
 struct CtcArgs {
   float* z;
   int C;
@@ -109,6 +111,8 @@ struct CtcArgs {
   int S_stride;
   float* e;
   float* alpha;
+  float* beta;
+  int32_t* chain;
   float* lse;
   float* loss_part;
   float scale;
