@@ -75,6 +75,7 @@ constexpr unsigned kNoRow = 0x7FFFFFF0u;  // an offset past every published arra
 constexpr int kDeviceScope = 16;           // sc1
 constexpr int kMaxSteps = 6144;  // batch tables kept in LDS: T_max above this is not handled here
 constexpr int kBwdUnits = 16;    // hidden units per backward workgroup
+constexpr int kEpiWaves = 4;     // backward waves running the gate-gradient algebra (256 threads)
 
 // Reduction-dimension chunking of one MFMA group: fp32 16x16x4 takes 4
 // k per lane group (4 groups), bf16 16x16x32 takes 8.
@@ -469,7 +470,7 @@ __device__ inline void store_or_publish(float* p, float v, bool pub) {
 // threads 0..255 then run the gate-gradient algebra of one (row, unit) each,
 // carrying dc*f (LSTM) or dh*z (GRU) of their row and unit in a register and
 // summing the unit's gate gradients over the steps for the bias gradients.
-template <int G, bool BF16, int NW, int MAXC>
+template <int G, bool BF16, int NW, int MAXC, bool SPLIT>
 __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
@@ -498,8 +499,17 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   const int lr = lane & 15, lq = lane >> 4;
   const bool has_up = U.up != nullptr;
   const int kup = has_up ? U.k_up : 0;
-  const Slots sup{wave, NW, kup / CH, lq * CPL};
-  const Slots srec{wave, NW, GH / CH, lq * CPL};
+  // SPLIT (8 or 16 waves): the four gate-gradient waves neither poll nor
+  // multiply.  Their per-step operand loads (saved gates, cell states, the
+  // gradient from above) come from HBM, and loads complete in issue order,
+  // so in a polling wave they would hold up every poll behind them.
+  static_assert(!SPLIT || NW >= 8, "the split needs waves beyond the gate-gradient ones");
+  constexpr int NMMA = SPLIT ? NW - kEpiWaves : NW;
+  const bool mma_wave = !SPLIT || wave >= kEpiWaves;
+  const int mw = SPLIT ? wave - kEpiWaves : wave;
+  const int first = mma_wave ? mw : (1 << 20);  // no slots for the others
+  const Slots sup{first, NMMA, kup / CH, lq * CPL};
+  const Slots srec{first, NMMA, GH / CH, lq * CPL};
 
   // Weight fragments: column lr is hidden unit j0 + lr.
   typename WFrag<BF16>::T wup[MAXC], wrec[MAXC];
@@ -527,36 +537,40 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   auto up_off = [&](const BwdIdx& q) {
     return (has_up && r < q.rows) ? 4u * (unsigned)((int64_t)(q.row0 + r) * kup) : kNoRow;
   };
+  // Operands of the gate-gradient algebra that do not depend on other
+  // workgroups (inactive rows read frame 0 and are ignored).
+  auto fetch_ops = [&](const BwdIdx& q, float& dhv_, float& s0_, float& s1_, float& s2_,
+                       float& s3_, float& cc_, float& cp_) {
+    const int64_t fq = erow < q.rows ? q.row0 + erow : 0;
+    const int64_t fp = erow < q.prev_rows ? q.prev0 + erow : 0;
+    dhv_ = U.dh_in ? U.dh_in[fq * U.ld_dh + U.hcol + ej] : 0.f;
+    const float* st = U.stash + fq * 4 * H;
+    s0_ = st[ej];
+    s1_ = st[H + ej];
+    s2_ = st[2 * H + ej];
+    s3_ = st[3 * H + ej];
+    if constexpr (G == 4) {
+      cc_ = U.cst[fq * H + ej];
+      cp_ = U.cst[fp * H + ej];
+    } else {
+      cc_ = 0.f;
+      cp_ = U.hout[fp * a.ldh + U.hcol + ej];
+    }
+  };
+  float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cprev = 0.f;
   BwdIdx s = bwd_step(tbs, toff, a.T, U.dir, 0);
   unsigned uup[CPL * MAXC];
-  issue_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
+  if (mma_wave) issue_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
   for (int k = 0; k < a.T; ++k) {
     BwdIdx nx = s;
     if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
     const bool active = r0 < s.rows;
-    // Operands that do not depend on other workgroups, loaded without
-    // branches inside the gate-gradient threads (inactive rows read frame
-    // 0 and are ignored).
-    float dhv = 0.f, st0, st1, st2, st3, cc, cprev;
     const int64_t f = erow < s.rows ? s.row0 + erow : 0;
     const bool has_prev = erow < s.prev_rows;
-    if (epi) {
-      const int64_t fp = has_prev ? s.prev0 + erow : 0;
-      if (U.dh_in) dhv = U.dh_in[f * U.ld_dh + U.hcol + ej];
-      const float* st = U.stash + f * 4 * H;
-      st0 = st[ej];
-      st1 = st[H + ej];
-      st2 = st[2 * H + ej];
-      st3 = st[3 * H + ej];
-      if constexpr (G == 4) {
-        cc = U.cst[f * H + ej];
-        cprev = U.cst[fp * H + ej];
-      } else {
-        cc = 0.f;
-        cprev = U.hout[fp * a.ldh + U.hcol + ej];
-      }
-    }
-    if (active) {
+    // Loaded at the top of the step.  (With the split, fetching them one
+    // step ahead instead measured slower.)
+    if (epi) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
+    if (active && mma_wave) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       // Gradient arriving from the layer above (fetched one step ahead).
       if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
@@ -569,15 +583,15 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       settle_segment<BF16, MAXC>(rrec, roff, srec, GH, urec);
       mma_segment<BF16, MAXC>(acc, urec, wrec, srec);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) red[wave * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
+      for (int q = 0; q < 4; ++q) red[mw * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
-    if (k + 1 < a.T) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
+    if (k + 1 < a.T && mma_wave) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
       float dh_red = 0.f;
 #pragma unroll
-      for (int w_ = 0; w_ < NW; ++w_) dh_red += red[w_ * 256 + threadIdx.x];
+      for (int w_ = 0; w_ < NMMA; ++w_) dh_red += red[w_ * 256 + threadIdx.x];
       if constexpr (G == 4) {
         const float dh = dhv + dh_red;
         const float tc = act_tanh(cc);
@@ -788,53 +802,57 @@ constexpr int bwd_maxc_cap(int nw, bool bf16) {
   return nw == 16 ? (bf16 ? 8 : 16) : bwd_maxc_fit(nw, bf16);
 }
 
-template <int G, bool BF16, int NW, int M>
+template <int G, bool BF16, int NW, int M, bool SP>
 const void* bwd_kernel_m() {
-  if constexpr (M <= bwd_maxc_cap(NW, BF16))
-    return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, M>);
+  if constexpr (M <= bwd_maxc_cap(NW, BF16) && (!SP || NW >= 8) && (SP || NW != 8))
+    return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, M, SP>);
   return nullptr;
 }
 
-template <int G, bool BF16, int NW>
+template <int G, bool BF16, int NW, bool SP>
 const void* bwd_kernel_nw(int maxc) {
   switch (maxc) {
-    case 1: return bwd_kernel_m<G, BF16, NW, 1>();
-    case 2: return bwd_kernel_m<G, BF16, NW, 2>();
-    case 4: return bwd_kernel_m<G, BF16, NW, 4>();
-    case 8: return bwd_kernel_m<G, BF16, NW, 8>();
-    case 16: return bwd_kernel_m<G, BF16, NW, 16>();
+    case 1: return bwd_kernel_m<G, BF16, NW, 1, SP>();
+    case 2: return bwd_kernel_m<G, BF16, NW, 2, SP>();
+    case 3: return bwd_kernel_m<G, BF16, NW, 3, SP>();
+    case 4: return bwd_kernel_m<G, BF16, NW, 4, SP>();
+    case 8: return bwd_kernel_m<G, BF16, NW, 8, SP>();
+    case 16: return bwd_kernel_m<G, BF16, NW, 16, SP>();
   }
   return nullptr;
 }
 
 template <int G, bool BF16>
-const void* bwd_kernel_g(int nw, int maxc) {
+const void* bwd_kernel_g(int nw, int maxc, bool split) {
   switch (nw) {
-    case 4: return bwd_kernel_nw<G, BF16, 4>(maxc);
-    case 8: return bwd_kernel_nw<G, BF16, 8>(maxc);
-    case 16: return bwd_kernel_nw<G, BF16, 16>(maxc);
+    case 4: return split ? nullptr : bwd_kernel_nw<G, BF16, 4, false>(maxc);
+    case 8: return split ? bwd_kernel_nw<G, BF16, 8, true>(maxc) : nullptr;
+    case 16:
+      return split ? bwd_kernel_nw<G, BF16, 16, true>(maxc) : bwd_kernel_nw<G, BF16, 16, false>(maxc);
   }
   return nullptr;
 }
 
-const void* bwd_kernel(int cell, bool bf16, int nw, int maxc) {
-  if (cell == RNNBKT_CELL_LSTM) return bf16 ? bwd_kernel_g<4, true>(nw, maxc) : bwd_kernel_g<4, false>(nw, maxc);
-  return bf16 ? bwd_kernel_g<3, true>(nw, maxc) : bwd_kernel_g<3, false>(nw, maxc);
+const void* bwd_kernel(int cell, bool bf16, int nw, int maxc, bool split) {
+  if (cell == RNNBKT_CELL_LSTM)
+    return bf16 ? bwd_kernel_g<4, true>(nw, maxc, split) : bwd_kernel_g<4, false>(nw, maxc, split);
+  return bf16 ? bwd_kernel_g<3, true>(nw, maxc, split) : bwd_kernel_g<3, false>(nw, maxc, split);
 }
 
 struct BwdPlan {
   const void* kernel;
   int nw, maxc, blocks;
+  bool split;
   size_t shmem;
 };
 
-// Waves per workgroup: the fewest that bring a wave's share of the longer
-// segment down to kBwdChain chunks (each chunk is a serial MFMA group on
-// the step's critical path), else the most that fit in registers.
-constexpr int kBwdChain = 2;
-
+// Waves per workgroup and slots per wave: each slot is a serial MFMA group
+// on the step's critical path, and gate-gradient waves that also poll delay
+// their polls behind their HBM operand loads (worth about 1.5 slots on
+// lstm2); more waves cost a little in the barriers.  The cheapest candidate
+// that fits in registers without spilling wins.
 BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
-  BwdPlan p{nullptr, 0, 0, 0, 0};
+  BwdPlan p{nullptr, 0, 0, 0, false, 0};
   const int ch = bf16 ? 32 : 16;
   const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
   if (a.T > kMaxSteps || a.nunits < 1 || a.nunits > kMaxUnits || a.H % kBwdUnits != 0) return p;
@@ -845,28 +863,39 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     if (u.rec_bytes >= kNoRow || (u.up && (u.k_up % ch != 0 || u.up_bytes >= kNoRow))) return p;
     nch = std::max(nch, std::max(u.up ? u.k_up / ch : 0, G * a.H / ch));
   }
-  for (int nw : {4, 8, 16}) {
-    const int per = (nch + nw - 1) / nw;
-    int m = 1;
-    while (m < per) m *= 2;
-    if (m > bwd_maxc_fit(nw, bf16)) continue;
-    p.nw = nw;
-    p.maxc = m;
-    if (m <= kBwdChain) break;
+  struct Cand {
+    int nw;
+    bool split;
+  };
+  float best = 1e30f;
+  for (const Cand c : {Cand{4, false}, Cand{8, true}, Cand{16, true}, Cand{16, false}}) {
+    const int nmma = c.split ? c.nw - kEpiWaves : c.nw;  // waves that poll and multiply
+    const int per = (nch + nmma - 1) / nmma;
+    int m = 1;  // slots per wave: 1, 2, 3 or a power of two
+    while (m < per) m = m == 2 && per == 3 ? 3 : m * 2;
+    if (m > bwd_maxc_fit(c.nw, bf16)) continue;
+    const float cost = m + (c.split ? 0.f : 1.5f) + (c.nw == 16 ? 0.5f : c.nw == 8 ? 0.25f : 0.f);
+    if (cost < best) {
+      best = cost;
+      p.nw = c.nw;
+      p.maxc = m;
+      p.split = c.split;
+    }
   }
   if (p.nw == 0) {
-    // Very wide layers: 16 waves with spilled registers.
+    // Very wide layers: 16 polling waves with spilled registers.
     int m = 1;
     while (m < (nch + 15) / 16) m *= 2;
     if (m <= bwd_maxc_cap(16, bf16)) {
       p.nw = 16;
       p.maxc = m;
+      p.split = false;
     }
   }
   if (p.nw == 0) return p;
   p.blocks = a.nunits * (a.H / kBwdUnits) * ((B + 15) / 16);
   p.shmem = sizeof(float) * std::max(p.nw, 8) * 256 + sizeof(int32_t) * (2 * a.T + 1);
-  p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc);
+  p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc, p.split);
   return p;
 }
 
