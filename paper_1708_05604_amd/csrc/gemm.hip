@@ -199,6 +199,119 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     }
 }
 
+// fp32 C = A^T B with both operands K-outer (A element (m, k) at
+// A[k*lda + m], B element (k, n) at B[row(k)*ldb + n]): the weight-gradient
+// products, reduced over all valid frames.  Tiles are staged untransposed
+// ([k][m] and [k][n], float4 stores, rows padded by 16 floats so the four
+// k-rows a wave reads sit in different banks), which is the order
+// v_mfma_f32_16x16x4_f32 wants: lane (row r, group q) feeds element
+// (m0 + r, k0 + q) -- one float per lane per MFMA.  K-tiles are double
+// buffered: the next tile's global loads are in flight during this tile's
+// MFMAs.
+constexpr int TN_LD = BM + 16;
+
+__device__ inline void tn_load(f4 (&v)[2], const float* P, int64_t ld, const int32_t* gather,
+                               int c0, int clim, int k0, int klim) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    f4 x = {0.f, 0.f, 0.f, 0.f};
+    if (k0 + k < klim && c0 + c < clim) {
+      int64_t row = k0 + k;
+      if (gather) row = gather[row];
+      if (row >= 0) x = *reinterpret_cast<const f4*>(P + row * ld + c0 + c);
+    }
+    v[rep] = x;
+  }
+}
+
+__device__ inline void tn_store(float* S, const f4 (&v)[2]) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    *reinterpret_cast<f4*>(S + k * TN_LD + c) = v[rep];
+  }
+}
+
+__global__ __launch_bounds__(256) void k_gemm_tn_f32(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) float As[2][BK * TN_LD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][BK * TN_LD];
+  const int m0 = blockIdx.x * BM;
+  const int n0 = blockIdx.y * BN;
+  const int split = blockIdx.z;
+  const int kbeg = split * g.k_per_split;
+  const int kend = min(g.K, kbeg + g.k_per_split);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * 32;
+  const int wn = (wave & 1) * 32;
+  const int lr = lane & 15;
+  const int lq = lane >> 4;
+
+  f4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  f4 ra[2], rb[2];
+  tn_load(ra, g.A, g.lda, nullptr, m0, g.M, kbeg, kend);
+  tn_load(rb, g.B, g.ldb, g.gather_b, n0, g.N, kbeg, kend);
+  int buf = 0;
+  for (int k0 = kbeg; k0 < kend; k0 += BK) {
+    tn_store(As[buf], ra);
+    tn_store(Bs[buf], rb);
+    __syncthreads();
+    if (k0 + BK < kend) {
+      tn_load(ra, g.A, g.lda, nullptr, m0, g.M, k0 + BK, kend);
+      tn_load(rb, g.B, g.ldb, g.gather_b, n0, g.N, k0 + BK, kend);
+    }
+    const float* a_s = As[buf];
+    const float* b_s = Bs[buf];
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 4) {
+      const int kr = (kk + lq) * TN_LD;
+      float a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = a_s[kr + wm + i * 16 + lr];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = b_s[kr + wn + j * 16 + lr];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    buf ^= 1;
+  }
+
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn + j * 16 + lr;
+      if (n >= g.N) continue;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm + i * 16 + lq * 4 + r;
+        if (m >= g.M) continue;
+        float v = acc[i][j][r];
+        if (g.splits > 1) {
+          g.partial[((int64_t)split * g.M + m) * g.N + n] = v;
+        } else {
+          if (g.bias) v += g.bias[n];
+          float* c = g.C + (int64_t)m * g.ldc + n;
+          if (g.accumulate) v += *c;
+          *c = v;
+        }
+      }
+    }
+}
+
 __global__ void k_splitk_reduce(const float* __restrict__ partial, int S, int M, int N,
                                 float* __restrict__ out, int64_t ldc,
                                 const float* __restrict__ bias, int accumulate) {
@@ -258,7 +371,10 @@ hipError_t launch_gemm(const GemmArgs& g, bool a_kc, bool b_kc, bool bf16, hipSt
   RNNBKT_GEMM_CASE(true, true, true)
   RNNBKT_GEMM_CASE(true, false, false)
   RNNBKT_GEMM_CASE(true, false, true)
-  RNNBKT_GEMM_CASE(false, false, false)
+  if (!a_kc && !b_kc && !bf16) {
+    hipLaunchKernelGGL(k_gemm_tn_f32, grid, block, 0, st, g);
+    return hipGetLastError();
+  }
   RNNBKT_GEMM_CASE(false, false, true)
 #undef RNNBKT_GEMM_CASE
   return hipErrorInvalidValue;
