@@ -94,13 +94,14 @@ def describe(w: synth.Workload, K: int) -> str:
 class Epoch:
     """One epoch's batches staged on the GPU."""
 
-    def __init__(self, w, data, K, epoch, torch, dev, targets=None):
+    def __init__(self, w, data, K, epoch, torch, dev, targets=None, ordering="ascending"):
         t0 = time.perf_counter()
         self.upper, bof, self.keff, self.p_bucket = lib.bucket_plan(data.lengths, K)
         self.plan_ms = (time.perf_counter() - t0) * 1e3
         t0 = time.perf_counter()
         self.batches = lib.epoch_schedule(data.lengths, bof, self.keff,
-                                          synth.shuffle_keys(0, epoch, w.n), w.batch)
+                                          synth.shuffle_keys(0, epoch, w.n), w.batch,
+                                          ordering, synth.order_keys(0, epoch, w.n))
         self.sched_ms = (time.perf_counter() - t0) * 1e3
         self.lens, self.x, self.y, self.useful = [], [], [], []
         self.p_batch = 0
@@ -211,6 +212,8 @@ def main(argv=None):
                          "(one label per 8 frames)")
     ap.add_argument("--optimizer", default="sgd", choices=("sgd", "adadelta"),
                     help="parameter update of each step (adadelta: rho 0.95, eps 1e-6)")
+    ap.add_argument("--ordering", default="ascending", choices=list(lib.ORDERINGS),
+                    help="feeding order of the buckets / batches (the paper's: ascending)")
     ap.add_argument("--no-k1", action="store_true", help="skip the K=1 epoch")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--no-timer", action="store_true", help="skip the per-kernel pass")
@@ -245,8 +248,8 @@ def main(argv=None):
         del cp, cg
 
     targets = synth.ctc_targets(data.lengths, w.num_classes, 0) if args.loss == "ctc" else None
-    ep = Epoch(w, data, K, 0, torch, dev, targets)
-    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev, targets)
+    ep = Epoch(w, data, K, 0, torch, dev, targets, args.ordering)
+    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev, targets, args.ordering)
     eps = [e for e in (ep, ep1) if e is not None]
     rb, wb = lib.buffer_sizes(desc, max(e.max_T for e in eps), max(e.max_B for e in eps),
                               max(e.max_N for e in eps))
@@ -279,6 +282,7 @@ def main(argv=None):
         "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.gemm_dtype == synth.BF16 else "f32", "data": "synthetic",
         "config": {"workload": describe(w, K), "loss": args.loss, "optimizer": args.optimizer,
+                   "ordering": args.ordering,
                    "batches_per_epoch": nb,
                    "useful_timesteps_per_epoch": ep.U, "parallelism": "single GPU"},
         "mfma_util_pct": 100.0 * flops * value / (peak * 1e12),

@@ -111,6 +111,36 @@ int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* bucket_of,
                               int32_t B, int64_t* order, int64_t* batch_start,
                               int64_t* num_batches);
 
+/* Feeding orders of rnnbkt_epoch_schedule_ordered.  The paper feeds the
+ * buckets shortest first (Sec. IV.A) and leaves other orders to future work
+ * (Sec. V); every ordering feeds the same batches. */
+#define RNNBKT_ORDER_ASCENDING 0        /* bucket 0, 1, ..., K_eff-1 (the paper's order) */
+#define RNNBKT_ORDER_DESCENDING 1       /* bucket K_eff-1, ..., 0 */
+#define RNNBKT_ORDER_RANDOM_BUCKETS 2   /* whole buckets by (order_keys[b], b) ascending */
+#define RNNBKT_ORDER_SHUFFLED_BATCHES 3 /* batches of all buckets interleaved: the
+                                           ascending list of batches sorted by
+                                           (order_keys[i], i), i = ascending position */
+
+/*
+ * rnnbkt_epoch_schedule_ordered -- rnnbkt_epoch_schedule with a choice of
+ * feeding order.  The batches are built exactly as rnnbkt_epoch_schedule
+ * builds them; only their sequence in `order` / `batch_start` differs.
+ *
+ *   ordering     RNNBKT_ORDER_*
+ *   order_keys   host uint64[n] random keys, read for RANDOM_BUCKETS (entries
+ *                0..K_eff-1; then K_eff <= n) and SHUFFLED_BATCHES (entries
+ *                0..num_batches-1); may be null for the other two
+ *   other arguments as for rnnbkt_epoch_schedule, which equals this call
+ *   with RNNBKT_ORDER_ASCENDING.
+ * Host-only.  Errors: EINVAL (as rnnbkt_epoch_schedule; unknown ordering;
+ * null order_keys where it is read).
+ */
+int32_t rnnbkt_epoch_schedule_ordered(const int32_t* lengths, const int32_t* bucket_of,
+                                      int64_t n, int32_t K_eff, const uint64_t* keys,
+                                      int32_t B, int32_t ordering,
+                                      const uint64_t* order_keys, int64_t* order,
+                                      int64_t* batch_start, int64_t* num_batches);
+
 /* Model description.  Shapes: G = 4 (LSTM) or 3 (GRU) gates, H = hidden,
  * dirs = 2 if bidirectional else 1, D_in(layer 0) = input_dim,
  * D_in(layer > 0) = dirs * H, H_top = dirs * H. */

@@ -113,15 +113,25 @@ extern "C" int32_t rnnbkt_bucket_plan(const int32_t* lengths, int64_t n, int32_t
   return RNNBKT_OK;
 }
 
-extern "C" int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* bucket_of,
-                                         int64_t n, int32_t K_eff, const uint64_t* keys,
-                                         int32_t B, int64_t* order, int64_t* batch_start,
-                                         int64_t* num_batches) {
+extern "C" int32_t rnnbkt_epoch_schedule_ordered(const int32_t* lengths,
+                                                 const int32_t* bucket_of, int64_t n,
+                                                 int32_t K_eff, const uint64_t* keys,
+                                                 int32_t B, int32_t ordering,
+                                                 const uint64_t* order_keys, int64_t* order,
+                                                 int64_t* batch_start, int64_t* num_batches) {
   rnnbkt::clear_error();
   RNNBKT_REQUIRE(lengths && bucket_of && keys && order && batch_start && num_batches,
                  RNNBKT_EINVAL, "epoch_schedule: null pointer");
   RNNBKT_REQUIRE(n >= 1 && K_eff >= 1 && B >= 1, RNNBKT_EINVAL,
                  "epoch_schedule: need n >= 1, K_eff >= 1, B >= 1");
+  RNNBKT_REQUIRE(ordering >= RNNBKT_ORDER_ASCENDING && ordering <= RNNBKT_ORDER_SHUFFLED_BATCHES,
+                 RNNBKT_EINVAL, "epoch_schedule: unknown ordering %d", ordering);
+  const bool keyed =
+      ordering == RNNBKT_ORDER_RANDOM_BUCKETS || ordering == RNNBKT_ORDER_SHUFFLED_BATCHES;
+  RNNBKT_REQUIRE(!keyed || order_keys, RNNBKT_EINVAL,
+                 "epoch_schedule: this ordering needs order_keys");
+  RNNBKT_REQUIRE(ordering != RNNBKT_ORDER_RANDOM_BUCKETS || K_eff <= n, RNNBKT_EINVAL,
+                 "epoch_schedule: K_eff %d > n leaves buckets without a key", K_eff);
   std::vector<std::vector<int64_t>> members(K_eff);
   for (int64_t s = 0; s < n; ++s) {
     RNNBKT_REQUIRE(bucket_of[s] >= 0 && bucket_of[s] < K_eff, RNNBKT_EINVAL,
@@ -130,9 +140,20 @@ extern "C" int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* 
     RNNBKT_REQUIRE(lengths[s] >= 1, RNNBKT_EINVAL, "epoch_schedule: length < 1");
     members[bucket_of[s]].push_back(s);
   }
-  int64_t pos = 0, nb = 0;
-  batch_start[0] = 0;
-  for (int32_t b = 0; b < K_eff; ++b) {
+  // Bucket order: ascending, descending, or by (order_keys[b], b).
+  std::vector<int32_t> bucket_seq(K_eff);
+  for (int32_t b = 0; b < K_eff; ++b)
+    bucket_seq[b] = ordering == RNNBKT_ORDER_DESCENDING ? K_eff - 1 - b : b;
+  if (ordering == RNNBKT_ORDER_RANDOM_BUCKETS)
+    std::sort(bucket_seq.begin(), bucket_seq.end(), [&](int32_t a, int32_t c) {
+      return order_keys[a] != order_keys[c] ? order_keys[a] < order_keys[c] : a < c;
+    });
+  // Batches are built in the bucket sequence; each is written as a contiguous
+  // run of `order` and recorded by its [begin, end) range.
+  std::vector<int64_t> ranges;  // begin of batch i at 2i, end at 2i+1
+  std::vector<int64_t> staged(static_cast<size_t>(n));
+  int64_t pos = 0;
+  for (int32_t b : bucket_seq) {
     auto& m = members[b];
     std::sort(m.begin(), m.end(), [&](int64_t a, int64_t c) {
       return keys[a] != keys[c] ? keys[a] < keys[c] : a < c;
@@ -142,10 +163,36 @@ extern "C" int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* 
       std::sort(m.begin() + st, m.begin() + en, [&](int64_t a, int64_t c) {
         return lengths[a] != lengths[c] ? lengths[a] > lengths[c] : a < c;
       });
-      for (size_t k = st; k < en; ++k) order[pos++] = m[k];
-      batch_start[++nb] = pos;
+      ranges.push_back(pos);
+      for (size_t k = st; k < en; ++k) staged[pos++] = m[k];
+      ranges.push_back(pos);
     }
+  }
+  const int64_t nb = static_cast<int64_t>(ranges.size() / 2);
+  // Batch order: as built, or by (order_keys[i], i) with i the batch's
+  // position in the ascending build (the bucket sequence is ascending here).
+  std::vector<int64_t> batch_seq(nb);
+  for (int64_t i = 0; i < nb; ++i) batch_seq[i] = i;
+  if (ordering == RNNBKT_ORDER_SHUFFLED_BATCHES)
+    std::sort(batch_seq.begin(), batch_seq.end(), [&](int64_t a, int64_t c) {
+      return order_keys[a] != order_keys[c] ? order_keys[a] < order_keys[c] : a < c;
+    });
+  pos = 0;
+  batch_start[0] = 0;
+  for (int64_t i = 0; i < nb; ++i) {
+    const int64_t j = batch_seq[i];
+    for (int64_t k = ranges[2 * j]; k < ranges[2 * j + 1]; ++k) order[pos++] = staged[k];
+    batch_start[i + 1] = pos;
   }
   *num_batches = nb;
   return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_epoch_schedule(const int32_t* lengths, const int32_t* bucket_of,
+                                         int64_t n, int32_t K_eff, const uint64_t* keys,
+                                         int32_t B, int64_t* order, int64_t* batch_start,
+                                         int64_t* num_batches) {
+  return rnnbkt_epoch_schedule_ordered(lengths, bucket_of, n, K_eff, keys, B,
+                                       RNNBKT_ORDER_ASCENDING, nullptr, order, batch_start,
+                                       num_batches);
 }

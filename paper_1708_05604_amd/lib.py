@@ -65,6 +65,10 @@ _SIGNATURES = {
     "rnnbkt_sync_check": (ctypes.c_int32, [_vp]),
     "rnnbkt_bucket_plan": (ctypes.c_int32, [_i32p, ctypes.c_int64, ctypes.c_int32, _i32p, _i32p,
                                             _i32p, _i64p]),
+    "rnnbkt_epoch_schedule_ordered": (ctypes.c_int32, [_i32p, _i32p, ctypes.c_int64,
+                                                       ctypes.c_int32, _u64p, ctypes.c_int32,
+                                                       ctypes.c_int32, _u64p, _i64p, _i64p,
+                                                       _i64p]),
     "rnnbkt_epoch_schedule": (ctypes.c_int32, [_i32p, _i32p, ctypes.c_int64, ctypes.c_int32,
                                                _u64p, ctypes.c_int32, _i64p, _i64p, _i64p]),
     "rnnbkt_param_count": (ctypes.c_int64, [_descp]),
@@ -186,19 +190,36 @@ def bucket_plan(lengths, K: int):
     return upper[:keff.value].copy(), bof, keff.value, padded.value
 
 
-def epoch_schedule(lengths, bucket_of, K_eff: int, keys, B: int):
-    """-> list of int64 arrays (sequence indices of each batch, in order)."""
+ORDERINGS = {"ascending": 0, "descending": 1, "random_buckets": 2, "shuffled_batches": 3}
+
+
+def epoch_schedule(lengths, bucket_of, K_eff: int, keys, B: int, ordering: str = "ascending",
+                   order_keys=None):
+    """-> list of int64 arrays (sequence indices of each batch, in feeding order)."""
     lib = load()
     L = _i32(lengths)
     bo = _i32(bucket_of)
     k = np.ascontiguousarray(keys, dtype=np.uint64)
     n = L.size
+    if ordering not in ORDERINGS:
+        raise RnnbktError(-1, f"unknown ordering {ordering!r}")
+    ok = None
+    if order_keys is not None:
+        ok = np.ascontiguousarray(order_keys, dtype=np.uint64)
+        if ok.size != n:
+            raise RnnbktError(-1, "order_keys must have one entry per sequence")
     order = np.zeros(n, np.int64)
     starts = np.zeros(n + 1, np.int64)
     nb = ctypes.c_int64(0)
-    _check(lib.rnnbkt_epoch_schedule(_ptr(L, _i32p), _ptr(bo, _i32p), n, int(K_eff),
-                                     _ptr(k, _u64p), int(B), _ptr(order, _i64p),
-                                     _ptr(starts, _i64p), ctypes.byref(nb)))
+    if ordering == "ascending" and ok is None:
+        _check(lib.rnnbkt_epoch_schedule(_ptr(L, _i32p), _ptr(bo, _i32p), n, int(K_eff),
+                                         _ptr(k, _u64p), int(B), _ptr(order, _i64p),
+                                         _ptr(starts, _i64p), ctypes.byref(nb)))
+    else:
+        _check(lib.rnnbkt_epoch_schedule_ordered(
+            _ptr(L, _i32p), _ptr(bo, _i32p), n, int(K_eff), _ptr(k, _u64p), int(B),
+            ORDERINGS[ordering], None if ok is None else _ptr(ok, _u64p),
+            _ptr(order, _i64p), _ptr(starts, _i64p), ctypes.byref(nb)))
     return [order[starts[i]:starts[i + 1]].copy() for i in range(nb.value)]
 
 

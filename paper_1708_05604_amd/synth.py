@@ -156,3 +156,10 @@ def padded_batch(data: Data, order: np.ndarray, t_max: Optional[int] = None):
         x[:L, b, :] = data.X[o:o + L]
         y[:L, b] = data.Y[o:o + L]
     return x, y, lens.astype(np.int32)
+
+
+def order_keys(seed: int, epoch: int, n: int) -> np.ndarray:
+    """Random uint64 keys that rank buckets or batches for the randomised
+    feeding orders (one stream per epoch, independent of the shuffle keys)."""
+    rng = np.random.default_rng([seed, 0x0DE5, epoch])
+    return rng.integers(0, np.iinfo(np.int64).max, n, dtype=np.int64).astype(np.uint64)

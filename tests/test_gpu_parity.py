@@ -107,6 +107,37 @@ def test_sgd_trajectory_tiny():
         assert err < 1e-4
 
 
+@pytest.mark.parametrize("ordering", ["descending", "shuffled_batches"])
+def test_epoch_sgd_under_feeding_order(ordering):
+    """One SGD epoch over the tiny workload (K=2) fed in another order: the
+    library's schedule equals the oracle's, and the parameters carried batch
+    after batch follow the oracle's trajectory."""
+    from oracle import schedule as osch
+    w = synth.WORKLOADS["tiny"]
+    spec = H.Spec.of(w)
+    P = orn.param_count(spec.model())
+    data = synth.make_workload(w, 0, param_count=P)
+    _, bof, keff, _ = lib.bucket_plan(data.lengths, 2)
+    keys, ok = synth.shuffle_keys(0, 3, w.n), synth.order_keys(0, 3, w.n)
+    batches = lib.epoch_schedule(data.lengths, bof, keff, keys, w.batch, ordering, ok)
+    ref = osch.epoch_batches(data.lengths, bof, keff, keys, w.batch, ordering, ok)
+    assert [b.tolist() for b in batches] == [b.tolist() for b in ref]
+    lr = 0.2
+    p0 = data.params.astype(np.float64)
+    cur = data.params.astype(np.float32)
+    theta = p0.copy()
+    for i, order in enumerate(batches):
+        gb = H.GpuBatch(spec, cur, data, order)
+        gb.run()
+        gb.sgd(lr)
+        cur = gb.params.cpu().numpy()
+        _, grad, _ = H.oracle_batch(spec, theta, data, order)
+        theta = orn.sgd(theta, grad, lr)
+        err = H.normwise_err(cur.astype(np.float64) - p0, theta - p0)
+        print(f"[case] {ordering} batch {i} B={len(order)} update err {err:.2e}", flush=True)
+        assert err < 1e-4
+
+
 def test_sgd_apply_exact():
     import torch
     rng = np.random.default_rng(0)

@@ -180,3 +180,36 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
         lib.load()
     with pytest.raises(lib.LibraryMissing):
         lib.bucket_plan([1, 2], 1)
+
+
+@pytest.mark.parametrize("ordering", ["ascending", "descending", "random_buckets",
+                                      "shuffled_batches"])
+@pytest.mark.parametrize("name,K", [("tiny", 3), ("lstm2", 8), ("longtail", 1)])
+def test_ordered_schedule_matches_oracle(ordering, name, K):
+    w = synth.WORKLOADS[name]
+    lengths = synth.draw_lengths(np.random.default_rng(1), w.law, w.law_args, w.n)
+    _, bof, keff, _ = lib.bucket_plan(lengths, K)
+    for epoch in (0, 1):
+        keys = synth.shuffle_keys(1, epoch, w.n)
+        ok = synth.order_keys(1, epoch, w.n)
+        a = osch.epoch_batches(lengths, bof, keff, keys, w.batch, ordering, ok)
+        b = lib.epoch_schedule(lengths, bof, keff, keys, w.batch, ordering, ok)
+        assert len(a) == len(b)
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+
+
+def test_ordered_schedule_rejects_bad_input():
+    lengths = np.array([3, 1, 2], np.int32)
+    bof = np.zeros(3, np.int32)
+    keys = np.arange(3, dtype=np.uint64)
+    with pytest.raises(lib.RnnbktError):
+        lib.epoch_schedule(lengths, bof, 1, keys, 2, "random_buckets")  # needs order_keys
+    with pytest.raises(lib.RnnbktError):
+        lib.epoch_schedule(lengths, bof, 1, keys, 2, "shuffled_batches", np.zeros(2, np.uint64))
+    with pytest.raises(lib.RnnbktError):
+        lib.epoch_schedule(lengths, bof, 1, keys, 2, "sideways")
+    # descending needs no keys and equals the ascending list for one bucket
+    a = lib.epoch_schedule(lengths, bof, 1, keys, 2, "descending")
+    b = lib.epoch_schedule(lengths, bof, 1, keys, 2)
+    assert [x.tolist() for x in a] == [x.tolist() for x in b]

@@ -114,3 +114,69 @@ def test_schedule_invariants():
     _, bo1, k1, _ = ob.bucket_plan(data.lengths, 1)
     b1 = osch.epoch_batches(data.lengths, bo1, k1, keys, w.batch)
     assert osch.padded_batch_steps(data.lengths, b1) >= osch.padded_batch_steps(data.lengths, batches)
+
+
+def _hand_schedule():
+    # 9 sequences in 3 buckets; bucket 0 = {0, 1, 2}, 1 = {3, 4, 5, 6}, 2 = {7, 8}
+    lengths = np.array([3, 2, 3, 6, 5, 6, 4, 9, 8], np.int32)
+    bucket_of = np.array([0, 0, 0, 1, 1, 1, 1, 2, 2], np.int32)
+    keys = np.array([2, 1, 0, 7, 5, 6, 4, 1, 0], np.uint64)
+    return lengths, bucket_of, keys
+
+
+def test_orderings_hand_worked():
+    """Batches worked out by hand from the definitions (B = 2): inside each
+    bucket the sequences go by key, pairs form the batches, each batch is
+    sorted longest first."""
+    lengths, bucket_of, keys = _hand_schedule()
+    # bucket 0 by key: 2, 1, 0 -> pairs [2, 1], [0]; bucket 1 by key: 6, 4, 5, 3
+    # -> pairs [4, 6] (4 is longer), [3, 5];
+    # bucket 2 by key: 8, 7 -> sorted longest first [7, 8];
+    # equal lengths (3 and 5) go by index
+    asc = [[2, 1], [0], [4, 6], [3, 5], [7, 8]]
+    got = osch.epoch_batches(lengths, bucket_of, 3, keys, 2)
+    assert [b.tolist() for b in got] == asc
+    got = osch.epoch_batches(lengths, bucket_of, 3, keys, 2, "descending")
+    assert [b.tolist() for b in got] == [[7, 8], [4, 6], [3, 5], [2, 1], [0]]
+    ok = np.array([9, 3, 3, 0, 0, 0, 0, 0, 0], np.uint64)  # bucket order 1, 2, 0
+    got = osch.epoch_batches(lengths, bucket_of, 3, keys, 2, "random_buckets", ok)
+    assert [b.tolist() for b in got] == [[4, 6], [3, 5], [7, 8], [2, 1], [0]]
+    ok = np.array([4, 0, 3, 0, 1, 0, 0, 0, 0], np.uint64)  # fed: batches 1, 3, 4, 2, 0
+    got = osch.epoch_batches(lengths, bucket_of, 3, keys, 2, "shuffled_batches", ok)
+    assert [b.tolist() for b in got] == [[0], [3, 5], [7, 8], [4, 6], [2, 1]]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_orderings_are_permutations_of_the_same_batches(seed):
+    w = synth.WORKLOADS["tiny"]
+    data = synth.make_workload(w, seed)
+    _, bucket_of, K_eff, _ = ob.bucket_plan(data.lengths, 3)
+    keys = synth.shuffle_keys(seed, 0, w.n)
+    ok = synth.order_keys(seed, 0, w.n)
+    asc = osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch)
+    ref = sorted(tuple(b.tolist()) for b in asc)
+    for ordering in osch.ORDERINGS:
+        got = osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch, ordering, ok)
+        assert sorted(tuple(b.tolist()) for b in got) == ref
+        runs = [int(bucket_of[b[0]]) for b in got]
+        if ordering == "descending":
+            assert runs == sorted(runs, reverse=True)
+        if ordering in ("ascending", "descending", "random_buckets"):
+            # whole buckets stay together: each bucket is one contiguous run
+            seen = [r for i, r in enumerate(runs) if i == 0 or runs[i - 1] != r]
+            assert len(seen) == len(set(seen)) == K_eff
+    # keys that rank the batches (or buckets) in their ascending order change nothing
+    rising = np.arange(w.n, dtype=np.uint64)
+    for ordering in ("random_buckets", "shuffled_batches"):
+        got = osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch, ordering, rising)
+        assert [b.tolist() for b in got] == [b.tolist() for b in asc]
+    falling = rising[::-1].copy()
+    got = osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch, "random_buckets",
+                             falling)
+    desc = osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch, "descending")
+    assert [b.tolist() for b in got] == [b.tolist() for b in desc]
+    got = osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch, "shuffled_batches",
+                             falling)
+    assert [b.tolist() for b in got] == [b.tolist() for b in asc[::-1]]
+    with pytest.raises(ValueError):
+        osch.epoch_batches(data.lengths, bucket_of, K_eff, keys, w.batch, "sideways")
