@@ -11,6 +11,12 @@ zero initial state:
     a_t = W_ih x_t + W_hh h_{t-1} + b
     i = sig(a_i), f = sig(a_f), g = tanh(a_g), o = sig(a_o)
     c_t = f * c_{t-1} + i * g,   h_t = o * tanh(c_t)
+LSTM with peepholes (the paper trains its LSTM with Lasagne, Sec. IV.A,
+whose LSTM layer has them by default): diagonal weights p_i, p_f, p_o let the
+input and forget gates see the previous cell state and the output gate the
+new one,
+    i = sig(a_i + p_i * c_{t-1}), f = sig(a_f + p_f * c_{t-1}), g = tanh(a_g)
+    c_t = f * c_{t-1} + i * g,   o = sig(a_o + p_o * c_t),   h_t = o * tanh(c_t)
 GRU, gates r, z, n, the reset gate scaling the whole recurrent term of n:
     r = sig(W_ir x + b_ir + W_hr h + b_hr)
     z = sig(W_iz x + b_iz + W_hz h + b_hz)
@@ -29,6 +35,7 @@ Flat parameter layout (float32 on the wire, float64 inside), row-major:
   for each layer, for each direction (forward first):
     W_ih [G*H, D_in], W_hh [G*H, H], then
     LSTM: b [4H]          GRU: b_ih [3H], b_hh [3H]
+    LSTM with peepholes: b [4H], then p [3H] = (p_i, p_f, p_o)
   then W_out [C, H_top], b_out [C]
 with G = 4 (LSTM) or 3 (GRU), D_in = input dim for layer 0 and
 H * (2 if bidirectional else 1) above, H_top = the same width for the top.
@@ -41,6 +48,7 @@ import numpy as np
 
 LSTM = 0
 GRU = 1
+LSTM_PEEPHOLE = 2
 
 
 @dataclasses.dataclass(frozen=True)
@@ -54,7 +62,11 @@ class Model:
 
     @property
     def gates(self) -> int:
-        return 4 if self.cell == LSTM else 3
+        return 3 if self.cell == GRU else 4
+
+    @property
+    def is_lstm(self) -> bool:
+        return self.cell in (LSTM, LSTM_PEEPHOLE)
 
     @property
     def dirs(self) -> int:
@@ -72,8 +84,10 @@ def param_layout(m: Model):
         for d in range(m.dirs):
             out.append((("W_ih", l, d), (G * H, m.layer_input(l))))
             out.append((("W_hh", l, d), (G * H, H)))
-            if m.cell == LSTM:
+            if m.is_lstm:
                 out.append((("b", l, d), (G * H,)))
+                if m.cell == LSTM_PEEPHOLE:
+                    out.append((("p", l, d), (3 * H,)))
             else:
                 out.append((("b_ih", l, d), (G * H,)))
                 out.append((("b_hh", l, d), (G * H,)))
@@ -111,11 +125,13 @@ def _time_order(L: int, d: int):
     return range(L) if d == 0 else range(L - 1, -1, -1)
 
 
-def lstm_dir_forward(W_ih, W_hh, b, X, d):
-    """One direction of one LSTM layer over one sequence X [L, D_in].
+def lstm_dir_forward(W_ih, W_hh, b, X, d, peep=None):
+    """One direction of one LSTM layer over one sequence X [L, D_in];
+    `peep` = [p_i ; p_f ; p_o] (3H) for the peephole cell, else None.
     Returns (Hseq [L, H], cache)."""
     L = X.shape[0]
     H = W_hh.shape[1]
+    p_i, p_f, p_o = (np.zeros(H),) * 3 if peep is None else np.reshape(peep, (3, H))
     ax = X @ W_ih.T + b                           # input part of a_t, all t
     Hs = np.zeros((L, H))
     cache = {"i": np.zeros((L, H)), "f": np.zeros((L, H)), "g": np.zeros((L, H)),
@@ -125,13 +141,13 @@ def lstm_dir_forward(W_ih, W_hh, b, X, d):
     c = np.zeros(H)
     for t in _time_order(L, d):
         a = ax[t] + W_hh @ h
-        i = _sig(a[0:H])
-        f = _sig(a[H:2 * H])
+        i = _sig(a[0:H] + p_i * c)
+        f = _sig(a[H:2 * H] + p_f * c)
         g = np.tanh(a[2 * H:3 * H])
-        o = _sig(a[3 * H:4 * H])
         cache["h_prev"][t] = h
         cache["c_prev"][t] = c
         c = f * c + i * g
+        o = _sig(a[3 * H:4 * H] + p_o * c)
         h = o * np.tanh(c)
         Hs[t] = h
         for k, v in (("i", i), ("f", f), ("g", g), ("o", o), ("c", c)):
@@ -139,35 +155,41 @@ def lstm_dir_forward(W_ih, W_hh, b, X, d):
     return Hs, cache
 
 
-def lstm_dir_backward(W_ih, W_hh, X, cache, dH, d):
+def lstm_dir_backward(W_ih, W_hh, X, cache, dH, d, peep=None):
     """Reverse-mode pass of ``lstm_dir_forward`` given dLoss/dh_t = dH [L, H].
-    Returns (dW_ih, dW_hh, db, dX)."""
+    Returns (dW_ih, dW_hh, db, dX, dpeep); dpeep (3H) is zero without
+    peepholes."""
     L = X.shape[0]
     H = W_hh.shape[1]
+    p_i, p_f, p_o = (np.zeros(H),) * 3 if peep is None else np.reshape(peep, (3, H))
     dA = np.zeros((L, 4 * H))
     dh_rec = np.zeros(H)      # gradient reaching h_t through the next step's W_hh
-    dc_rec = np.zeros(H)      # gradient reaching c_t through the next step's forget gate
+    dc_rec = np.zeros(H)      # gradient reaching c_t through the next step's gates
     dW_hh = np.zeros_like(W_hh)
+    dp = np.zeros((3, H))
     for t in reversed(list(_time_order(L, d))):
         i, f, g, o = cache["i"][t], cache["f"][t], cache["g"][t], cache["o"][t]
         c, c_prev, h_prev = cache["c"][t], cache["c_prev"][t], cache["h_prev"][t]
         dh = dH[t] + dh_rec
         tc = np.tanh(c)
-        dc = dh * o * (1.0 - tc * tc) + dc_rec
-        da = np.concatenate([
-            dc * g * i * (1.0 - i),          # input gate
-            dc * c_prev * f * (1.0 - f),     # forget gate
-            dc * i * (1.0 - g * g),          # cell candidate
-            dh * tc * o * (1.0 - o),         # output gate
-        ])
+        da_o = dh * tc * o * (1.0 - o)       # output gate
+        # c_t reaches the loss through h_t, the output gate's peephole and
+        # (dc_rec) the next step
+        dc = dh * o * (1.0 - tc * tc) + da_o * p_o + dc_rec
+        da_i = dc * g * i * (1.0 - i)        # input gate
+        da_f = dc * c_prev * f * (1.0 - f)   # forget gate
+        da_g = dc * i * (1.0 - g * g)        # cell candidate
+        da = np.concatenate([da_i, da_f, da_g, da_o])
         dA[t] = da
         dW_hh += np.outer(da, h_prev)
+        dp += np.stack([da_i * c_prev, da_f * c_prev, da_o * c])
         dh_rec = W_hh.T @ da
-        dc_rec = dc * f
+        # c_{t-1} reaches the loss through the forget path and the two peepholes
+        dc_rec = dc * f + da_i * p_i + da_f * p_f
     dW_ih = dA.T @ X
     db = dA.sum(axis=0)
     dX = dA @ W_ih
-    return dW_ih, dW_hh, db, dX
+    return dW_ih, dW_hh, db, dX, dp.reshape(-1)
 
 
 def gru_dir_forward(W_ih, W_hh, b_ih, b_hh, X, d):
@@ -245,9 +267,10 @@ def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True, ctc_target
         for l in range(m.num_layers):
             outs = []
             for d in range(dirs):
-                if m.cell == LSTM:
+                if m.is_lstm:
                     Hs, cache = lstm_dir_forward(p[("W_ih", l, d)], p[("W_hh", l, d)],
-                                                 p[("b", l, d)], inputs[-1], d)
+                                                 p[("b", l, d)], inputs[-1], d,
+                                                 p.get(("p", l, d)))
                 else:
                     Hs, cache = gru_dir_forward(p[("W_ih", l, d)], p[("W_hh", l, d)],
                                                 p[("b_ih", l, d)], p[("b_hh", l, d)],
@@ -281,10 +304,13 @@ def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True, ctc_target
             for d in range(dirs):
                 cache = caches[l * dirs + d]
                 dH = dIn[:, d * H:(d + 1) * H]
-                if m.cell == LSTM:
-                    gWi, gWh, gb, gX = lstm_dir_backward(p[("W_ih", l, d)], p[("W_hh", l, d)],
-                                                         X, cache, dH, d)
+                if m.is_lstm:
+                    gWi, gWh, gb, gX, gp = lstm_dir_backward(p[("W_ih", l, d)],
+                                                             p[("W_hh", l, d)], X, cache, dH, d,
+                                                             p.get(("p", l, d)))
                     grads[("b", l, d)] += gb
+                    if m.cell == LSTM_PEEPHOLE:
+                        grads[("p", l, d)] += gp
                 else:
                     gWi, gWh, gbi, gbh, gX = gru_dir_backward(p[("W_ih", l, d)], p[("W_hh", l, d)],
                                                               X, cache, dH, d)

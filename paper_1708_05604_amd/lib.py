@@ -26,6 +26,7 @@ EHIP = -3
 
 CELL_LSTM = 0
 CELL_GRU = 1
+CELL_LSTM_PEEPHOLE = 2
 GEMM_FP32 = 0
 GEMM_BF16 = 1
 

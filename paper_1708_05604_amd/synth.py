@@ -39,6 +39,7 @@ import numpy as np
 
 LSTM = 0
 GRU = 1
+LSTM_PEEPHOLE = 2
 FP32 = 0
 BF16 = 1
 
@@ -46,7 +47,7 @@ BF16 = 1
 @dataclasses.dataclass(frozen=True)
 class Workload:
     name: str
-    cell: int            # LSTM or GRU
+    cell: int            # LSTM, GRU or LSTM_PEEPHOLE
     num_layers: int
     bidirectional: int   # 0 or 1
     input_dim: int

@@ -247,3 +247,93 @@ def test_param_count_formula():
     assert rnn.param_count(m) == 3733584
     m = rnn.Model(rnn.GRU, 2, 0, 8, 384, 80)
     assert rnn.param_count(m) == 1371728
+
+
+# ------------------------------------------------------------ peephole LSTM
+
+PEEP_MODELS = [
+    rnn.Model(rnn.LSTM_PEEPHOLE, 1, 0, 3, 4, 5),
+    rnn.Model(rnn.LSTM_PEEPHOLE, 2, 1, 2, 3, 4),
+]
+
+
+def _sig(v):
+    return 1.0 / (1.0 + math.exp(-v))
+
+
+def test_peephole_closed_form_two_steps():
+    """Weights zero, biases and peepholes set: the first two steps worked out
+    by hand.  Step 0 starts from c = 0, so only the output gate's peephole
+    (which sees the new cell state) acts; step 1 brings in p_i and p_f through
+    c_0.  Distinct p_i, p_f, p_o catch a swapped or mis-timed peephole."""
+    H = 2
+    m = rnn.Model(rnn.LSTM_PEEPHOLE, 1, 0, 2, H, 3)
+    p = {k: np.zeros(s) for k, s in rnn.param_layout(m)}
+    b_i, b_f, b_g, b_o = [0.4, -0.3], [0.2, 0.9], [1.1, -0.7], [-0.5, 0.3]
+    p_i, p_f, p_o = [1.5, -0.8], [-1.2, 0.6], [2.0, -2.5]
+    p[("b", 0, 0)][:] = np.concatenate([b_i, b_f, b_g, b_o])
+    p[("p", 0, 0)][:] = np.concatenate([p_i, p_f, p_o])
+    theta = rnn.pack(m, p)
+    x = np.random.default_rng(2).standard_normal((2, 2))
+    _, _, tops = rnn.forward_backward(m, theta, [x], [np.zeros(2, int)], need_grad=False)
+    for u in range(H):
+        c0 = _sig(b_i[u]) * math.tanh(b_g[u])
+        h0 = _sig(b_o[u] + p_o[u] * c0) * math.tanh(c0)
+        c1 = _sig(b_f[u] + p_f[u] * c0) * c0 + _sig(b_i[u] + p_i[u] * c0) * math.tanh(b_g[u])
+        h1 = _sig(b_o[u] + p_o[u] * c1) * math.tanh(c1)
+        np.testing.assert_allclose(tops[0][:, u], [h0, h1], rtol=1e-15, atol=0)
+
+
+@pytest.mark.parametrize("ctc", [False, True])
+def test_peephole_zero_is_the_plain_lstm(ctc):
+    """With p = 0 the peephole cell is the plain LSTM: the outputs, the loss
+    and every shared gradient block agree exactly."""
+    mp = rnn.Model(rnn.LSTM_PEEPHOLE, 2, 1, 3, 4, 5)
+    m0 = rnn.Model(rnn.LSTM, 2, 1, 3, 4, 5)
+    rng = np.random.default_rng(7)
+    p0 = {k: rng.uniform(-0.5, 0.5, s) for k, s in rnn.param_layout(m0)}
+    pp = dict(p0)
+    for l in range(2):
+        for d in range(2):
+            pp[("p", l, d)] = np.zeros(12)
+    lengths = [6, 4, 4, 1]
+    xs, ys = _rand_batch(rng, lengths, 3, 5)
+    tg = _rand_targets(rng, lengths, 5) if ctc else None
+    l0, g0, t0 = rnn.forward_backward(m0, rnn.pack(m0, p0), xs, ys, ctc_targets=tg)
+    lp, gp, tp = rnn.forward_backward(mp, rnn.pack(mp, pp), xs, ys, ctc_targets=tg)
+    assert l0 == lp
+    for a, b in zip(t0, tp):
+        np.testing.assert_array_equal(a, b)
+    g0, gp = rnn.unpack(m0, g0), rnn.unpack(mp, gp)
+    for k in g0:
+        np.testing.assert_array_equal(g0[k], gp[k])
+
+
+@pytest.mark.parametrize("mi", range(len(PEEP_MODELS)))
+@pytest.mark.parametrize("ctc", [False, True])
+def test_peephole_finite_differences(mi, ctc):
+    m = PEEP_MODELS[mi]
+    rng = np.random.default_rng(60 + mi)
+    theta = rng.uniform(-0.8, 0.8, rnn.param_count(m))
+    lengths = [6, 4, 1]
+    xs, ys = _rand_batch(rng, lengths, m.input_dim, m.num_classes)
+    tg = _rand_targets(rng, lengths, m.num_classes) if ctc else None
+    _, grad, _ = rnn.forward_backward(m, theta, xs, ys, ctc_targets=tg)
+    h = 1e-6
+    fd = np.zeros_like(theta)
+    for k in range(theta.size):
+        tp = theta.copy(); tp[k] += h
+        tm = theta.copy(); tm[k] -= h
+        fd[k] = (rnn.forward_backward(m, tp, xs, ys, False, tg)[0]
+                 - rnn.forward_backward(m, tm, xs, ys, False, tg)[0]) / (2 * h)
+    err = np.abs(fd - grad) / np.maximum(np.abs(grad), 1e-3)
+    assert err.max() < 1e-6, err.max()
+    # the peephole blocks carry gradient (a dropped term would leave them 0)
+    g = rnn.unpack(m, grad)
+    assert all(np.abs(v).max() > 1e-4 for (kind, _, _), v in g.items() if kind == "p")
+
+
+def test_peephole_param_count():
+    m = rnn.Model(rnn.LSTM_PEEPHOLE, 2, 0, 8, 128, 80)
+    plain = rnn.Model(rnn.LSTM, 2, 0, 8, 128, 80)
+    assert rnn.param_count(m) == rnn.param_count(plain) + 2 * 3 * 128
