@@ -70,7 +70,7 @@ def flops_per_useful_step(w: synth.Workload) -> int:
     """Matrix-core flops per valid frame of one training step (input and
     recurrent products forward, the same products and the weight gradients
     backward, output layer forward and backward)."""
-    G = 4 if w.cell == synth.LSTM else 3
+    G = 3 if w.cell == synth.GRU else 4
     H, dirs = w.hidden, 2 if w.bidirectional else 1
     GH = G * H
     total = 0
@@ -84,7 +84,7 @@ def flops_per_useful_step(w: synth.Workload) -> int:
 
 
 def describe(w: synth.Workload, K: int) -> str:
-    cell = "LSTM" if w.cell == synth.LSTM else "GRU"
+    cell = {synth.LSTM: "LSTM", synth.GRU: "GRU", synth.LSTM_PEEPHOLE: "peephole LSTM"}[w.cell]
     bi = "bidirectional " if w.bidirectional else ""
     return (f"{w.name}: {w.num_layers}-layer {bi}{cell} D={w.input_dim} H={w.hidden} "
             f"C={w.num_classes}, {w.n} sequences {w.law}{w.law_args}, B={w.batch}, K={K}, "

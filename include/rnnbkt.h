@@ -43,6 +43,8 @@ extern "C" {
 
 #define RNNBKT_CELL_LSTM 0 /* gates i, f, g, o */
 #define RNNBKT_CELL_GRU 1  /* gates r, z, n */
+#define RNNBKT_CELL_LSTM_PEEPHOLE 2 /* LSTM with diagonal peepholes (Sec. IV.A: the
+                                       paper's Lasagne LSTM has them by default) */
 
 #define RNNBKT_GEMM_FP32 0 /* GEMM operands and accumulation in fp32 */
 #define RNNBKT_GEMM_BF16 1 /* GEMM operands rounded to bf16 (nearest-even), fp32 accumulate */
@@ -141,11 +143,11 @@ int32_t rnnbkt_epoch_schedule_ordered(const int32_t* lengths, const int32_t* buc
                                       const uint64_t* order_keys, int64_t* order,
                                       int64_t* batch_start, int64_t* num_batches);
 
-/* Model description.  Shapes: G = 4 (LSTM) or 3 (GRU) gates, H = hidden,
+/* Model description.  Shapes: G = 4 (LSTM, either kind) or 3 (GRU) gates, H = hidden,
  * dirs = 2 if bidirectional else 1, D_in(layer 0) = input_dim,
  * D_in(layer > 0) = dirs * H, H_top = dirs * H. */
 typedef struct {
-  int32_t cell;          /* RNNBKT_CELL_LSTM or RNNBKT_CELL_GRU */
+  int32_t cell;          /* RNNBKT_CELL_LSTM, RNNBKT_CELL_GRU or RNNBKT_CELL_LSTM_PEEPHOLE */
   int32_t num_layers;    /* >= 1 */
   int32_t input_dim;     /* multiple of 4 */
   int32_t hidden;        /* multiple of 32 */
@@ -160,9 +162,12 @@ typedef struct {
  *     W_ih [G*H, D_in]  gate blocks in the order above
  *     W_hh [G*H, H]
  *     LSTM: b [G*H]          GRU: b_ih [3H], then b_hh [3H]
+ *     LSTM with peepholes: b [G*H], then p [3H] = (p_i, p_f, p_o)
  *   W_out [C, H_top], b_out [C]
  * LSTM:  a = W_ih x + W_hh h + b; i,f,o = sigmoid, g = tanh;
  *        c' = f*c + i*g; h' = o*tanh(c').
+ * Peephole LSTM: as LSTM but i = sigmoid(a_i + p_i*c), f = sigmoid(a_f +
+ *        p_f*c), and after the cell update o = sigmoid(a_o + p_o*c').
  * GRU:   r,z = sigmoid(W_i x + b_i + W_h h + b_h) of their blocks;
  *        n = tanh(W_in x + b_in + r*(W_hn h + b_hn)); h' = (1-z)*n + z*h.
  * Initial states are zero; the reverse direction runs over each sequence's

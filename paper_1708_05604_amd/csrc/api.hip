@@ -22,14 +22,17 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Shape {
   int G, H, D, C, L, dirs, Htop;
   bool bf16;
-  int cell;
+  int cell;   // RNNBKT_CELL_LSTM (either kind) or RNNBKT_CELL_GRU
+  bool peep;  // LSTM with peepholes
   int din(int l) const { return l == 0 ? D : dirs * H; }
 };
 
 int32_t check_desc(const rnnbkt_model_desc* d, Shape* s) {
   RNNBKT_REQUIRE(d != nullptr, RNNBKT_EINVAL, "model desc is null");
-  RNNBKT_REQUIRE(d->cell == RNNBKT_CELL_LSTM || d->cell == RNNBKT_CELL_GRU, RNNBKT_EINVAL,
-                 "desc.cell must be 0 (LSTM) or 1 (GRU), got %d", d->cell);
+  RNNBKT_REQUIRE(d->cell == RNNBKT_CELL_LSTM || d->cell == RNNBKT_CELL_GRU ||
+                     d->cell == RNNBKT_CELL_LSTM_PEEPHOLE,
+                 RNNBKT_EINVAL, "desc.cell must be 0 (LSTM), 1 (GRU) or 2 (peephole LSTM), got %d",
+                 d->cell);
   RNNBKT_REQUIRE(d->num_layers >= 1 && d->input_dim >= 1 && d->hidden >= 1 &&
                      d->num_classes >= 1,
                  RNNBKT_EINVAL, "desc sizes must be >= 1");
@@ -43,8 +46,9 @@ int32_t check_desc(const rnnbkt_model_desc* d, Shape* s) {
                  "input_dim must be a multiple of 4 (got %d)", d->input_dim);
   RNNBKT_REQUIRE(d->num_classes % 4 == 0 && d->num_classes <= 1024, RNNBKT_EUNSUPPORTED,
                  "num_classes must be a multiple of 4 and <= 1024 (got %d)", d->num_classes);
-  s->cell = d->cell;
-  s->G = d->cell == RNNBKT_CELL_LSTM ? 4 : 3;
+  s->cell = d->cell == RNNBKT_CELL_GRU ? RNNBKT_CELL_GRU : RNNBKT_CELL_LSTM;
+  s->peep = d->cell == RNNBKT_CELL_LSTM_PEEPHOLE;
+  s->G = s->cell == RNNBKT_CELL_LSTM ? 4 : 3;
   s->H = d->hidden;
   s->D = d->input_dim;
   s->C = d->num_classes;
@@ -57,7 +61,7 @@ int32_t check_desc(const rnnbkt_model_desc* d, Shape* s) {
 
 // Offsets (in floats) of each block of the flat parameter vector.
 struct ParamOffsets {
-  std::vector<int64_t> wih, whh, b, bhh;  // indexed by layer*dirs + dir
+  std::vector<int64_t> wih, whh, b, bhh, peep;  // indexed by layer*dirs + dir
   int64_t wout = 0, bout = 0, total = 0;
 };
 
@@ -78,6 +82,12 @@ ParamOffsets param_offsets(const Shape& s) {
         pos += GH;
       } else {
         p.bhh.push_back(-1);
+      }
+      if (s.peep) {
+        p.peep.push_back(pos);
+        pos += 3 * (int64_t)s.H;
+      } else {
+        p.peep.push_back(-1);
       }
     }
   p.wout = pos;
@@ -119,9 +129,10 @@ struct Carve {
   size_t gx[2], loss_part;
   size_t ws_fwd;
   // workspace (backward)
-  size_t dha, dhb, carry, splitk, colsum;
+  size_t dha, dhb, carry, peep_acc, splitk, colsum;
   std::vector<size_t> da, dah;  // per layer*dirs
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
+  std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
 
   size_t ws_bwd;
   size_t workspace;
@@ -165,6 +176,7 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     c.dah.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0);
   }
   c.carry = take(sizeof(float) * (size_t)B * s.H);
+  c.peep_acc = s.peep ? take(sizeof(float) * (size_t)B * 3 * s.H) : 0;
   size_t sk = 0;
   auto need = [&](int64_t M, int64_t Nn, int64_t K) {
     const SplitK p = choose_splitk(M, Nn, K);
@@ -176,12 +188,14 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     need(GH, s.H, N);
   }
   c.splitk = take(sizeof(float) * std::max<size_t>(sk, 1));
-  const int64_t cs_splits = (N + colsum_rows(N) - 1) / colsum_rows(N);
-  c.colsum = take(sizeof(float) * cs_splits * std::max<int64_t>(GH, s.C));
+  // Column sums run over N frames (bias gradients) or B rows (peephole
+  // running sums): at most kColsumSplits partial rows either way.
+  c.colsum = take(sizeof(float) * kColsumSplits * std::max<int64_t>(GH, s.C));
   const int rgroups = (B + 15) / 16;
   for (int q = 0; q < s.L * s.dirs; ++q) {
     c.bpart.push_back(take(sizeof(float) * rgroups * GH));
     c.bpart_h.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * rgroups * GH) : 0);
+    c.ppart.push_back(s.peep ? take(sizeof(float) * rgroups * 3 * s.H) : 0);
   }
   c.ws_bwd = pos;
   c.workspace = std::max(c.ws_fwd, c.ws_bwd);
@@ -488,6 +502,7 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     u.out_bytes = hout_bytes < 0x7FFFFFF0u ? (uint32_t)hout_bytes : 0x7FFFFFF0u;
     u.stash = at<float>(reserve, c.stash[ld]);
     u.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+    u.peep = s.peep ? params + po.peep[ld] : nullptr;
     u.dir = d;
     u.hcol = d * s.H;
     return u;
@@ -573,6 +588,7 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       a.hout = hout + d * s.H;
       a.stash = at<float>(reserve, c.stash[ld]);
       a.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
+      a.peep = s.peep ? params + po.peep[ld] : nullptr;
       a.H = s.H;
       a.ldh = ldh;
       for (int k = 0; k < T; ++k) {
@@ -757,6 +773,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     u.dah = dah_of(l, d);
     u.bias_part = at<float>(workspace, c.bpart[ld]);
     u.bias_part_h = gru ? at<float>(workspace, c.bpart_h[ld]) : nullptr;
+    u.peep = s.peep ? params + po.peep[ld] : nullptr;
+    u.peep_part = s.peep ? at<float>(workspace, c.ppart[ld]) : nullptr;
     u.rec_bytes = rec_bytes;
     u.publish_dax = publish_dax ? 1 : 0;
     u.dir = d;
@@ -865,6 +883,13 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         a.da = da_of(l, d);
         a.dah = dah_of(l, d);
         a.carry = carry;
+        a.peep = s.peep ? params + po.peep[ld] : nullptr;
+        a.peep_acc = s.peep ? at<float>(workspace, c.peep_acc) : nullptr;
+        if (a.peep_acc) {
+          Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+          RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(a.peep_acc),
+                                     (int64_t)B * 3 * s.H, 0u, st));
+        }
         a.H = s.H;
         a.ldd = s.Htop;
         a.ldh = s.dirs * s.H;
@@ -885,6 +910,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
           }
           Timed tm(RNNBKT_KERNEL_STEP_BWD, 2.0 * a.next_rows * GH * s.H, 0.0, st);
           RNNBKT_HIP(launch_step_bwd(a, s.cell, s.bf16, st));
+        }
+        if (a.peep_acc) {
+          // Peephole gradients: the per-row running sums, summed over rows.
+          Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+          RNNBKT_HIP(launch_colsum(a.peep_acc, B, 3 * s.H, 3 * s.H, colsum_rows(B), cs,
+                                   grads + po.peep[ld], st));
         }
       }
       if (l > 0) {
@@ -921,6 +952,10 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
           if (gru)
             RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.bpart_h[ld]), rgroups, 1, GH,
                                             grads + po.bhh[ld], GH, nullptr, 0, st));
+          if (s.peep)
+            RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.ppart[ld]), rgroups, 1,
+                                            3 * s.H, grads + po.peep[ld], 3 * s.H, nullptr, 0,
+                                            st));
         } else {
           RNNBKT_HIP(launch_colsum(dax, N, GH, GH, colsum_rows(N), cs, grads + po.b[ld], st));
           if (gru)

@@ -139,6 +139,7 @@ struct StepFwdArgs {
   float* hout;       // layer output, already offset to this direction's columns
   float* stash;      // [N x 4H] gate activations (LSTM i,f,g,o; GRU r,z,n,W_hn h + b_hn)
   float* cst;        // LSTM: [N x H] cell state; GRU: unused
+  const float* peep; // LSTM peepholes [3H] (p_i, p_f, p_o), or nullptr
   int32_t H, ldh;
   int32_t row0, rows;
   int32_t prev0, prev_rows;
@@ -155,7 +156,11 @@ struct StepBwdArgs {
   const float* hout;     // GRU: layer output (previous state), offset to direction
   float* da;             // [N x G*H] LSTM dA / GRU dAx
   float* dah;            // GRU: [N x 3H] dAh
-  float* carry;          // [B x H] LSTM dc*f, GRU dh*z of the next step
+  float* carry;          // [B x H] LSTM: gradient reaching c_t from the next step
+                         // (dc*f + peephole terms); GRU: dh*z of the next step
+  const float* peep;     // LSTM peepholes [3H], or nullptr
+  float* peep_acc;       // with peep: [B x 3H] per-row sums over the steps of
+                         // da_i*c_{t-1}, da_f*c_{t-1}, da_o*c_t (zeroed before the first step)
   int32_t H, ldd, ldh;
   int32_t row0, rows;
   int32_t next0, next_rows;
@@ -188,6 +193,7 @@ struct FwdUnit {
   float* hout;         // layer output base [N x ldh]; this unit writes columns hcol..hcol+H-1
   float* stash;        // [N x 4H] (LSTM i,f,g,o; GRU r,z,n,W_hn h + b_hn)
   float* cst;          // LSTM [N x H]; GRU unused
+  const float* peep;   // LSTM peepholes [3H] (p_i, p_f, p_o), or nullptr
   uint32_t in_bytes;   // bytes of the array `in` addresses (< 2^31 - 16)
   uint32_t out_bytes;  // bytes of hout (< 2^31 - 16)
   int32_t ld_in, kin;  // input row stride and length
@@ -222,6 +228,8 @@ struct BwdUnit {
   float* dah;            // GRU dAh [N x 3H]
   float* bias_part;      // [rgroups x G*H]: per row group, sum over frames of dA / dAx
   float* bias_part_h;    // GRU: [rgroups x 3H] sums of dAh
+  const float* peep;     // LSTM peepholes [3H], or nullptr
+  float* peep_part;      // with peep: [rgroups x 3H] sums of da_i*c_{t-1}, da_f*c_{t-1}, da_o*c_t
   uint32_t up_bytes;     // bytes of `up`'s array (< 2^31 - 16)
   uint32_t rec_bytes;    // bytes of the recurrent array (LSTM da, GRU dah; < 2^31 - 16)
   int32_t k_up, din_up;  // columns of `up` and of W_ih above

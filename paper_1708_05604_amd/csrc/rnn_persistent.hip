@@ -331,7 +331,15 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   const int erow = r0 + (lane >> 2);
   const int ej = j0 + 4 * (epi ? wave : 0) + (lane & 3);
   float bi[4] = {0.f, 0.f, 0.f, 0.f}, bh[3] = {0.f, 0.f, 0.f};
+  // LSTM peepholes of this unit (the test is uniform over the workgroup).
+  const bool peep = G == 4 && U.peep != nullptr;
+  float pi = 0.f, pf = 0.f, po = 0.f;
   if (epi) {
+    if (peep) {
+      pi = U.peep[ej];
+      pf = U.peep[H + ej];
+      po = U.peep[2 * H + ej];
+    }
 #pragma unroll
     for (int g = 0; g < G; ++g) bi[g] = U.b[g * H + ej];
     if constexpr (G == 3) {
@@ -394,12 +402,18 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
       const int64_t f = s.row0 + erow;
       float* st = U.stash + f * 4 * H;
       if constexpr (G == 4) {
-        const float ig = act_sigmoid(sg[0] + bi[0]);
-        const float fg = act_sigmoid(sg[1] + bi[1]);
-        const float gg = act_tanh(sg[2] + bi[2]);
-        const float og = act_sigmoid(sg[3] + bi[3]);
         const float cp = has_prev ? c_state : 0.f;
+        float ai = sg[0] + bi[0], af = sg[1] + bi[1], ao = sg[3] + bi[3];
+        if (peep) {
+          ai += pi * cp;
+          af += pf * cp;
+        }
+        const float ig = act_sigmoid(ai);
+        const float fg = act_sigmoid(af);
+        const float gg = act_tanh(sg[2] + bi[2]);
         c_state = fg * cp + ig * gg;
+        if (peep) ao += po * c_state;
+        const float og = act_sigmoid(ao);
         h_state = og * act_tanh(c_state);
         publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
         st[ej] = ig;
@@ -526,7 +540,15 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   const int ej = j0 + (threadIdx.x & 15);
   float carry = 0.f;
   float bsum[4] = {0.f, 0.f, 0.f, 0.f};  // sum over steps of this (row, unit)'s dA (LSTM) / dAx (GRU)
-  float bsumh[3] = {0.f, 0.f, 0.f};      // GRU: sum of dAh
+  float bsumh[3] = {0.f, 0.f, 0.f};      // GRU: sum of dAh; peephole LSTM: peephole gradients
+  // LSTM peepholes of this unit (the test is uniform over the workgroup).
+  const bool peep = G == 4 && U.peep != nullptr;
+  float pi = 0.f, pf = 0.f, po = 0.f;
+  if (epi && peep) {
+    pi = U.peep[ej];
+    pf = U.peep[H + ej];
+    po = U.peep[2 * H + ej];
+  }
   const float* rec = G == 3 ? U.dah : U.da;
   const __amdgpu_buffer_rsrc_t rup = published_rsrc(has_up ? U.up : U.da, has_up ? U.up_bytes : 0u);
   const __amdgpu_buffer_rsrc_t rrec = published_rsrc(rec, U.rec_bytes);
@@ -595,22 +617,31 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       if constexpr (G == 4) {
         const float dh = dhv + dh_red;
         const float tc = act_tanh(cc);
-        const float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
+        const float dout = dh * tc * st3 * (1.f - st3);
+        // c_t reaches the loss through h_t, the next step and the output peephole
+        float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
+        if (peep) dc += dout * po;
         const float cp = has_prev ? cprev : 0.f;
         const float di = dc * st2 * st0 * (1.f - st0);
         const float df = dc * cp * st1 * (1.f - st1);
         const float dg = dc * st0 * (1.f - st2 * st2);
-        const float dout = dh * tc * st3 * (1.f - st3);
         float* dar = U.da + f * GH;
         publish(dar + ej, di);
         publish(dar + H + ej, df);
         publish(dar + 2 * H + ej, dg);
         publish(dar + 3 * H + ej, dout);
+        // c_{t-1} reaches the loss through the forget path and two peepholes
         carry = dc * st1;
         bsum[0] += di;
         bsum[1] += df;
         bsum[2] += dg;
         bsum[3] += dout;
+        if (peep) {
+          carry += di * pi + df * pf;
+          bsumh[0] += di * cp;
+          bsumh[1] += df * cp;
+          bsumh[2] += dout * cc;
+        }
       } else {
         const float dh = dhv + dh_red + (has_next ? carry : 0.f);
         const float rr = st0, z = st1, n = st2, ahn = st3;
@@ -643,24 +674,29 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   }
   // Bias gradients of this workgroup: sum its 16 rows in a fixed order and
   // write one partial per row group (folded over row groups afterwards).
+  // Peephole gradients likewise (LSTM with peepholes): slots 4..6.
+  const bool second = G == 3 || peep;
   if (epi) {
 #pragma unroll
     for (int g = 0; g < G; ++g) red[g * 256 + threadIdx.x] = bsum[g];
-    if constexpr (G == 3) {
+    if (second) {
 #pragma unroll
       for (int g = 0; g < 3; ++g) red[(4 + g) * 256 + threadIdx.x] = bsumh[g];
     }
   }
   __syncthreads();
-  const int nsum = G == 4 ? 4 : 6;
+  const int nsum = G + (second ? 3 : 0);
   if ((int)threadIdx.x < nsum * 16) {
     const int g = threadIdx.x >> 4, u = threadIdx.x & 15;
-    const int slot = G == 3 && g >= 3 ? 4 + (g - 3) : g;
+    const bool hi = g >= G;  // a sum of the second set
+    const int slot = hi ? 4 + (g - G) : g;
     float v = 0.f;
     for (int row = 0; row < 16; ++row) v += red[slot * 256 + row * 16 + u];
-    const int gate = G == 3 && g >= 3 ? g - 3 : g;
-    float* dst = (G == 3 && g >= 3) ? U.bias_part_h : U.bias_part;
-    dst[(int64_t)rg * GH + gate * H + j0 + u] = v;
+    const int gate = hi ? g - G : g;
+    if (hi)
+      (G == 3 ? U.bias_part_h : U.peep_part)[(int64_t)rg * 3 * H + gate * H + j0 + u] = v;
+    else
+      U.bias_part[(int64_t)rg * GH + gate * H + j0 + u] = v;
   }
 }
 

@@ -118,12 +118,18 @@ __global__ __launch_bounds__(256) void k_step_fwd(StepFwdArgs a) {
   const float* gx = a.gx + f * GH;
   const bool has_prev = row < a.prev_rows;
   if constexpr (G == 4) {
-    const float ig = act_sigmoid(gx[j] + s[0]);
-    const float fg = act_sigmoid(gx[H + j] + s[1]);
-    const float gg = act_tanh(gx[2 * H + j] + s[2]);
-    const float og = act_sigmoid(gx[3 * H + j] + s[3]);
     const float cp = has_prev ? a.cst[(int64_t)(a.prev0 + row) * H + j] : 0.f;
+    float ai = gx[j] + s[0], af = gx[H + j] + s[1], ao = gx[3 * H + j] + s[3];
+    if (a.peep) {
+      ai += a.peep[j] * cp;
+      af += a.peep[H + j] * cp;
+    }
+    const float ig = act_sigmoid(ai);
+    const float fg = act_sigmoid(af);
+    const float gg = act_tanh(gx[2 * H + j] + s[2]);
     const float c = fg * cp + ig * gg;
+    if (a.peep) ao += a.peep[2 * H + j] * c;
+    const float og = act_sigmoid(ao);
     const float h = og * act_tanh(c);
     float* st = a.stash + f * 4 * H;
     st[j] = ig;
@@ -217,14 +223,28 @@ __global__ __launch_bounds__(256) void k_step_bwd(StepBwdArgs a) {
     const float ig = st[j], fg = st[H + j], gg = st[2 * H + j], og = st[3 * H + j];
     const float c = a.cst[f * H + j];
     const float tc = act_tanh(c);
-    const float dc = dh * og * (1.f - tc * tc) + (has_next ? *carry : 0.f);
+    const float dout = dh * tc * og * (1.f - og);
+    float dc = dh * og * (1.f - tc * tc) + (has_next ? *carry : 0.f);
+    if (a.peep) dc += dout * a.peep[2 * H + j];
     const float cp = has_prev ? a.cst[(int64_t)(a.prev0 + row) * H + j] : 0.f;
+    const float di = dc * gg * ig * (1.f - ig);
+    const float df = dc * cp * fg * (1.f - fg);
     float* da = a.da + f * GH;
-    da[j] = dc * gg * ig * (1.f - ig);
-    da[H + j] = dc * cp * fg * (1.f - fg);
+    da[j] = di;
+    da[H + j] = df;
     da[2 * H + j] = dc * ig * (1.f - gg * gg);
-    da[3 * H + j] = dh * tc * og * (1.f - og);
-    *carry = dc * fg;
+    da[3 * H + j] = dout;
+    float cr = dc * fg;
+    if (a.peep) {
+      // c_{t-1} also feeds the input and forget gates; this thread owns
+      // (row, j) at every step, so the running sums need no atomics.
+      cr += di * a.peep[j] + df * a.peep[H + j];
+      float* acc = a.peep_acc + (int64_t)row * 3 * H + j;
+      acc[0] += di * cp;
+      acc[H] += df * cp;
+      acc[2 * H] += dout * c;
+    }
+    *carry = cr;
   } else {
     const float dh = a.dh_in[f * a.ldd + j] + (has_next ? dh_rec + *carry : 0.f);
     const float r = st[j], z = st[H + j], n = st[2 * H + j], ahn = st[3 * H + j];

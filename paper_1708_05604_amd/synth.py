@@ -1,7 +1,7 @@
 """Seeded synthetic workloads standing in for the paper's handwriting data.
 
 The paper trains on a private online-handwriting corpus (Sec. IV.A) that is not
-available, so every input here is synthetic, with the shapes of the five
+available, so every input here is synthetic, with the shapes of the six
 workloads this library is measured on:
 
   tiny      1-layer LSTM, D=4,  H=32,  C=20, n=64,    lengths U[10,100],        B=16,  fp32
@@ -11,6 +11,7 @@ workloads this library is measured on:
   longtail  2-layer LSTM, D=16, H=512, C=100, n=8192, Pareto(1.5, x_m=50)[50,4000],
             B=128, bf16 GEMM operands
   gru2      2-layer GRU,  D=8,  H=384, C=80, n=16384, lognormal(300,0.6)[20,1500], B=96, fp32
+  lstm2p    lstm2 with the peephole LSTM cell
 
 This module is shared by the oracle and by the GPU path; it only draws random
 numbers and holds none of the method's arithmetic (no bucketing, no batching,
@@ -72,6 +73,8 @@ WORKLOADS = {
                          (1, 4, 16, 32), "pareto", (1.5, 50, 4000)),
     "gru2": Workload("gru2", GRU, 2, 0, 8, 384, 80, 16384, 96, FP32, (1, 8),
                      "lognormal", (300.0, 0.6, 20, 1500)),
+    "lstm2p": Workload("lstm2p", LSTM_PEEPHOLE, 2, 0, 8, 128, 80, 4096, 64, FP32, (1, 8),
+                       "lognormal", (300.0, 0.6, 20, 1500)),
 }
 
 

@@ -47,6 +47,12 @@ SHAPES = [
     ("equal-lengths", H.Spec(0, 1, 0, 4, 32, 8), [12] * 18),
     ("one-long", H.Spec(0, 2, 1, 4, 32, 8), [40, 1, 1, 1]),
     ("wide-classes", H.Spec(0, 1, 0, 16, 32, 1024), [5, 4]),
+    # peephole LSTM (cell 2): uni/bi, a two-layer stack in one launch, bf16
+    ("peep-h64-b37-ragged", H.Spec(2, 1, 0, 4, 64, 12), [31, 30, 30, 29]
+     + list(range(28, 0, -1)) + [1, 1, 1, 1, 1]),
+    ("peep-2l-bi", H.Spec(2, 2, 1, 8, 32, 8), [9, 7, 7, 3, 1]),
+    ("peep-bf16-2l", H.Spec(2, 2, 0, 8, 64, 16, synth.BF16), [20, 18, 11, 4, 4, 1]),
+    ("peep-one-long", H.Spec(2, 2, 0, 4, 32, 8), [40, 1, 1, 1]),
 ]
 
 
@@ -58,7 +64,9 @@ def test_shapes(label, spec, lengths):
 
 
 STEP_SHAPES = [s for s in SHAPES if s[0] in ("lstm-h64-b37-ragged", "lstm-2l-bi", "gru-bi",
-                                              "lstm-bf16-2l-bi", "gru-bf16", "one-long")]
+                                              "lstm-bf16-2l-bi", "gru-bf16", "one-long",
+                                              "peep-h64-b37-ragged", "peep-2l-bi",
+                                              "peep-bf16-2l")]
 
 
 @pytest.mark.parametrize("label,spec,lengths", STEP_SHAPES, ids=[s[0] for s in STEP_SHAPES])
@@ -274,7 +282,8 @@ def test_lstm2_bench_config_sampled():
         H.assert_batch_close(spec, data.params, data, order, label=f"lstm2 bucket {bucket}")
 
 
-@pytest.mark.parametrize("name,K", [("bilstm3", 16), ("longtail", 16), ("gru2", 8)])
+@pytest.mark.parametrize("name,K", [("bilstm3", 16), ("longtail", 16), ("gru2", 8),
+                                    ("lstm2p", 8)])
 def test_workload_sampled_first_bucket(name, K):
     spec, data, bof, batches = _workload_batches(name, K)
     order = _first_of_bucket(data, bof, batches, 0)

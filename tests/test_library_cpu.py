@@ -137,7 +137,7 @@ def test_validation_errors_before_launch():
         lib.param_count(bad)
     assert e.value.code == lib.EUNSUPPORTED
     with pytest.raises(lib.RnnbktError) as e:
-        lib.param_count(lib.ModelDesc.of(2, 1, 4, 32, 20, 0, 0))
+        lib.param_count(lib.ModelDesc.of(3, 1, 4, 32, 20, 0, 0))
     assert e.value.code == lib.EINVAL
     L = lib.load()
     import ctypes
