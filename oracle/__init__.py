@@ -17,6 +17,8 @@ Modules
              (Sec. III.B, step 4)
   ctc        the CTC loss of the paper's experiments (Sec. IV.A) and its
              gradient, log-space forward-backward over the blank-extended target
+  aggregate  the epoch-end mean of parallel replicas with decay (Sec. III.B,
+             eq. 3)
 
 Every function is written to be checked by eye against the paper or against
 textbook definitions, not to be fast.  Pins (brute force, closed forms, finite
