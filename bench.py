@@ -165,6 +165,70 @@ def timed(ep, state, warmup, steps, torch):
     return useful, a.elapsed_time(b) / 1e3
 
 
+class Replicated:
+    """R training replicas on R streams of the one GPU, the paper's parallel
+    scheme (Sec. III.B) with a portion of the epoch per replica: replica r
+    takes the epoch's batches r, r + R, ...; at the epoch end eq. 3 merges
+    them (rnnbkt_epoch_aggregate) and every replica continues from the
+    merged parameters."""
+
+    def __init__(self, R, desc, data, rb, wb, lr, optimizer, ctc_bytes, torch, dev):
+        self.torch = torch
+        P = len(data.params)
+        self.P = P
+        stride = (P + 3) // 4 * 4
+        self.reps = torch.zeros((R, stride), dtype=torch.float32, device=dev)
+        init = torch.from_numpy(data.params).to(dev)
+        for r in range(R):
+            self.reps[r, :P] = init
+        self.prev = init.clone()
+        self.states = []
+        for r in range(R):
+            g = torch.zeros(P, dtype=torch.float32, device=dev)
+            opt = None
+            if optimizer == "adadelta":
+                opt = (torch.zeros_like(g), torch.zeros_like(g))
+            cw = None if ctc_bytes is None else torch.empty(ctc_bytes, dtype=torch.uint8,
+                                                            device=dev)
+            self.states.append((desc, self.reps[r, :P], g,
+                                torch.empty(rb, dtype=torch.uint8, device=dev),
+                                torch.empty(wb, dtype=torch.uint8, device=dev),
+                                torch.zeros(1, dtype=torch.float32, device=dev), lr, opt, cw))
+        self.streams = [torch.cuda.Stream() for _ in range(R)]
+        torch.cuda.synchronize()
+
+    def run(self, ep, first, count):
+        useful = 0
+        nb = len(ep.batches)
+        R = len(self.streams)
+        for k in range(count):
+            with self.torch.cuda.stream(self.streams[k % R]):
+                useful += run_steps(ep, self.states[k % R], (first + k) % nb, 1, self.torch)
+        return useful
+
+    def merge(self):
+        cur = self.torch.cuda.current_stream()
+        for s in self.streams:
+            cur.wait_stream(s)
+        lib.epoch_aggregate(self.reps, self.prev, n=self.P)
+        for s in self.streams:
+            s.wait_stream(cur)
+
+
+def timed_replicated(ep, rep, warmup, steps, torch):
+    """One epoch portion per replica, concurrently, then the eq. 3 merge;
+    host clock around it with the device synchronised on both sides."""
+    rep.run(ep, 0, warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    useful = rep.run(ep, warmup, steps)
+    rep.merge()
+    torch.cuda.synchronize()
+    secs = time.perf_counter() - t0
+    lib.sync_check()
+    return useful, secs
+
+
 def cpu_baseline(w, data, ep, budget_s=15.0, targets=None):
     """The float64 oracle on the host: first batch of each bucket in turn
     until about `budget_s` seconds of work, BLAS pinned to one thread."""
@@ -214,6 +278,12 @@ def main(argv=None):
                     help="parameter update of each step (adadelta: rho 0.95, eps 1e-6)")
     ap.add_argument("--ordering", default="ascending", choices=list(lib.ORDERINGS),
                     help="feeding order of the buckets / batches (the paper's: ascending)")
+    ap.add_argument("--replicas", type=int, default=1,
+                    help="R > 1: the headline is R replicas training at once on R streams, "
+                         "each on its portion of the epoch, merged by eq. 3 (Sec. III.B)")
+    ap.add_argument("--extra-replicas", type=int, default=3, metavar="R",
+                    help="with --replicas 1, also measure R concurrent replicas and report "
+                         "them beside the headline (0 = skip)")
     ap.add_argument("--no-k1", action="store_true", help="skip the K=1 epoch")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle baseline")
     ap.add_argument("--no-timer", action="store_true", help="skip the per-kernel pass")
@@ -225,7 +295,8 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "the paper's multi-GPU map-reduce is outside this library.", file=sys.stderr)
+              "its parallel scheme runs as concurrent replicas on the one GPU (--replicas).",
+              file=sys.stderr)
         return 2
 
     import torch
@@ -271,7 +342,23 @@ def main(argv=None):
     nb = len(ep.batches)
     steps = args.steps or nb
     warmup = args.warmup
-    useful, secs = timed(ep, state, warmup, steps, torch)
+    ctc_bytes = None if ctc_ws is None else ctc_ws.numel()
+
+    def replicated(R, e, n_steps):
+        lib.set_concurrency(R)
+        try:
+            rep = Replicated(R, desc, data, rb, wb, args.lr, args.optimizer, ctc_bytes, torch,
+                             dev)
+            return timed_replicated(e, rep, warmup, n_steps, torch)
+        finally:
+            lib.set_concurrency(1)
+
+    def run_epoch(e, n_steps):
+        if args.replicas > 1:
+            return replicated(args.replicas, e, n_steps)
+        return timed(e, state, warmup, n_steps, torch)
+
+    useful, secs = run_epoch(ep, steps)
     value = useful / secs
     ms_per_step = secs * 1e3 / steps
     flops = flops_per_useful_step(w)
@@ -284,7 +371,10 @@ def main(argv=None):
         "config": {"workload": describe(w, K), "loss": args.loss, "optimizer": args.optimizer,
                    "ordering": args.ordering,
                    "batches_per_epoch": nb,
-                   "useful_timesteps_per_epoch": ep.U, "parallelism": "single GPU"},
+                   "useful_timesteps_per_epoch": ep.U,
+                   "parallelism": "single GPU" if args.replicas == 1 else
+                   f"{args.replicas} replicas on one GPU (concurrent streams, each a portion "
+                   "of the epoch, merged by eq. 3 at its end)"},
         "mfma_util_pct": 100.0 * flops * value / (peak * 1e12),
         "achieved_tflops": flops * value / 1e12,
         "pad_waste_pct": {"P_batch": 100.0 * (1 - ep.U / ep.p_batch),
@@ -294,11 +384,20 @@ def main(argv=None):
         "bucket_upper": [int(u) for u in ep.upper],
     }
     if ep1 is not None:
-        u1, s1 = timed(ep1, state, warmup, len(ep1.batches), torch)
+        u1, s1 = run_epoch(ep1, len(ep1.batches))
         out["k1"] = {"value": u1 / s1, "steps": len(ep1.batches),
                      "pad_waste_pct_P_batch": 100.0 * (1 - ep1.U / ep1.p_batch)}
         out["speedup_vs_k1"] = value / (u1 / s1)
 
+    if args.replicas == 1 and args.extra_replicas > 1:
+        Rx = args.extra_replicas
+        ux, sx = replicated(Rx, ep, steps)
+        out["replicas"] = {
+            "R": Rx, "value": ux / sx, "ms_per_epoch": sx * 1e3, "vs_sequential": ux / sx / value,
+            "note": (f"the same batches dealt to {Rx} replicas training at once on {Rx} streams "
+                     "(the paper's parallel scheme, Sec. III.B, on one GPU), merged by eq. 3 "
+                     "at the end; a different optimisation trajectory from the sequential "
+                     "headline")}
     if not args.no_timer:
         torch.cuda.synchronize()
         lib.kernel_timer(True)

@@ -206,6 +206,12 @@ int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_
  *   loss       device fp32[1] out: mean over the batch's valid frames of
  *              -log softmax(W_out h_top + b_out)[label]
  * The loss gradient w.r.t. the logits is computed here and kept in reserve.
+ * Recurrence kernels (this call and rnnbkt_lstm_bwd): all steps of a layer
+ * (or of a unidirectional stack) in one launch whose workgroups stay
+ * resident, when the grid fits (see rnnbkt_set_concurrency), else one
+ * launch per step.  Environment: RNNBKT_RECURRENCE=steps forces the
+ * per-step kernels; RNNBKT_LAUNCH=cooperative launches the resident grids
+ * through the runtime's cooperative launch (alone on the device).
  * Errors: EINVAL (null pointer, bad lengths, buffers too small),
  * EUNSUPPORTED (hidden % 32 != 0, input_dim % 4 != 0, num_classes % 4 != 0
  * or > 1024), EHIP.
@@ -293,6 +299,40 @@ int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,
 int32_t rnnbkt_adadelta_apply(float* params, const float* grads, float* acc_g2, float* acc_dx2,
                               int64_t n, float rho, float eps, float lr, void* stream);
 
+/* rnnbkt_epoch_aggregate -- the epoch-end step of the paper's parallel
+ * training (Sec. III.B, step 5, eq. 3 with alpha = 1): R replicas trained on
+ * separate portions of the epoch are merged into
+ *   V(t) = (1/R) sum_r V_r(t) - beta * V(t-1)
+ * and every replica starts the next epoch from V(t).  In place, for i < n:
+ *   replicas   device fp32; replica r's parameters at replicas + r*stride
+ *              (r = 0..R-1); in: V_r(t), out: V(t) in every replica
+ *   R          1..1024
+ *   stride     floats between replicas, >= n and a multiple of 4
+ *   prev       device fp32[n]; in: V(t-1) (the initial parameters for the
+ *              first epoch), out: V(t); must not overlap any replica's n values
+ *   beta       finite (1e-6 in the paper)
+ * The sum and the scaling run in double; each result is rounded to float
+ * once.  replicas and prev 16-byte aligned.  On one GPU the replicas are R
+ * concurrent training streams (rnnbkt_set_concurrency); across GPUs an
+ * all-reduce of the replicas would come first.
+ * Errors: RNNBKT_EINVAL (null pointer, R, n or stride out of range,
+ * misalignment, overlap, non-finite beta), before any launch. */
+int32_t rnnbkt_epoch_aggregate(float* replicas, int32_t R, int64_t stride, int64_t n,
+                               float* prev, float beta, void* stream);
+
+/* rnnbkt_set_concurrency -- declares how many streams may run this
+ * library's training calls at the same time in this process (default 1).
+ * The recurrence kernels keep all their workgroups resident for a whole
+ * batch (each waits for values other workgroups publish); with `streams`
+ * declared, each such launch claims at most 1/streams of the GPU's capacity
+ * for it, so the launches of all streams can be resident together.  A
+ * batch whose grid does not fit its share runs on the per-step kernels
+ * instead.  Running more streams than declared can make the waits of a
+ * launch time out: the results are then invalid and rnnbkt_sync_check
+ * reports it (no hang: every wait is bounded).  Set it while no call is in
+ * flight.  Errors: RNNBKT_EINVAL if streams is outside [1, 64]. */
+int32_t rnnbkt_set_concurrency(int32_t streams);
+
 /*
  * rnnbkt_top_hidden -- copies the top layer's per-frame output of the batch
  * held in `reserve` (after rnnbkt_lstm_fwd) into the padded layout
@@ -324,7 +364,7 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
 #define RNNBKT_KERNEL_STEP_BWD 1 /* recurrent step, backward through time */
 #define RNNBKT_KERNEL_GEMM 2     /* dense contractions incl. split-K folds */
 #define RNNBKT_KERNEL_XENT 3     /* output loss and its gradient (cross-entropy or CTC) */
-#define RNNBKT_KERNEL_SGD 4      /* parameter update (SGD or ADADELTA) */
+#define RNNBKT_KERNEL_SGD 4      /* parameter update (SGD, ADADELTA, eq. 3 aggregation) */
 #define RNNBKT_KERNEL_OTHER 5    /* batch tables, packing, column sums, loss sum */
 #define RNNBKT_KERNEL_KINDS 6
 

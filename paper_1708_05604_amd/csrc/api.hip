@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -997,6 +998,40 @@ extern "C" int32_t rnnbkt_adadelta_apply(float* params, const float* grads, floa
   hipStream_t st = static_cast<hipStream_t>(stream);
   Timed tm(RNNBKT_KERNEL_SGD, 0.0, 28.0 * n, st);
   RNNBKT_HIP(launch_adadelta(params, grads, acc_g2, acc_dx2, n, rho, eps, lr, st));
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_epoch_aggregate(float* replicas, int32_t R, int64_t stride, int64_t n,
+                                          float* prev, float beta, void* stream) {
+  clear_error();
+  RNNBKT_REQUIRE(replicas && prev, RNNBKT_EINVAL, "epoch_aggregate: null pointer");
+  RNNBKT_REQUIRE(R >= 1 && R <= 1024, RNNBKT_EINVAL, "epoch_aggregate: R = %d outside [1, 1024]",
+                 R);
+  RNNBKT_REQUIRE(n >= 0 && stride >= n && stride % 4 == 0, RNNBKT_EINVAL,
+                 "epoch_aggregate: need n >= 0 and stride >= n, a multiple of 4");
+  RNNBKT_REQUIRE(aligned16(replicas) && aligned16(prev), RNNBKT_EINVAL,
+                 "epoch_aggregate: replicas and prev must be 16-byte aligned");
+  RNNBKT_REQUIRE(std::isfinite(beta), RNNBKT_EINVAL, "epoch_aggregate: beta must be finite");
+  if (n == 0) return RNNBKT_OK;
+  // prev must not overlap any replica's n values.
+  const uintptr_t p0 = reinterpret_cast<uintptr_t>(prev), p1 = p0 + sizeof(float) * n;
+  for (int32_t r = 0; r < R; ++r) {
+    const uintptr_t r0 = reinterpret_cast<uintptr_t>(replicas + (int64_t)r * stride);
+    const uintptr_t r1 = r0 + sizeof(float) * n;
+    RNNBKT_REQUIRE(p1 <= r0 || r1 <= p0, RNNBKT_EINVAL,
+                   "epoch_aggregate: prev overlaps replica %d", r);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Timed tm(RNNBKT_KERNEL_SGD, 0.0, 8.0 * (R + 1) * n, st);
+  RNNBKT_HIP(launch_aggregate(replicas, R, stride, n, prev, beta, st));
+  return RNNBKT_OK;
+}
+
+extern "C" int32_t rnnbkt_set_concurrency(int32_t streams) {
+  clear_error();
+  RNNBKT_REQUIRE(streams >= 1 && streams <= 64, RNNBKT_EINVAL,
+                 "set_concurrency: streams = %d outside [1, 64]", streams);
+  set_concurrency(streams);
   return RNNBKT_OK;
 }
 

@@ -214,6 +214,43 @@ __global__ void k_adadelta(float* __restrict__ p, const float* __restrict__ g,
   }
 }
 
+// Eq. 3 over four consecutive parameters: the replica mean minus beta times
+// the previous aggregate, accumulated in double (the result is the exact
+// value rounded once to float), written back to every replica and to prev.
+__device__ inline float4 aggregate4(const float* reps, int R, int64_t stride, int64_t i4,
+                                    const float* prev, double beta) {
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  for (int r = 0; r < R; ++r) {
+    const float4 v = *reinterpret_cast<const float4*>(reps + r * stride + i4);
+    s0 += v.x;
+    s1 += v.y;
+    s2 += v.z;
+    s3 += v.w;
+  }
+  const float4 pv = *reinterpret_cast<const float4*>(prev + i4);
+  const double inv = 1.0 / R;
+  return make_float4((float)(s0 * inv - beta * pv.x), (float)(s1 * inv - beta * pv.y),
+                     (float)(s2 * inv - beta * pv.z), (float)(s3 * inv - beta * pv.w));
+}
+
+__global__ void k_aggregate(float* __restrict__ reps, int R, int64_t stride, int64_t n,
+                            float* __restrict__ prev, double beta) {
+  const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i4 + 3 < n) {
+    const float4 v = aggregate4(reps, R, stride, i4, prev, beta);
+    for (int r = 0; r < R; ++r) *reinterpret_cast<float4*>(reps + r * stride + i4) = v;
+    *reinterpret_cast<float4*>(prev + i4) = v;
+  } else {
+    for (int64_t i = i4; i < n; ++i) {
+      double s = 0.0;
+      for (int r = 0; r < R; ++r) s += reps[r * stride + i];
+      const float v = (float)(s * (1.0 / R) - beta * prev[i]);
+      for (int r = 0; r < R; ++r) reps[r * stride + i] = v;
+      prev[i] = v;
+    }
+  }
+}
+
 __global__ void k_fill_u32(unsigned* __restrict__ p, int64_t n, unsigned v) {
   const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i4 + 3 < n) {
@@ -310,6 +347,15 @@ hipError_t launch_adadelta(float* p, const float* g, float* eg2, float* edx2, in
   const int64_t quads = (n + 3) / 4;
   hipLaunchKernelGGL(k_adadelta, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads),
                      0, st, p, g, eg2, edx2, n, rho, eps, lr);
+  return hipGetLastError();
+}
+
+hipError_t launch_aggregate(float* reps, int R, int64_t stride, int64_t n, float* prev,
+                            float beta, hipStream_t st) {
+  const int threads = 256;
+  const int64_t quads = (n + 3) / 4;
+  hipLaunchKernelGGL(k_aggregate, dim3((unsigned)((quads + threads - 1) / threads)), dim3(threads),
+                     0, st, reps, R, stride, n, prev, (double)beta);
   return hipGetLastError();
 }
 

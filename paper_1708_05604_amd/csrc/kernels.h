@@ -127,6 +127,10 @@ hipError_t launch_store_ints(const int32_t* values, int n, int32_t* dst, hipStre
 // One ADADELTA step over n elements (p, eg2, edx2 updated in place).
 hipError_t launch_adadelta(float* p, const float* g, float* eg2, float* edx2, int64_t n,
                            float rho, float eps, float lr, hipStream_t st);
+// Eq. 3 in place: replicas r = 0..R-1 at reps + r*stride (16-byte aligned,
+// stride % 4 == 0) and prev all receive mean_r(reps) - beta * prev.
+hipError_t launch_aggregate(float* reps, int R, int64_t stride, int64_t n, float* prev,
+                            float beta, hipStream_t st);
 
 // ---------------------------------------------------------------- recurrent steps
 // One time step of one layer/direction over the active rows [0, rows) of the
@@ -257,6 +261,9 @@ int bwd_persistent_blocks(const BwdLaunch& a, int cell, bool bf16, int B);
 hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
                                  bool* fits);
 // Number of waits for published values that gave up (should stay 0).
+// Streams that may run persistent launches at once (each launch then claims
+// at most 1/streams of the GPU's co-resident capacity).
+void set_concurrency(int streams);
 hipError_t read_wait_timeouts(unsigned* count);
 constexpr unsigned kPublishSentinel = 0xFFFFFFFFu;
 

@@ -31,6 +31,8 @@
 // rnnbkt_sync_check) and later waits return at once, so a launch always ends.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
@@ -700,6 +702,9 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   }
 }
 
+// Streams that may run persistent launches at the same time (>= 1).
+std::atomic<int> g_concurrency{1};
+
 // Dynamic LDS above 64 KiB has to be allowed per kernel once.
 hipError_t allow_lds(const void* kernel, size_t shmem) {
   static std::mutex mu;
@@ -713,7 +718,9 @@ hipError_t allow_lds(const void* kernel, size_t shmem) {
   return e;
 }
 
-// Co-resident workgroups a launch of `kernel` can have (0 on error).
+// Co-resident workgroups a launch of `kernel` may claim (0 on error): the
+// GPU's capacity for it divided among the streams that may run persistent
+// launches at the same time.
 int max_coresident(const void* kernel, int threads, size_t shmem) {
   int dev = 0, cus = 0, per_cu = 0;
   if (allow_lds(kernel, shmem) != hipSuccess) return 0;
@@ -722,14 +729,20 @@ int max_coresident(const void* kernel, int threads, size_t shmem) {
     return 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, shmem) != hipSuccess)
     return 0;
-  return cus * per_cu;
+  return cus * per_cu / g_concurrency.load();
 }
 
-// Launches a grid that must be resident all at once.  By default the
-// runtime's cooperative launch guarantees it; RNNBKT_LAUNCH=plain uses an
-// ordinary launch instead (for tools that cannot follow cooperative
-// launches), relying on the occupancy check alone -- if another stream
-// occupied the GPU, waits would time out and rnnbkt_sync_check reports it.
+// Launches a grid that must be resident all at once.  By default an
+// ordinary launch: the grid fits in its share of the GPU (the check above),
+// so every workgroup is dispatched once the work already running drains --
+// kernels of other streams that do not wait on this one.  Several streams
+// may each run a persistent launch at once provided rnnbkt_set_concurrency
+// declared them (each then claims at most its share).  Waits stay bounded
+// either way: a launch whose grid could not all be resident ends with
+// timeouts that rnnbkt_sync_check reports.  RNNBKT_LAUNCH=cooperative uses
+// the runtime's cooperative launch instead, which guarantees residency by
+// running the grid alone on the device (measured about 25 us slower per
+// launch, and it serialises launches from different streams).
 hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem, void* args,
                        hipStream_t st, bool* fits) {
   if (blocks > max_coresident(kernel, threads, shmem)) {
@@ -739,9 +752,9 @@ hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem
   *fits = true;
   void* argv[] = {args};
   const char* mode = getenv("RNNBKT_LAUNCH");
-  if (mode && strcmp(mode, "plain") == 0)
-    return hipLaunchKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
-  return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
+  if (mode && strcmp(mode, "cooperative") == 0)
+    return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
+  return hipLaunchKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
 }
 
 }  // namespace
@@ -955,6 +968,8 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
   for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
   return coop_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
 }
+
+void set_concurrency(int streams) { g_concurrency.store(streams); }
 
 hipError_t read_wait_timeouts(unsigned* count) {
   return hipMemcpyFromSymbol(count, HIP_SYMBOL(g_wait_timeouts), sizeof(unsigned), 0,

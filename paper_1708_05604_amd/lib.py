@@ -87,6 +87,10 @@ _SIGNATURES = {
     "rnnbkt_lstm_bwd": (ctypes.c_int32, [_descp, _vp, _i32p, ctypes.c_int32, ctypes.c_int32,
                                          _vp, ctypes.c_size_t, _vp, ctypes.c_size_t, _vp, _vp]),
     "rnnbkt_sgd_apply": (ctypes.c_int32, [_vp, _vp, ctypes.c_int64, ctypes.c_float, _vp]),
+    "rnnbkt_epoch_aggregate": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                                ctypes.c_int64, ctypes.c_void_p, ctypes.c_float,
+                                                ctypes.c_void_p]),
+    "rnnbkt_set_concurrency": (ctypes.c_int32, [ctypes.c_int32]),
     "rnnbkt_adadelta_apply": (ctypes.c_int32, [_vp, _vp, _vp, _vp, ctypes.c_int64, ctypes.c_float,
                                                ctypes.c_float, ctypes.c_float, _vp]),
     "rnnbkt_top_hidden": (ctypes.c_int32, [_descp, _i32p, ctypes.c_int32, ctypes.c_int32, _vp,
@@ -324,6 +328,33 @@ def adadelta_apply(params, grads, acc_g2, acc_dx2, rho: float = 0.95, eps: float
     _check(load().rnnbkt_adadelta_apply(_dev(params, "float32"), _dev(grads, "float32"),
                                         _dev(acc_g2, "float32"), _dev(acc_dx2, "float32"), count,
                                         float(rho), float(eps), float(lr), _stream(stream)))
+
+
+def epoch_aggregate(replicas, prev, beta: float = 1e-6, stream=None, R: Optional[int] = None,
+                    stride: Optional[int] = None, n: Optional[int] = None):
+    """Eq. 3 in place: `replicas` is a [R, stride] float32 tensor (replica r in
+    row r; or an address with R, stride and n given), `prev` holds V(t-1);
+    both receive V(t) = mean over replicas - beta * prev."""
+    if isinstance(replicas, int):
+        if R is None or stride is None or n is None:
+            raise ValueError("an address needs R, stride and n")
+    else:
+        if replicas.dim() != 2:
+            raise ValueError("replicas must be a [R, stride] tensor")
+        R = replicas.shape[0] if R is None else R
+        stride = replicas.shape[1] if stride is None else stride
+        n = stride if n is None else n
+        if R > replicas.shape[0] or stride != replicas.shape[1] or n > stride:
+            raise ValueError("R, stride or n do not match the replicas tensor")
+    if not isinstance(prev, int) and prev.numel() < n:
+        raise ValueError("prev holds fewer than n values")
+    _check(load().rnnbkt_epoch_aggregate(_dev(replicas, "float32"), int(R), int(stride), int(n),
+                                         _dev(prev, "float32"), float(beta), _stream(stream)))
+
+
+def set_concurrency(streams: int):
+    """Declares how many streams may run training calls at once (default 1)."""
+    _check(load().rnnbkt_set_concurrency(int(streams)))
 
 
 def top_hidden(desc, lengths, reserve, out, stream=None):

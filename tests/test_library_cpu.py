@@ -213,3 +213,33 @@ def test_ordered_schedule_rejects_bad_input():
     a = lib.epoch_schedule(lengths, bof, 1, keys, 2, "descending")
     b = lib.epoch_schedule(lengths, bof, 1, keys, 2)
     assert [x.tolist() for x in a] == [x.tolist() for x in b]
+
+
+def test_epoch_aggregate_validation():
+    """Bad arguments are rejected before any launch (host addresses only)."""
+    L = lib.load()
+    base, prev = 1 << 20, 1 << 30
+
+    def call(reps=base, R=2, stride=8, n=8, pv=prev, beta=1e-6):
+        return L.rnnbkt_epoch_aggregate(reps, R, stride, n, pv, beta, None)
+
+    assert call(reps=None) == lib.EINVAL
+    assert call(pv=None) == lib.EINVAL
+    assert call(R=0) == lib.EINVAL
+    assert call(R=1025) == lib.EINVAL
+    assert call(n=-1) == lib.EINVAL
+    assert call(stride=6, n=6) == lib.EINVAL          # stride not a multiple of 4
+    assert call(stride=4, n=8) == lib.EINVAL          # stride < n
+    assert call(reps=base + 4) == lib.EINVAL          # misaligned
+    assert call(beta=float("nan")) == lib.EINVAL
+    assert call(pv=base + 4 * 8) == lib.EINVAL        # prev overlaps replica 1
+    assert call(pv=base + 4 * 4) == lib.EINVAL        # prev overlaps replica 0's tail
+    assert call(n=0) == lib.OK                        # nothing to do, nothing launched
+
+
+def test_set_concurrency_validation():
+    L = lib.load()
+    assert L.rnnbkt_set_concurrency(0) == lib.EINVAL
+    assert L.rnnbkt_set_concurrency(65) == lib.EINVAL
+    assert L.rnnbkt_set_concurrency(3) == lib.OK
+    assert L.rnnbkt_set_concurrency(1) == lib.OK
