@@ -131,6 +131,7 @@ struct Carve {
   size_t ws_fwd;
   // workspace (backward)
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
+  size_t splitk_out, colsum_out;  // output-layer gradients (run beside the recurrence)
   std::vector<size_t> da, dah;  // per layer*dirs
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
   std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
@@ -183,7 +184,11 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     const SplitK p = choose_splitk(M, Nn, K);
     if (p.S > 1) sk = std::max(sk, (size_t)p.S * M * Nn);
   };
-  need(s.C, s.Htop, N);
+  {
+    const SplitK p = choose_splitk(s.C, s.Htop, N);
+    c.splitk_out = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * s.C * s.Htop : 1));
+  }
+  c.colsum_out = take(sizeof(float) * kColsumSplits * s.C);
   for (int l = 0; l < s.L; ++l) {
     need(GH, s.din(l), N);
     need(GH, s.H, N);
@@ -280,6 +285,32 @@ class Timed {
   TimerRec rec_{};
   bool active_ = false;
 };
+
+// A side stream per caller stream, with the two events that fork work onto
+// it and join it back.  Created on first use and kept for the process.
+struct Side {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+std::vector<std::pair<hipStream_t, Side>> g_sides;
+
+hipError_t side_for(hipStream_t st, Side* out) {
+  std::lock_guard<std::mutex> lk(g_side_mu);
+  for (auto& e : g_sides)
+    if (e.first == st) {
+      *out = e.second;
+      return hipSuccess;
+    }
+  Side sd;
+  hipError_t e = hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.join, hipEventDisableTiming);
+  if (e != hipSuccess) return e;
+  g_sides.emplace_back(st, sd);
+  *out = sd;
+  return hipSuccess;
+}
 
 // Host copy of the batch tables (active rows per step and frame offsets).
 void host_tables(const int32_t* len, int T, int B, std::vector<int>& bs, std::vector<int>& off) {
@@ -736,15 +767,25 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   const bool gru = s.cell == RNNBKT_CELL_GRU;
 
   // Output layer: dH_top = dZ W_out, dW_out = dZ^T H_top, db_out = colsum dZ.
+  // dW_out and db_out need nothing the recurrence produces: they run on a
+  // side stream beside it (the resident recurrence grids leave most CUs
+  // idle), into buffers of their own, and are joined before the layer weight
+  // gradients.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
+  Side side;
+  RNNBKT_HIP(side_for(st, &side));
+  RNNBKT_HIP(hipEventRecord(side.fork, st));
+  RNNBKT_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
+  RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
+                  nullptr, 0, s.bf16, side.s, nullptr, at<float>(workspace, c.splitk_out)));
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
+    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
+                             grads + po.bout, side.s));
+  }
+  RNNBKT_HIP(hipEventRecord(side.join, side.s));
   RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dha, s.Htop, n, s.Htop, s.C,
                   nullptr, 0, s.bf16, st));
-  RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
-                  nullptr, 0, s.bf16, st, nullptr, sk));
-  {
-    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), cs, grads + po.bout, st));
-  }
 
   auto da_of = [&](int l, int d) { return at<float>(workspace, c.da[l * s.dirs + d]); };
   auto dah_of = [&](int l, int d) {
@@ -930,6 +971,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     }
   }
 
+  RNNBKT_HIP(hipStreamWaitEvent(st, side.join, 0));
   // Weight gradients of every layer, reduced over every valid frame.
   for (int l = 0; l < s.L; ++l) {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
