@@ -132,6 +132,7 @@ struct Carve {
   // workspace (backward)
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
   size_t splitk_out, colsum_out;  // output-layer gradients (run beside the recurrence)
+  size_t splitk_rec;              // recurrent weight gradients (run beside the input ones)
   std::vector<size_t> da, dah;  // per layer*dirs
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
   std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
@@ -189,6 +190,10 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     c.splitk_out = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * s.C * s.Htop : 1));
   }
   c.colsum_out = take(sizeof(float) * kColsumSplits * s.C);
+  {
+    const SplitK p = choose_splitk(GH, s.H, N);
+    c.splitk_rec = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * GH * s.H : 1));
+  }
   for (int l = 0; l < s.L; ++l) {
     need(GH, s.din(l), N);
     need(GH, s.H, N);
@@ -972,7 +977,13 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   }
 
   RNNBKT_HIP(hipStreamWaitEvent(st, side.join, 0));
-  // Weight gradients of every layer, reduced over every valid frame.
+  // Weight gradients of every layer, reduced over every valid frame.  The
+  // input and recurrent products of a layer read the same dA and are
+  // independent: the recurrent ones run on the side stream (own split-K
+  // buffer), overlapping the other stream's products and reductions.
+  RNNBKT_HIP(hipEventRecord(side.fork, st));
+  RNNBKT_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
+  float* sk_rec = at<float>(workspace, c.splitk_rec);
   for (int l = 0; l < s.L; ++l) {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
     const int din = s.din(l);
@@ -984,7 +995,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
                       nullptr, 0, s.bf16, st, nullptr, sk));
       RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
-                      s.H, GH, s.H, n, nullptr, 0, s.bf16, st, d == 0 ? pf : pr, sk));
+                      s.H, GH, s.H, n, nullptr, 0, s.bf16, side.s, d == 0 ? pf : pr, sk_rec));
       {
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
         if (persistent) {
@@ -1007,6 +1018,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       }
     }
   }
+  RNNBKT_HIP(hipEventRecord(side.join, side.s));
+  RNNBKT_HIP(hipStreamWaitEvent(st, side.join, 0));
   return RNNBKT_OK;
 }
 
