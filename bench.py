@@ -358,6 +358,12 @@ def main(argv=None):
             return replicated(args.replicas, e, n_steps)
         return timed(e, state, warmup, n_steps, torch)
 
+    # The replicated figure is taken first: its streams then get hardware
+    # queues of their own (the library's side stream, created by the first
+    # sequential call, would otherwise share one with a replica).
+    extra = None
+    if args.replicas == 1 and args.extra_replicas > 1:
+        extra = (args.extra_replicas,) + replicated(args.extra_replicas, ep, steps)
     useful, secs = run_epoch(ep, steps)
     value = useful / secs
     ms_per_step = secs * 1e3 / steps
@@ -389,9 +395,8 @@ def main(argv=None):
                      "pad_waste_pct_P_batch": 100.0 * (1 - ep1.U / ep1.p_batch)}
         out["speedup_vs_k1"] = value / (u1 / s1)
 
-    if args.replicas == 1 and args.extra_replicas > 1:
-        Rx = args.extra_replicas
-        ux, sx = replicated(Rx, ep, steps)
+    if extra is not None:
+        Rx, ux, sx = extra
         out["replicas"] = {
             "R": Rx, "value": ux / sx, "ms_per_epoch": sx * 1e3, "vs_sequential": ux / sx / value,
             "note": (f"the same batches dealt to {Rx} replicas training at once on {Rx} streams "

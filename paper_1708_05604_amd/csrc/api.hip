@@ -775,12 +775,24 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   // dW_out and db_out need nothing the recurrence produces: they run on a
   // side stream beside it (the resident recurrence grids leave most CUs
   // idle), into buffers of their own, and are joined before the layer weight
-  // gradients.
+  // gradients.  With several streams declared (rnnbkt_set_concurrency) the
+  // caller's streams already share the GPU and more queues would only
+  // contend: the side work then stays on the caller's stream.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
   Side side;
-  RNNBKT_HIP(side_for(st, &side));
-  RNNBKT_HIP(hipEventRecord(side.fork, st));
-  RNNBKT_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
+  const bool split = concurrency() == 1;
+  if (split)
+    RNNBKT_HIP(side_for(st, &side));
+  else
+    side.s = st;
+  auto fork = [&]() -> hipError_t {
+    if (!split) return hipSuccess;
+    const hipError_t e = hipEventRecord(side.fork, st);
+    return e != hipSuccess ? e : hipStreamWaitEvent(side.s, side.fork, 0);
+  };
+  auto mark_join = [&]() { return split ? hipEventRecord(side.join, side.s) : hipSuccess; };
+  auto wait_join = [&]() { return split ? hipStreamWaitEvent(st, side.join, 0) : hipSuccess; };
+  RNNBKT_HIP(fork());
   RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
                   nullptr, 0, s.bf16, side.s, nullptr, at<float>(workspace, c.splitk_out)));
   {
@@ -788,7 +800,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
                              grads + po.bout, side.s));
   }
-  RNNBKT_HIP(hipEventRecord(side.join, side.s));
+  RNNBKT_HIP(mark_join());
   RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dha, s.Htop, n, s.Htop, s.C,
                   nullptr, 0, s.bf16, st));
 
@@ -976,13 +988,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     }
   }
 
-  RNNBKT_HIP(hipStreamWaitEvent(st, side.join, 0));
+  RNNBKT_HIP(wait_join());
   // Weight gradients of every layer, reduced over every valid frame.  The
   // input and recurrent products of a layer read the same dA and are
   // independent: the recurrent ones run on the side stream (own split-K
   // buffer), overlapping the other stream's products and reductions.
-  RNNBKT_HIP(hipEventRecord(side.fork, st));
-  RNNBKT_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
+  RNNBKT_HIP(fork());
   float* sk_rec = at<float>(workspace, c.splitk_rec);
   for (int l = 0; l < s.L; ++l) {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
@@ -1018,8 +1029,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       }
     }
   }
-  RNNBKT_HIP(hipEventRecord(side.join, side.s));
-  RNNBKT_HIP(hipStreamWaitEvent(st, side.join, 0));
+  RNNBKT_HIP(mark_join());
+  RNNBKT_HIP(wait_join());
   return RNNBKT_OK;
 }
 

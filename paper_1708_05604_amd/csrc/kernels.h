@@ -264,6 +264,7 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
 // Streams that may run persistent launches at once (each launch then claims
 // at most 1/streams of the GPU's co-resident capacity).
 void set_concurrency(int streams);
+int concurrency();
 hipError_t read_wait_timeouts(unsigned* count);
 constexpr unsigned kPublishSentinel = 0xFFFFFFFFu;
 

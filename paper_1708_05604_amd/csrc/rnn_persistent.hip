@@ -970,6 +970,7 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
 }
 
 void set_concurrency(int streams) { g_concurrency.store(streams); }
+int concurrency() { return g_concurrency.load(); }
 
 hipError_t read_wait_timeouts(unsigned* count) {
   return hipMemcpyFromSymbol(count, HIP_SYMBOL(g_wait_timeouts), sizeof(unsigned), 0,
