@@ -191,12 +191,17 @@ constexpr unsigned kMaxPolls = 1u << 20;
 template <bool BF16, int MAXC>
 __device__ inline void settle_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
                                       int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC]) {
-  if (segment_clear(u) || waits_abandoned()) return;
+  if (segment_clear(u)) return;
   for (unsigned polls = 1;; ++polls) {
     __builtin_amdgcn_s_sleep(1);
     poll_fence();
     issue_segment<BF16, MAXC>(r, row_off, sl, klim, u);
     if (segment_clear(u)) return;
+    // The abandoned flag is a device-scope load: checking it only every
+    // 1024 polls keeps its round trip off the path of a wait that is about
+    // to succeed (checked at every wait's first miss, it cost a round trip
+    // per step).
+    if ((polls & 1023u) == 0 && waits_abandoned()) return;
     if (polls >= kMaxPolls) {
       report_timeout();
       return;
