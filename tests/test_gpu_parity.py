@@ -288,3 +288,22 @@ def test_workload_sampled_first_bucket(name, K):
     spec, data, bof, batches = _workload_batches(name, K)
     order = _first_of_bucket(data, bof, batches, 0)
     H.assert_batch_close(spec, data.params, data, order, label=f"{name} bucket 0")
+
+
+def test_sequence_longer_than_resident_limit():
+    """T_max above the 6144 steps whose batch tables the resident kernels keep
+    in LDS: the recurrences fall back to one launch per step."""
+    spec = H.Spec(0, 2, 0, 4, 32, 8)
+    data = H.data_from_lengths(spec, [6200, 6150, 17, 1], seed=21, scale=0.3)
+    order = H.batch_order(data, range(4))
+    H.assert_batch_close(spec, data.params, data, order, label="T=6200 per-step fallback")
+
+
+def test_wide_batch_many_row_groups():
+    """B = 256 (16 row groups of 16 rows) with ragged lengths down to 1."""
+    spec = H.Spec(0, 2, 0, 8, 64, 16)
+    rng = np.random.default_rng(31)
+    lengths = sorted(rng.integers(1, 41, 256).tolist(), reverse=True)
+    data = H.data_from_lengths(spec, lengths, seed=31, scale=0.3)
+    order = H.batch_order(data, range(256))
+    H.assert_batch_close(spec, data.params, data, order, label="B=256")
