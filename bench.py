@@ -152,17 +152,21 @@ def run_steps(ep, state, first, count, torch):
     return useful
 
 
-def timed(ep, state, warmup, steps, torch):
+def timed(ep, state, warmup, steps, torch, repeats=1):
+    """`repeats` runs of `steps` steps back to back after `warmup` untimed
+    ones, an event between runs (no host synchronisation inside).  Returns
+    (useful timesteps, seconds) of each run."""
     run_steps(ep, state, 0, warmup, torch)
     torch.cuda.synchronize()
-    a = torch.cuda.Event(enable_timing=True)
-    b = torch.cuda.Event(enable_timing=True)
-    a.record()
-    useful = run_steps(ep, state, warmup, steps, torch)
-    b.record()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(repeats + 1)]
+    ev[0].record()
+    useful = []
+    for i in range(repeats):
+        useful.append(run_steps(ep, state, warmup + i * steps, steps, torch))
+        ev[i + 1].record()
     torch.cuda.synchronize()
     lib.sync_check()
-    return useful, a.elapsed_time(b) / 1e3
+    return [(u, ev[i].elapsed_time(ev[i + 1]) / 1e3) for i, u in enumerate(useful)]
 
 
 class Replicated:
@@ -258,9 +262,18 @@ def cpu_baseline(w, data, ep, budget_s=15.0, targets=None):
             used.append(b)
             if t_total >= budget_s:
                 break
+    cpu = "unknown CPU"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": useful / t_total, "unit": "timesteps/s", "cores": 1, "kind": "oracle",
             "sample": (f"float64 oracle fwd+bwd+SGD on the first batch of buckets {used} "
-                       f"of epoch 0 ({useful} useful timesteps, {t_total:.1f} s, 1 thread)")}
+                       f"of epoch 0 ({useful} useful timesteps, {t_total:.1f} s, 1 thread "
+                       f"of {cpu})")}
 
 
 def main(argv=None):
@@ -268,6 +281,9 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=0, help="0 = one full epoch")
     ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--epochs", type=int, default=0,
+                    help="timed runs of --steps steps, back to back (0 = 3 with a full epoch, "
+                         "else 1); value = the median run's rate")
     ap.add_argument("--workload", default="lstm2", choices=list(synth.WORKLOADS))
     ap.add_argument("--K", type=int, default=0, help="buckets (0 = largest of the workload)")
     ap.add_argument("--lr", type=float, default=0.1, help="SGD step size")
@@ -353,10 +369,12 @@ def main(argv=None):
         finally:
             lib.set_concurrency(1)
 
-    def run_epoch(e, n_steps):
+    repeats = args.epochs or (3 if not args.steps else 1)
+
+    def run_epoch(e, n_steps, reps=1):
         if args.replicas > 1:
-            return replicated(args.replicas, e, n_steps)
-        return timed(e, state, warmup, n_steps, torch)
+            return [replicated(args.replicas, e, n_steps) for _ in range(reps)]
+        return timed(e, state, warmup, n_steps, torch, reps)
 
     # The replicated figure is taken first: its streams then get hardware
     # queues of their own (the library's side stream, created by the first
@@ -364,13 +382,17 @@ def main(argv=None):
     extra = None
     if args.replicas == 1 and args.extra_replicas > 1:
         extra = (args.extra_replicas,) + replicated(args.extra_replicas, ep, steps)
-    useful, secs = run_epoch(ep, steps)
-    value = useful / secs
-    ms_per_step = secs * 1e3 / steps
+    runs = run_epoch(ep, steps, repeats)
+    rates = sorted(u / t for u, t in runs)
+    secs = sum(t for _, t in runs)
+    value = rates[len(rates) // 2]
+    ms_per_step = secs * 1e3 / (steps * repeats)
     flops = flops_per_useful_step(w)
     peak = PEAK_TFLOPS[w.gemm_dtype]
     out = {
-        "metric": METRIC, "value": value, "unit": "timesteps/s", "n_gpus": 1, "steps": steps,
+        "metric": METRIC, "value": value, "unit": "timesteps/s", "n_gpus": 1,
+        "steps": steps * repeats, "value_min": rates[0], "value_max": rates[-1],
+        "timed_runs": repeats,
         "warmup": warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.gemm_dtype == synth.BF16 else "f32", "data": "synthetic",
@@ -390,7 +412,7 @@ def main(argv=None):
         "bucket_upper": [int(u) for u in ep.upper],
     }
     if ep1 is not None:
-        u1, s1 = run_epoch(ep1, len(ep1.batches))
+        ((u1, s1),) = run_epoch(ep1, len(ep1.batches))
         out["k1"] = {"value": u1 / s1, "steps": len(ep1.batches),
                      "pad_waste_pct_P_batch": 100.0 * (1 - ep1.U / ep1.p_batch)}
         out["speedup_vs_k1"] = value / (u1 / s1)
@@ -429,6 +451,12 @@ def main(argv=None):
         out["kernels"] = {k: {"ms": v["ms"], "launches": v["launches"],
                               "avg_us": 1e3 * v["ms"] / max(v["launches"], 1)}
                           for k, v in kinds.items()}
+        # Recurrence time per time step of the batches (the latency the
+        # resident kernels are bound by; all layers of a launch together).
+        t_sum = sum(int(ep.lens[(warmup + k) % nb][0]) for k in range(steps))
+        out["recurrence_us_per_timestep"] = {
+            "fwd": 1e3 * kinds["step_fwd"]["ms"] / t_sum,
+            "bwd": 1e3 * kinds["step_bwd"]["ms"] / t_sum}
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(w, data, ep, targets=targets)
     print(json.dumps(out), flush=True)
