@@ -176,7 +176,7 @@ hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_
 
 // ---------------------------------------------------------------- persistent recurrence
 // All T steps of a set of recurrences (the layers of a unidirectional stack,
-// or the two directions of one layer) in one cooperative launch.  Tables
+// or the two directions of one layer) in one resident launch.  Tables
 // bs/off are the device batch tables.  Every array published during the
 // launch (hout of each unit forward; LSTM dA, GRU dAh and, when read by a
 // unit below, GRU dAx backward) must hold the sentinel 0xFFFFFFFF in every

@@ -3,7 +3,7 @@
 // consuming the one below as it is published), or both directions of one
 // bidirectional layer.
 //
-// A launch keeps every workgroup resident (cooperative launch) and walks
+// A launch keeps every workgroup resident (its grid fits the GPU at once) and walks
 // the T steps of the batch itself.  Each workgroup owns a fixed block of 16
 // batch rows and a fixed slice of hidden units, so
 //   - its slice of W_hh stays in registers for the whole launch (each lane
