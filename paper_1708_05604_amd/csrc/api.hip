@@ -133,6 +133,7 @@ struct Carve {
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
   size_t splitk_out, colsum_out;  // output-layer gradients (run beside the recurrence)
   size_t splitk_rec;              // recurrent weight gradients (run beside the input ones)
+  size_t wgpart;                  // streamed weight gradients: partial tiles of every layer
   std::vector<size_t> da, dah;  // per layer*dirs
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
   std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
@@ -193,6 +194,12 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   {
     const SplitK p = choose_splitk(GH, s.H, N);
     c.splitk_rec = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * GH * s.H : 1));
+  }
+  {
+    size_t wg = 0;  // kWgRepsMax partial copies of dW_ih and dW_hh of every layer
+    if (s.dirs == 1 && s.cell == RNNBKT_CELL_LSTM && !s.bf16)
+      for (int l = 0; l < s.L; ++l) wg += (size_t)kWgRepsMax * GH * (s.din(l) + s.H);
+    c.wgpart = take(sizeof(float) * std::max<size_t>(wg, 1));
   }
   for (int l = 0; l < s.L; ++l) {
     need(GH, s.din(l), N);
@@ -295,7 +302,7 @@ class Timed {
 // it and join it back.  Created on first use and kept for the process.
 struct Side {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, mid = nullptr, join = nullptr;
 };
 std::mutex g_side_mu;
 std::vector<std::pair<hipStream_t, Side>> g_sides;
@@ -310,6 +317,7 @@ hipError_t side_for(hipStream_t st, Side* out) {
   Side sd;
   hipError_t e = hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.mid, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.join, hipEventDisableTiming);
   if (e != hipSuccess) return e;
   g_sides.emplace_back(st, sd);
@@ -800,7 +808,6 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
                              grads + po.bout, side.s));
   }
-  RNNBKT_HIP(mark_join());
   RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dha, s.Htop, n, s.Htop, s.C,
                   nullptr, 0, s.bf16, st));
 
@@ -876,6 +883,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       hi -= best;
     }
   }
+  // Weight gradients streamed beside the recurrence (k_wgrad_stream): fp32
+  // unidirectional LSTM stacks whose layers all run in one resident launch,
+  // with the side stream in use.  RNNBKT_WGRAD=after computes them after it.
+  const char* wg_env = getenv("RNNBKT_WGRAD");
+  bool streamw = persistent && split && !gru && s.dirs == 1 && !s.bf16 && groups.size() == 1 &&
+                 !(wg_env && strcmp(wg_env, "after") == 0);
 
   if (persistent) {
     float* dh_in = dha;  // gradient w.r.t. the output of the top layer of the next group
@@ -905,6 +918,62 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
           if (gru && u.publish_dax)
             RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(u.da), N * GH, kPublishSentinel,
                                        st));
+        }
+      }
+      if (streamw) {
+        // The weight gradients start on the side stream once the published
+        // buffers hold the sentinel; the grid leaves the recurrence enough
+        // CUs to be resident whatever order the two are dispatched in.
+        const int free_cus = cu_count() - bwd_persistent_blocks(Lc, s.cell, s.bf16, B);
+        WgStreamArgs wa{};
+        float* part = at<float>(workspace, c.wgpart);
+        for (int l = 0; l < s.L; ++l) {
+          const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
+          WgJob ji{}, jh{};
+          ji.A = jh.A = da_of(l, 0);
+          ji.a_bytes = jh.a_bytes = rec_bytes;
+          ji.lda = jh.lda = GH;
+          ji.M = jh.M = GH;
+          ji.B = xin;
+          ji.ldb = s.din(l);
+          ji.N = s.din(l);
+          jh.B = at<float>(reserve, c.hout[l]);
+          jh.ldb = s.H;
+          jh.gather = pf;
+          jh.N = s.H;
+          for (WgJob* j : {&ji, &jh}) {
+            j->tile_begin = wa.tiles;
+            wa.tiles += wg_tiles(j->M, j->N);
+            wa.job[wa.njobs++] = *j;
+          }
+        }
+        wa.reps = std::min(kWgRepsMax, free_cus / std::max(wa.tiles, 1));
+        if (wa.reps < 1) {
+          streamw = false;
+        } else {
+          for (int q = 0; q < wa.njobs; ++q) {
+            wa.job[q].partial = part;
+            part += (size_t)wa.reps * wa.job[q].M * wa.job[q].N;
+          }
+          wa.off = d_off;
+          wa.T = T;
+          wa.spc = kWgStepsPerChunk;
+          wa.nchunks = (T + kWgStepsPerChunk - 1) / kWgStepsPerChunk;
+          RNNBKT_HIP(hipEventRecord(side.mid, st));
+          RNNBKT_HIP(hipStreamWaitEvent(side.s, side.mid, 0));
+          double wfl = 0;
+          for (int l = 0; l < s.L; ++l) wfl += 2.0 * N * GH * (s.din(l) + s.H);
+          {
+            Timed tm(RNNBKT_KERNEL_GEMM, wfl, 0.0, side.s);
+            RNNBKT_HIP(launch_wgrad_stream(wa, side.s));
+          }
+          for (int q = 0; q < wa.njobs; ++q) {
+            const int l = q / 2;
+            float* out = grads + (q % 2 == 0 ? po.wih[l] : po.whh[l]);
+            Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
+            RNNBKT_HIP(launch_splitk_reduce(wa.job[q].partial, wa.reps, wa.job[q].M, wa.job[q].N,
+                                            out, wa.job[q].N, nullptr, 0, side.s));
+          }
         }
       }
       bool fits = false;
@@ -988,12 +1057,14 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     }
   }
 
+  RNNBKT_HIP(mark_join());
   RNNBKT_HIP(wait_join());
-  // Weight gradients of every layer, reduced over every valid frame.  The
-  // input and recurrent products of a layer read the same dA and are
-  // independent: the recurrent ones run on the side stream (own split-K
-  // buffer), overlapping the other stream's products and reductions.
-  RNNBKT_HIP(fork());
+  // Weight gradients of every layer, reduced over every valid frame (unless
+  // they were streamed beside the recurrence).  The input and recurrent
+  // products of a layer read the same dA and are independent: the recurrent
+  // ones run on the side stream (own split-K buffer), overlapping the other
+  // stream's products and reductions.
+  if (!streamw) RNNBKT_HIP(fork());
   float* sk_rec = at<float>(workspace, c.splitk_rec);
   for (int l = 0; l < s.L; ++l) {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
@@ -1003,10 +1074,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       const int ld = l * s.dirs + d;
       const float* dax = da_of(l, d);
       const float* dahh = gru ? dah_of(l, d) : dax;
-      RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
-                      nullptr, 0, s.bf16, st, nullptr, sk));
-      RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
-                      s.H, GH, s.H, n, nullptr, 0, s.bf16, side.s, d == 0 ? pf : pr, sk_rec));
+      if (!streamw) {
+        RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
+                        nullptr, 0, s.bf16, st, nullptr, sk));
+        RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
+                        s.H, GH, s.H, n, nullptr, 0, s.bf16, side.s, d == 0 ? pf : pr, sk_rec));
+      }
       {
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
         if (persistent) {
@@ -1029,8 +1102,10 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       }
     }
   }
-  RNNBKT_HIP(mark_join());
-  RNNBKT_HIP(wait_join());
+  if (!streamw) {
+    RNNBKT_HIP(mark_join());
+    RNNBKT_HIP(wait_join());
+  }
   return RNNBKT_OK;
 }
 

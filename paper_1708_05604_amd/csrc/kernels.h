@@ -260,6 +260,40 @@ hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStr
 int bwd_persistent_blocks(const BwdLaunch& a, int cell, bool bf16, int B);
 hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
                                  bool* fits);
+// Weight gradients streamed beside the backward recurrence (fp32 LSTM
+// stacks): C = A^T B summed over the valid frames, for every (A, B) job,
+// while the recurrence is still publishing A.  The frames are taken in
+// chunks of `spc` time steps from the last step down (the order the
+// recurrence finishes them); each workgroup owns one 64 x 64 output tile of
+// one job and accumulates every `reps`-th chunk in registers, waiting (with
+// device-scope polls of the sentinel) for the A rows it reads.  It writes
+// one partial tile; partial[r] of job j (r < reps) are then summed in order.
+constexpr int kWgJobs = 8;      // two per layer, up to kMaxUnits layers
+constexpr int kWgRepsMax = 8;   // workgroups per output tile, at most
+struct WgJob {
+  const float* A;          // published gate gradients [frames x lda] (LSTM dA)
+  uint32_t a_bytes;        // bytes of A's array (< 2^31 - 16)
+  int32_t lda;
+  const float* B;          // B rows: frame f reads row gather ? gather[f] : f (-1 = zeros)
+  int64_t ldb;
+  const int32_t* gather;
+  int32_t M, N;            // output M x N (M = columns of A used, N = columns of B)
+  int32_t tile_begin;      // first tile index of this job
+  float* partial;          // [reps][M][N]
+};
+struct WgStreamArgs {
+  WgJob job[kWgJobs];
+  int32_t njobs, tiles, reps;
+  const int32_t* off;      // device frame offsets per step [T+1]
+  int32_t T, spc, nchunks;
+};
+hipError_t launch_wgrad_stream(const WgStreamArgs& a, hipStream_t stream);
+constexpr int kWgStepsPerChunk = 16;
+// Compute units of the current device (0 on error).
+int cu_count();
+// Output tiles of one job (64 x 64).
+inline int32_t wg_tiles(int32_t M, int32_t N) { return ((M + 63) / 64) * ((N + 63) / 64); }
+
 // Number of waits for published values that gave up (should stay 0).
 // Streams that may run persistent launches at once (each launch then claims
 // at most 1/streams of the GPU's co-resident capacity).

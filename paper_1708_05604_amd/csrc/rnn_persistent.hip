@@ -710,6 +710,176 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
 // Streams that may run persistent launches at the same time (>= 1).
 std::atomic<int> g_concurrency{1};
 
+// ---------------------------------------------------------------- streamed weight gradients
+// C = A^T B over the frames of the batch, beside the backward recurrence that
+// publishes A (see WgStreamArgs).  The tile loop is the fp32 TN product of
+// the GEMM kernels: 32-frame K-tiles staged untransposed in LDS ([k][m] and
+// [k][n], rows padded by 16 floats), double buffered, fed to
+// v_mfma_f32_16x16x4_f32 with 4 waves of 32 x 32 each.  A's K-tile is read
+// with device-scope loads and re-read until no element holds the sentinel.
+constexpr int kWgBK = 32;
+constexpr int kWgLD = 64 + 16;
+
+__device__ inline void wg_load_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0, int clim,
+                                 int k0, int klim) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    const unsigned o = (k0 + k < klim && c0 + c < clim)
+                           ? 4u * (unsigned)((int64_t)(k0 + k) * lda + c0 + c)
+                           : kNoRow;
+    v[rep] = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, kDeviceScope);
+  }
+}
+
+__device__ inline bool wg_clear(const u4 (&v)[2]) {
+  bool ok = true;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ok &= v[rep][e] != kSentinel;
+  return ok;
+}
+
+// Re-reads this thread's part of an A K-tile until it is all published.
+__device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0,
+                                   int clim, int k0, int klim) {
+  if (wg_clear(v)) return;
+  for (unsigned polls = 1;; ++polls) {
+    __builtin_amdgcn_s_sleep(2);
+    poll_fence();
+    wg_load_a(v, r, lda, c0, clim, k0, klim);
+    if (wg_clear(v)) return;
+    if ((polls & 1023u) == 0 && waits_abandoned()) return;
+    if (polls >= kMaxPolls) {
+      __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+  }
+}
+
+__device__ inline void wg_load_b(f4 (&v)[2], const float* P, int64_t ld, const int32_t* gather,
+                                 int c0, int clim, int k0, int klim) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    f4 x = {0.f, 0.f, 0.f, 0.f};
+    if (k0 + k < klim && c0 + c < clim) {
+      int64_t row = k0 + k;
+      if (gather) row = gather[row];
+      if (row >= 0) x = *reinterpret_cast<const f4*>(P + row * ld + c0 + c);
+    }
+    v[rep] = x;
+  }
+}
+
+__device__ inline void wg_store(float* S, const f4 (&v)[2]) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    *reinterpret_cast<f4*>(S + k * kWgLD + c) = v[rep];
+  }
+}
+
+__device__ inline void wg_store(float* S, const u4 (&v)[2]) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    *reinterpret_cast<u4*>(S + k * kWgLD + c) = v[rep];
+  }
+}
+
+__device__ inline WgJob pick_job(const WgStreamArgs& a, int j) {
+  WgJob u = a.job[0];
+#pragma unroll
+  for (int q = 1; q < kWgJobs; ++q)
+    if (j == q) u = a.job[q];
+  return u;
+}
+
+__global__ __launch_bounds__(256) void k_wgrad_stream(WgStreamArgs a) {
+  __shared__ __attribute__((aligned(16))) float As[2][kWgBK * kWgLD];
+  __shared__ __attribute__((aligned(16))) float Bs[2][kWgBK * kWgLD];
+  const int tile = blockIdx.x % a.tiles;
+  const int rep = blockIdx.x / a.tiles;
+  int j = 0;
+  for (int q = 1; q < a.njobs; ++q)
+    if (tile >= a.job[q].tile_begin) j = q;
+  const WgJob J = pick_job(a, j);
+  const int lt = tile - J.tile_begin;
+  const int mtiles = (J.M + 63) / 64;
+  const int m0 = (lt % mtiles) * 64, n0 = (lt / mtiles) * 64;
+  const __amdgpu_buffer_rsrc_t ra = published_rsrc(J.A, J.a_bytes);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int lr = lane & 15, lq = lane >> 4;
+  f4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) acc[i][jj] = f4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c = rep; c < a.nchunks; c += a.reps) {
+    // chunk c: steps [t_lo, t_hi), the c-th group of spc steps from the end
+    const int t_hi = a.T - c * a.spc;
+    const int t_lo = t_hi - a.spc > 0 ? t_hi - a.spc : 0;
+    const int kbeg = a.off[t_lo], kend = a.off[t_hi];
+    u4 ua[2];
+    f4 rb[2];
+    wg_load_a(ua, ra, J.lda, m0, J.M, kbeg, kend);
+    wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, kbeg, kend);
+    int buf = 0;
+    for (int k0 = kbeg; k0 < kend; k0 += kWgBK) {
+      wg_settle_a(ua, ra, J.lda, m0, J.M, k0, kend);
+      wg_store(As[buf], ua);
+      wg_store(Bs[buf], rb);
+      __syncthreads();
+      if (k0 + kWgBK < kend) {
+        wg_load_a(ua, ra, J.lda, m0, J.M, k0 + kWgBK, kend);
+        wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, k0 + kWgBK, kend);
+      }
+      const float* a_s = As[buf];
+      const float* b_s = Bs[buf];
+#pragma unroll
+      for (int kk = 0; kk < kWgBK; kk += 4) {
+        const int kr = (kk + lq) * kWgLD;
+        float av[2], bv[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) av[i] = a_s[kr + wm + i * 16 + lr];
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) bv[jj] = b_s[kr + wn + jj * 16 + lr];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[jj], acc[i][jj], 0, 0, 0);
+      }
+      buf ^= 1;
+    }
+    __syncthreads();  // the next chunk's first K-tile reuses buffer 0
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int n = n0 + wn + jj * 16 + lr;
+      if (n >= J.N) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = m0 + wm + i * 16 + lq * 4 + q;
+        if (m < J.M) J.partial[((int64_t)rep * J.M + m) * J.N + n] = acc[i][jj][q];
+      }
+    }
+}
+
 // Dynamic LDS above 64 KiB has to be allowed per kernel once.
 hipError_t allow_lds(const void* kernel, size_t shmem) {
   static std::mutex mu;
@@ -972,6 +1142,20 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
   const int per_unit = a.slices * a.rgroups;
   for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
   return coop_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
+}
+
+int cu_count() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return 0;
+  return cus;
+}
+
+hipError_t launch_wgrad_stream(const WgStreamArgs& a, hipStream_t st) {
+  if (a.tiles <= 0 || a.reps <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_wgrad_stream, dim3(a.tiles * a.reps), dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 void set_concurrency(int streams) { g_concurrency.store(streams); }

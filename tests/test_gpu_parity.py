@@ -307,3 +307,22 @@ def test_wide_batch_many_row_groups():
     data = H.data_from_lengths(spec, lengths, seed=31, scale=0.3)
     order = H.batch_order(data, range(256))
     H.assert_batch_close(spec, data.params, data, order, label="B=256")
+
+
+@pytest.mark.parametrize("label,spec,lengths", [
+    ("stream-1l", H.Spec(0, 1, 0, 4, 64, 12), [31, 30, 30, 29] + list(range(28, 0, -1))),
+    ("stream-2l", H.Spec(0, 2, 0, 8, 32, 8), [70, 64, 40, 33, 17, 17, 3, 1]),
+    ("stream-peep-2l", H.Spec(2, 2, 0, 4, 32, 8), [50, 49, 20, 1]),
+])
+def test_streamed_weight_gradients(label, spec, lengths, monkeypatch):
+    """Weight gradients computed beside the backward recurrence (fp32 LSTM
+    stacks) match the oracle and the products computed after it (to
+    rounding: the frames are summed in another order)."""
+    data = H.data_from_lengths(spec, lengths, seed=41, scale=0.3)
+    order = H.batch_order(data, range(len(lengths)))
+    H.assert_batch_close(spec, data.params, data, order, label=label)
+    a = H.GpuBatch(spec, data.params, data, order).run()
+    monkeypatch.setenv("RNNBKT_WGRAD", "after")
+    b = H.GpuBatch(spec, data.params, data, order).run()
+    assert a[0] == b[0]
+    assert H.normwise_err(a[1], b[1]) < 1e-6

@@ -96,10 +96,16 @@ def test_concurrent_streams_match_sequential(name, K, nb):
     staged = [_stage(data, parts[r]) for r in range(2)]
     desc, seq = _buffers(spec, data, parts[0] + parts[1], 2)
     s0 = torch.cuda.current_stream()
-    for r in range(2):
-        _train(desc, seq[r], staged[r], 0.1, s0)
-    torch.cuda.synchronize()
-    lib.sync_check()
+    # Both runs with two streams declared, so both take the same kernels
+    # (with one stream the backward would also overlap work of its own).
+    lib.set_concurrency(2)
+    try:
+        for r in range(2):
+            _train(desc, seq[r], staged[r], 0.1, s0)
+        torch.cuda.synchronize()
+        lib.sync_check()
+    finally:
+        lib.set_concurrency(1)
     _, con = _buffers(spec, data, parts[0] + parts[1], 2)
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
     lib.set_concurrency(2)
