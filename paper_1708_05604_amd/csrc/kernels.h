@@ -288,7 +288,7 @@ struct WgStreamArgs {
   int32_t T, spc, nchunks;
 };
 hipError_t launch_wgrad_stream(const WgStreamArgs& a, hipStream_t stream);
-constexpr int kWgStepsPerChunk = 16;
+constexpr int kWgStepsPerChunk = 4;  // short chunks leave little after the recurrence ends
 // Compute units of the current device (0 on error).
 int cu_count();
 // Output tiles of one job (64 x 64).

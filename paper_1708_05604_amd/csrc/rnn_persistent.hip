@@ -748,7 +748,9 @@ __device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda
                                    int clim, int k0, int klim) {
   if (wg_clear(v)) return;
   for (unsigned polls = 1;; ++polls) {
-    __builtin_amdgcn_s_sleep(2);
+    // (not on the recurrence's path: polling gently leaves it the memory
+    // system; measured best of sleeps 2..64)
+    __builtin_amdgcn_s_sleep(32);
     poll_fence();
     wg_load_a(v, r, lda, c0, clim, k0, klim);
     if (wg_clear(v)) return;
