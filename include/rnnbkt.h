@@ -205,7 +205,13 @@ int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_
  *              rnnbkt_buffer_sizes(desc, T_max, B, sum(lengths))
  *   loss       device fp32[1] out: mean over the batch's valid frames of
  *              -log softmax(W_out h_top + b_out)[label]
- * The loss gradient w.r.t. the logits is computed here and kept in reserve.
+ * The loss gradient w.r.t. the logits, and its product with W_out (the
+ * gradient w.r.t. the top layer's output), are computed here and kept in
+ * reserve.  When the top layer runs in a resident launch (fp32, one stream
+ * declared), the output layer and loss run beside it on an internal stream,
+ * on rows of the top layer as they are published; the call still returns
+ * with all of its work ordered on `stream`.  RNNBKT_OUTPUT=after runs them
+ * after the recurrence instead.
  * Recurrence kernels (this call and rnnbkt_lstm_bwd): all steps of a layer
  * (or of a unidirectional stack) in one launch whose workgroups stay
  * resident, when the grid fits (see rnnbkt_set_concurrency), else one
@@ -250,7 +256,7 @@ int32_t rnnbkt_ctc_workspace_bytes(int32_t T_max, int32_t B, int32_t U_max, size
  *                   collapses to the target (repeats merged, blanks dropped)
  * Other arguments as in rnnbkt_lstm_fwd (no per-frame labels).  The loss
  * gradient w.r.t. the logits is kept in reserve, so rnnbkt_lstm_bwd follows
- * unchanged.  A target no path of its sequence's length can produce (equal
+ * unchanged (the output layer runs after the recurrence).  A target no path of its sequence's length can produce (equal
  * neighbours need a blank between them) gives an infinite loss and zero
  * gradient rows for that sequence.  Probabilities are renormalised every
  * frame in fp32; the per-sequence log-likelihood is summed in fp64.

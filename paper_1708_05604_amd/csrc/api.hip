@@ -123,6 +123,7 @@ int64_t colsum_rows(int64_t N) { return std::max<int64_t>(1, (N + kColsumSplits 
 struct Carve {
   // reserve
   size_t bs, off, xp, yp, prev_f, prev_r, dz;
+  size_t dhtop;                    // dH of the top layer's output, dZ W_out [N x Htop]
   std::vector<size_t> hout;        // per layer [N x dirs*H]
   std::vector<size_t> stash, cst;  // per layer*dirs
   size_t reserve;
@@ -158,6 +159,7 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   c.prev_f = take(sizeof(int32_t) * N);
   c.prev_r = take(sizeof(int32_t) * N);
   c.dz = take(sizeof(float) * N * s.C);
+  c.dhtop = take(sizeof(float) * N * s.Htop);
   for (int l = 0; l < s.L; ++l) c.hout.push_back(take(sizeof(float) * N * s.dirs * s.H));
   for (int l = 0; l < s.L; ++l)
     for (int d = 0; d < s.dirs; ++d) {
@@ -580,6 +582,17 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     }
     return best;
   };
+  // Output layer and loss run by extra workgroups of the launch that holds
+  // the top layer, on its rows as they are published: fp32 with per-frame
+  // labels, W_out plus a block of rows within a workgroup's LDS, and the
+  // grid still resident with them.  RNNBKT_OUTPUT=after runs them after the
+  // recurrence as separate kernels.
+  const char* out_env = getenv("RNNBKT_OUTPUT");
+  const bool stream_out_ok = !ctc && !s.bf16 && output_stream_lds(s.C, s.Htop) > 0 &&
+                             hout_bytes < 0x7FFFFFF0u &&
+                             !(out_env && strcmp(out_env, "after") == 0);
+  const int nblk = (int)((N + kOutRows - 1) / kOutRows);
+  bool streamed_out = false;
   std::vector<char> layer_done(s.L, 0);
   if (use_persistent()) {
     int l = 0;
@@ -604,8 +617,27 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
             RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l + q])),
                                        N * ldh, kPublishSentinel, st));
         }
+        if (l + n == s.L && stream_out_ok) {
+          OutStreamArgs& oa = L.out;
+          oa.h = at<float>(reserve, c.hout[s.L - 1]);
+          oa.h_bytes = (uint32_t)hout_bytes;
+          oa.Htop = s.Htop;
+          oa.C = s.C;
+          oa.W = params + po.wout;
+          oa.bias = params + po.bout;
+          oa.y = Yp;
+          oa.N = N;
+          oa.inv_n = 1.0f / (float)N;
+          oa.dz = dz;
+          oa.dh = at<float>(reserve, c.dhtop);
+          oa.partial = lp;
+          oa.nblocks = nblk;
+          L.out_blocks = std::min(kOutStreamGrid, nblk);
+          if (fwd_persistent_blocks(L, s.cell, s.bf16, B) == 0) L.out_blocks = 0;
+        }
         Timed tm(RNNBKT_KERNEL_STEP_FWD, fl, 0.0, st);
         RNNBKT_HIP(launch_fwd_persistent(L, s.cell, s.bf16, B, st, &fits));
+        streamed_out = fits && L.out_blocks > 0;
       }
       if (!fits) break;  // this layer and the ones above take the per-step kernels
       for (int q = 0; q < n; ++q) layer_done[l + q] = 1;
@@ -652,8 +684,14 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       }
     }
   }
-  // Output layer and loss.
+  if (streamed_out) {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    RNNBKT_HIP(launch_sum(lp, nblk, 1.0f / (float)N, loss, st));
+    return RNNBKT_OK;
+  }
+  // Output layer and loss, then dH of the top layer for the backward.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
+  float* dhtop = at<float>(reserve, c.dhtop);
   RNNBKT_HIP(gemm(top, s.Htop, true, params + po.wout, s.Htop, true, dz, s.C, (int)N, s.C,
                   s.Htop, params + po.bout, 0, s.bf16, st));
   if (ctc) {
@@ -685,8 +723,12 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       Timed tm(RNNBKT_KERNEL_XENT, 0.0, (8.0 * s.C + 4.0) * N, st);
       RNNBKT_HIP(launch_ctc(a, st));
     }
-    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-    RNNBKT_HIP(launch_sum(a.loss_part, B, 1.0f / (float)B, loss, st));
+    {
+      Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+      RNNBKT_HIP(launch_sum(a.loss_part, B, 1.0f / (float)B, loss, st));
+    }
+    RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dhtop, s.Htop, (int)N,
+                    s.Htop, s.C, nullptr, 0, s.bf16, st));
     return RNNBKT_OK;
   }
   int32_t nparts = 0;
@@ -698,6 +740,8 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
     RNNBKT_HIP(launch_sum(lp, nparts, 1.0f / (float)N, loss, st));
   }
+  RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dhtop, s.Htop, (int)N, s.Htop,
+                  s.C, nullptr, 0, s.bf16, st));
   return RNNBKT_OK;
 }
 
@@ -779,7 +823,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   const int n = (int)N;
   const bool gru = s.cell == RNNBKT_CELL_GRU;
 
-  // Output layer: dH_top = dZ W_out, dW_out = dZ^T H_top, db_out = colsum dZ.
+  // Output layer: dW_out = dZ^T H_top, db_out = colsum dZ (dH_top = dZ W_out
+  // was left in the reserve by the forward).
   // dW_out and db_out need nothing the recurrence produces: they run on a
   // side stream beside it (the resident recurrence grids leave most CUs
   // idle), into buffers of their own, and are joined before the layer weight
@@ -808,8 +853,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
                              grads + po.bout, side.s));
   }
-  RNNBKT_HIP(gemm(dz, s.C, true, params + po.wout, s.Htop, false, dha, s.Htop, n, s.Htop, s.C,
-                  nullptr, 0, s.bf16, st));
+  const float* dhtop = at<float>(reserve, c.dhtop);
 
   auto da_of = [&](int l, int d) { return at<float>(workspace, c.da[l * s.dirs + d]); };
   auto dah_of = [&](int l, int d) {
@@ -891,8 +935,11 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                  !(wg_env && strcmp(wg_env, "after") == 0);
 
   if (persistent) {
-    float* dh_in = dha;  // gradient w.r.t. the output of the top layer of the next group
-    float* dx = dhb;
+    // Gradient w.r.t. the output of the top layer of the next group; the
+    // dX GEMMs of bidirectional layers alternate between dha and dhb.
+    const float* dh_in = dhtop;
+    float* dx = dha;
+    float* spare = dhb;
     for (const Group& g : groups) {
       BwdLaunch Lc = base_launch();
       for (int q = 0; q < g.n; ++q) {
@@ -990,13 +1037,15 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
           RNNBKT_HIP(gemm(da_of(lo, d), GH, true, params + po.wih[ld], s.din(lo), false, dx,
                           s.din(lo), n, s.din(lo), GH, nullptr, d > 0 ? 1 : 0, s.bf16, st));
         }
-        std::swap(dh_in, dx);
+        dh_in = dx;
+        std::swap(dx, spare);
       }
     }
   } else {
     // One launch per time step: each layer needs the full gradient from above.
-    float* dh_in = dha;
-    float* dx = dhb;
+    const float* dh_in = dhtop;
+    float* dx = dha;
+    float* spare = dhb;
     for (int l = s.L - 1; l >= 0; --l) {
       const float* hout = at<float>(reserve, c.hout[l]);
       for (int d = 0; d < s.dirs; ++d) {
@@ -1052,7 +1101,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
           RNNBKT_HIP(gemm(da_of(l, d), GH, true, params + po.wih[ld], s.din(l), false, dx,
                           s.din(l), n, s.din(l), GH, nullptr, d > 0 ? 1 : 0, s.bf16, st));
         }
-        std::swap(dh_in, dx);
+        dh_in = dx;
+        std::swap(dx, spare);
       }
     }
   }

@@ -206,6 +206,34 @@ struct FwdUnit {
   int32_t wg_begin;      // first workgroup of this unit
 };
 
+// Output layer run by extra workgroups of the forward launch that holds the
+// top layer (fp32, per-frame loss): blocks of kOutRows frames in time order,
+// each waiting (device-scope polls of the sentinel) for its rows of the top
+// layer's published output, then logits = h W_out^T + b_out, softmax
+// cross-entropy against the frame's label (loss terms summed per block into
+// partial[block]), dlogits = (softmax - onehot) * inv_n into dz, and dh =
+// dlogits W_out.  W_out is staged in LDS once per workgroup; usable when
+// output_stream_lds(C, Htop) is nonzero.
+constexpr int kOutRows = 32;
+struct OutStreamArgs {
+  const float* h;    // top layer output [N x Htop], published by the launch
+  uint32_t h_bytes;  // bytes of h's array (< 2^31 - 16)
+  int32_t Htop, C;
+  const float* W;    // W_out [C x Htop]
+  const float* bias; // b_out [C]
+  const int32_t* y;  // packed labels [N]
+  int64_t N;
+  float inv_n;
+  float* dz;         // [N x C]
+  float* dh;         // [N x Htop]
+  float* partial;    // [nblocks]
+  int32_t nblocks;
+};
+// Output-layer workgroups of a launch at most.
+constexpr int kOutStreamGrid = 32;
+// Dynamic LDS of an output-layer workgroup (0: shape not supported).
+size_t output_stream_lds(int32_t C, int32_t Htop);
+
 struct FwdLaunch {
   FwdUnit u[kMaxUnits];
   int32_t nunits;
@@ -213,6 +241,10 @@ struct FwdLaunch {
   const int32_t* off;
   int32_t H, ldh, T;
   int32_t slices, rgroups;  // set by the launcher
+  // fp32 only: out_blocks > 0 adds that many output-layer workgroups after
+  // the recurrence ones, reading the last unit's published output.
+  OutStreamArgs out;
+  int32_t out_blocks;
 };
 
 // One (layer, direction) recurrence inside a backward launch.  The
@@ -293,6 +325,7 @@ constexpr int kWgStepsPerChunk = 4;  // short chunks leave little after the recu
 int cu_count();
 // Output tiles of one job (64 x 64).
 inline int32_t wg_tiles(int32_t M, int32_t N) { return ((M + 63) / 64) * ((N + 63) / 64); }
+
 
 // Number of waits for published values that gave up (should stay 0).
 // Streams that may run persistent launches at once (each launch then claims

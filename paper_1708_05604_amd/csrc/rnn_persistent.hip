@@ -266,10 +266,131 @@ __device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
 // share an XCD keeps each unit's row groups, which exchange values every
 // step, on one XCD.
 constexpr int kXcds = 8;
-__device__ inline int logical_block() {
-  const int b = blockIdx.x, n = gridDim.x;
+__device__ inline int logical_block(int n) {
+  const int b = blockIdx.x;
   if (n % kXcds != 0) return b;
   return (b % kXcds) * (n / kXcds) + b / kXcds;
+}
+
+// ---------------------------------------------------------------- output layer
+// See OutStreamArgs.  One 256-thread workgroup takes blocks first, first +
+// stride, ...  LDS: W_out [C][Htop + 1] (the +1 keeps the 16 rows a fragment
+// reads in different banks), the block's h rows [kOutRows][Htop + 1], its
+// logits / dlogits [kOutRows][C + 1], 4 wave sums.  Products on
+// v_mfma_f32_16x16x4_f32 as in the recurrence.
+constexpr int kOutGroup = 256 / kOutRows;  // threads per row in the softmax
+constexpr size_t kOutLdsMax = 96 * 1024;
+
+__device__ inline float out_group_max(float v) {
+#pragma unroll
+  for (int o = kOutGroup / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kOutGroup));
+  return v;
+}
+__device__ inline float out_group_sum(float v) {
+#pragma unroll
+  for (int o = kOutGroup / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kOutGroup);
+  return v;
+}
+
+__device__ void output_consumer(const OutStreamArgs& a, int first, int stride, char* out_smem) {
+  const int Htop = a.Htop, C = a.C;
+  const int WL = Htop + 1, ZL = C + 1;
+  float* Ws = reinterpret_cast<float*>(out_smem);  // [C][WL]
+  float* Hs = Ws + (size_t)C * WL;                 // [kOutRows][WL]
+  float* Zs = Hs + (size_t)kOutRows * WL;          // [kOutRows][ZL]
+  float* wsum = Zs + (size_t)kOutRows * ZL;        // [4]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lq = lane >> 4;
+  for (int i = tid; i < C * Htop; i += 256) Ws[(i / Htop) * WL + i % Htop] = a.W[i];
+  const __amdgpu_buffer_rsrc_t rh = published_rsrc(a.h, a.h_bytes);
+  constexpr int RT = kOutRows / 16;
+  const int ctiles = (C + 15) / 16, htiles = Htop / 16;
+  for (int blk = first; blk < a.nblocks; blk += stride) {
+    const int64_t f0 = (int64_t)blk * kOutRows;
+    // this block's h rows, re-read until published
+    for (int i = tid; i < kOutRows * Htop / 4; i += 256) {
+      const int r = (4 * i) / Htop, k = (4 * i) % Htop;
+      const unsigned o =
+          f0 + r < a.N ? 4u * (unsigned)((f0 + r) * Htop + k) : kNoRow;
+      u4 v = __builtin_amdgcn_raw_buffer_load_b128(rh, o, 0, kDeviceScope);
+      for (unsigned polls = 1; v[0] == kSentinel || v[1] == kSentinel || v[2] == kSentinel ||
+                               v[3] == kSentinel;
+           ++polls) {
+        __builtin_amdgcn_s_sleep(32);
+        poll_fence();
+        v = __builtin_amdgcn_raw_buffer_load_b128(rh, o, 0, kDeviceScope);
+        if ((polls & 1023u) == 0 && waits_abandoned()) break;
+        if (polls >= kMaxPolls) {
+          __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Hs[r * WL + k + e] = __uint_as_float(v[e]);
+    }
+    __syncthreads();
+    for (int t = wave; t < RT * ctiles; t += 4) {
+      const int r0 = (t % RT) * 16, c0 = (t / RT) * 16;
+      const int c = c0 + lr;
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < Htop; k += 4) {
+        const float av = Hs[(r0 + lr) * WL + k + lq];
+        const float bv = c < C ? Ws[c * WL + k + lq] : 0.f;
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+      }
+      if (c < C) {
+        const float b = a.bias[c];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Zs[(r0 + lq * 4 + q) * ZL + c] = acc[q] + b;
+      }
+    }
+    __syncthreads();
+    {
+      const int r = tid / kOutGroup, g = tid % kOutGroup;
+      const int64_t f = f0 + r;
+      float* zr = Zs + r * ZL;
+      float m = -INFINITY;
+      for (int c = g; c < C; c += kOutGroup) m = fmaxf(m, zr[c]);
+      m = out_group_max(m);
+      float sacc = 0.f;
+      for (int c = g; c < C; c += kOutGroup) sacc += expf(zr[c] - m);
+      sacc = out_group_sum(sacc);
+      const float lse = m + logf(sacc);
+      const int label = f < a.N ? a.y[f] : -1;
+      float zy = 0.f;
+      for (int c = g; c < C; c += kOutGroup) {
+        if (c == label) zy = zr[c];
+        const float d = (expf(zr[c] - lse) - (c == label ? 1.f : 0.f)) * a.inv_n;
+        zr[c] = f < a.N ? d : 0.f;
+        if (f < a.N) a.dz[f * C + c] = d;
+      }
+      zy = out_group_sum(zy);
+      float term = 0.f;
+      if (g == 0 && f < a.N) term = (label >= 0 && label < C) ? lse - zy : NAN;
+      // block sum of the row terms, fixed order: butterfly in a wave, then waves
+      for (int o = 32; o > 0; o >>= 1) term += __shfl_xor(term, o, 64);
+      if (lane == 0) wsum[wave] = term;
+    }
+    __syncthreads();
+    if (tid == 0) a.partial[blk] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+    for (int t = wave; t < RT * htiles; t += 4) {
+      const int r0 = (t % RT) * 16, h0 = (t / RT) * 16;
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < C; k += 4) {
+        const float av = Zs[(r0 + lr) * ZL + k + lq];
+        const float bv = Ws[(k + lq) * WL + h0 + lr];
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t f = f0 + r0 + lq * 4 + q;
+        if (f < a.N) a.dh[f * Htop + h0 + lr] = acc[q];
+      }
+    }
+    __syncthreads();  // Hs, Zs and wsum are rewritten for the next block
+  }
 }
 
 // Copies the batch tables into LDS.
@@ -295,8 +416,17 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   float* red = reinterpret_cast<float*>(smem);                     // [NW][NT][256]
   int32_t* tbs = reinterpret_cast<int32_t*>(red + NW * NT * 256);  // batch sizes [T]
   int32_t* toff = tbs + a.T;                                       // offsets [T+1]
+  // Output-layer workgroups follow the recurrence ones (physical ids, so the
+  // renumbering below is that of the recurrence grid alone).
+  const int rec_blocks = gridDim.x - a.out_blocks;
+  if constexpr (!BF16) {
+    if ((int)blockIdx.x >= rec_blocks) {
+      output_consumer(a.out, blockIdx.x - rec_blocks, a.out_blocks, smem);
+      return;
+    }
+  }
   load_tables(a.bs, a.off, a.T, tbs, toff);
-  const int bid = logical_block();
+  const int bid = logical_block(rec_blocks);
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
     if (bid >= a.u[q].wg_begin) ui = q;
@@ -500,7 +630,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   int32_t* tbs = reinterpret_cast<int32_t*>(red + (NW < 8 ? 8 : NW) * 256);
   int32_t* toff = tbs + a.T;
   load_tables(a.bs, a.off, a.T, tbs, toff);
-  const int bid = logical_block();
+  const int bid = logical_block(gridDim.x);
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
     if (bid >= a.u[q].wg_begin) ui = q;
@@ -991,6 +1121,12 @@ FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
   if (p.maxc == 0) return p;
   p.blocks = a.nunits * (a.H / (4 * p.nt)) * ((B + 15) / 16);
   p.shmem = sizeof(float) * 4 * p.nt * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  if (a.out_blocks > 0) {
+    const size_t out_lds = output_stream_lds(a.out.C, a.out.Htop);
+    if (bf16 || out_lds == 0) return p;
+    p.blocks += a.out_blocks;
+    p.shmem = std::max(p.shmem, out_lds);
+  }
   p.kernel = fwd_kernel(cell, bf16, p.nt, p.maxc);
   return p;
 }
@@ -1144,6 +1280,13 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
   const int per_unit = a.slices * a.rgroups;
   for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
   return coop_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
+}
+
+size_t output_stream_lds(int32_t C, int32_t Htop) {
+  if (C % 4 != 0 || Htop % 16 != 0) return 0;
+  const size_t b =
+      sizeof(float) * ((size_t)(C + kOutRows) * (Htop + 1) + (size_t)kOutRows * (C + 1) + 4);
+  return b <= kOutLdsMax ? b : 0;
 }
 
 int cu_count() {

@@ -326,3 +326,28 @@ def test_streamed_weight_gradients(label, spec, lengths, monkeypatch):
     b = H.GpuBatch(spec, data.params, data, order).run()
     assert a[0] == b[0]
     assert H.normwise_err(a[1], b[1]) < 1e-6
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("label,spec,lengths", [
+    ("out-1l-c12", H.Spec(0, 1, 0, 4, 64, 12), [31, 30, 30, 29] + list(range(28, 0, -1))),
+    ("out-2l-tiny", H.Spec(0, 2, 0, 8, 32, 8), [9, 5, 3, 1]),
+    ("out-2l-many-blocks", H.Spec(0, 2, 0, 8, 64, 20),
+     [int(v) for v in np.linspace(140, 3, 48)]),
+    ("out-peep-2l", H.Spec(2, 2, 0, 4, 32, 8), [50, 49, 20, 1]),
+    ("out-bi-2l", H.Spec(0, 2, 1, 4, 32, 16), [37, 36, 18, 2]),
+    ("out-gru-2l", H.Spec(1, 2, 0, 4, 32, 8), [44, 30, 29, 5]),
+])
+def test_streamed_output_layer(label, spec, lengths, monkeypatch):
+    """The output layer and loss computed beside the forward recurrence
+    (k_output_stream, blocks of 32 frames, grid-stride over more blocks than
+    workgroups) match the oracle and the separate kernels run after it (to
+    rounding: logits and loss are summed in another order)."""
+    data = H.data_from_lengths(spec, lengths, seed=43, scale=0.3)
+    order = H.batch_order(data, range(len(lengths)))
+    H.assert_batch_close(spec, data.params, data, order, label=label)
+    a = H.GpuBatch(spec, data.params, data, order).run()
+    monkeypatch.setenv("RNNBKT_OUTPUT", "after")
+    b = H.GpuBatch(spec, data.params, data, order).run()
+    assert abs(a[0] - b[0]) <= 1e-6 * abs(b[0])
+    assert H.normwise_err(a[1], b[1]) < 1e-5
