@@ -372,7 +372,10 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
 #define RNNBKT_KERNEL_XENT 3     /* output loss and its gradient (cross-entropy or CTC) */
 #define RNNBKT_KERNEL_SGD 4      /* parameter update (SGD, ADADELTA, eq. 3 aggregation) */
 #define RNNBKT_KERNEL_OTHER 5    /* batch tables, packing, column sums, loss sum */
-#define RNNBKT_KERNEL_KINDS 6
+#define RNNBKT_KERNEL_SIDE 6     /* any work on the library's internal side stream, which
+                                    runs beside the backward recurrence (output-layer and
+                                    weight gradients, their folds): overlapped time */
+#define RNNBKT_KERNEL_KINDS 7
 
 int32_t rnnbkt_kernel_timer(int32_t enable);
 int32_t rnnbkt_kernel_timer_read(int32_t kind, double* total_ms, int64_t* launches,

@@ -276,10 +276,15 @@ hipEvent_t pooled_event() {
 }
 
 // Brackets one launch with events when the timer is on.
+bool is_side_stream(hipStream_t st);
+
+// Work recorded on an internal side stream counts as RNNBKT_KERNEL_SIDE
+// whatever kind it is.
 class Timed {
  public:
   Timed(int kind, double flops, double bytes, hipStream_t st) : st_(st) {
     if (!g_timer_on) return;
+    if (is_side_stream(st)) kind = RNNBKT_KERNEL_SIDE;
     std::lock_guard<std::mutex> lk(g_tmu);
     rec_.kind = kind;
     rec_.flops = flops;
@@ -308,6 +313,13 @@ struct Side {
 };
 std::mutex g_side_mu;
 std::vector<std::pair<hipStream_t, Side>> g_sides;
+
+bool is_side_stream(hipStream_t st) {
+  std::lock_guard<std::mutex> lk(g_side_mu);
+  for (auto& e : g_sides)
+    if (e.second.s == st) return true;
+  return false;
+}
 
 hipError_t side_for(hipStream_t st, Side* out) {
   std::lock_guard<std::mutex> lk(g_side_mu);
@@ -519,17 +531,31 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   float* dz = at<float>(reserve, c.dz);
   float* lp = at<float>(workspace, c.loss_part);
 
-  {
-    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-    RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
-    // The CTC loss has no per-frame labels: nothing to pack (k_pack reads
-    // labels only when given somewhere to put them).
-    RNNBKT_HIP(launch_pack(x, ctc ? nullptr : labels, d_bs, d_off, T, B, s.D, Xp,
-                           ctc ? nullptr : Yp, pf, pr, st));
-  }
-
   const int GH = s.G * s.H;
   const int ldh = s.dirs * s.H;
+  const bool persist = use_persistent();
+  // Batch tables, packing and, for the resident kernels, the sentinel in
+  // every layer's output: one launch when the batch fits its arguments.
+  // The CTC loss has no per-frame labels: nothing to pack (labels are read
+  // only when given somewhere to put them).
+  bool prefilled = false;
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    FillJob pre[kFillJobs];
+    const int npre = persist ? s.L : 0;
+    for (int l = 0; l < npre && l < kFillJobs; ++l)
+      pre[l] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l])), N * ldh};
+    if (B <= kPrepMaxB && npre <= kFillJobs) {
+      RNNBKT_HIP(launch_prepare(lengths, B, T, x, ctc ? nullptr : labels, s.D, d_bs, d_off, Xp,
+                                ctc ? nullptr : Yp, pf, pr, pre, npre, kPublishSentinel, st));
+      prefilled = true;
+    } else {
+      RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
+      RNNBKT_HIP(launch_pack(x, ctc ? nullptr : labels, d_bs, d_off, T, B, s.D, Xp,
+                             ctc ? nullptr : Yp, pf, pr, st));
+    }
+  }
+
   const uint64_t hout_bytes = sizeof(float) * (uint64_t)N * ldh;
   // One recurrence unit (layer l, direction d) of a persistent launch.
   auto make_unit = [&](int l, int d, bool in_published) {
@@ -594,7 +620,7 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   const int nblk = (int)((N + kOutRows - 1) / kOutRows);
   bool streamed_out = false;
   std::vector<char> layer_done(s.L, 0);
-  if (use_persistent()) {
+  if (persist) {
     int l = 0;
     while (l < s.L) {
       FwdLaunch L = base_launch();
@@ -611,7 +637,7 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       if (n > 0) {
         double fl = 0;
         for (int q = 0; q < n; ++q) fl += s.dirs * unit_flops(l + q);
-        {
+        if (!prefilled) {
           Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
           for (int q = 0; q < n; ++q)
             RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l + q])),
@@ -957,15 +983,19 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * (kup + GH) * s.H;
       }
       {
+        // The sentinel in every buffer the launch publishes, in one launch.
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+        FillJob fills[2 * kMaxUnits];
+        int nf = 0;
         for (int q = 0; q < Lc.nunits; ++q) {
           const BwdUnit& u = Lc.u[q];
-          RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(gru ? u.dah : u.da), N * GH,
-                                     kPublishSentinel, st));
-          if (gru && u.publish_dax)
-            RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(u.da), N * GH, kPublishSentinel,
-                                       st));
+          fills[nf++] = {reinterpret_cast<unsigned*>(gru ? u.dah : u.da), N * GH};
+          if (gru && u.publish_dax) fills[nf++] = {reinterpret_cast<unsigned*>(u.da), N * GH};
         }
+        for (int q0 = 0; q0 < nf; q0 += kFillJobs)
+          RNNBKT_HIP(launch_prepare(nullptr, 0, 0, nullptr, nullptr, 0, nullptr, nullptr, nullptr,
+                                    nullptr, nullptr, nullptr, fills + q0,
+                                    std::min(kFillJobs, nf - q0), kPublishSentinel, st));
       }
       if (streamw) {
         // The weight gradients start on the side stream once the published
@@ -1014,13 +1044,14 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
             Timed tm(RNNBKT_KERNEL_GEMM, wfl, 0.0, side.s);
             RNNBKT_HIP(launch_wgrad_stream(wa, side.s));
           }
+          FoldJob folds[kWgJobs];
           for (int q = 0; q < wa.njobs; ++q) {
             const int l = q / 2;
-            float* out = grads + (q % 2 == 0 ? po.wih[l] : po.whh[l]);
-            Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
-            RNNBKT_HIP(launch_splitk_reduce(wa.job[q].partial, wa.reps, wa.job[q].M, wa.job[q].N,
-                                            out, wa.job[q].N, nullptr, 0, side.s));
+            folds[q] = {wa.job[q].partial, wa.reps, wa.job[q].M, wa.job[q].N,
+                        grads + (q % 2 == 0 ? po.wih[l] : po.whh[l]), wa.job[q].N};
           }
+          Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
+          RNNBKT_HIP(launch_splitk_reduce_multi(folds, wa.njobs, side.s));
         }
       }
       bool fits = false;
@@ -1107,6 +1138,27 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     }
   }
 
+  if (persistent) {
+    // Bias (GRU: both biases; peephole weights) gradients: the recurrence
+    // kernels left one partial per row group; all folded in one launch,
+    // which only needs this stream's kernels (it runs before the join).
+    const int rgroups = (B + 15) / 16;
+    std::vector<FoldJob> folds;
+    for (int ld = 0; ld < s.L * s.dirs; ++ld) {
+      folds.push_back({at<float>(workspace, c.bpart[ld]), rgroups, 1, GH, grads + po.b[ld], GH});
+      if (gru)
+        folds.push_back(
+            {at<float>(workspace, c.bpart_h[ld]), rgroups, 1, GH, grads + po.bhh[ld], GH});
+      if (s.peep)
+        folds.push_back(
+            {at<float>(workspace, c.ppart[ld]), rgroups, 1, 3 * s.H, grads + po.peep[ld], 3 * s.H});
+    }
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
+    for (size_t q0 = 0; q0 < folds.size(); q0 += kFoldJobs)
+      RNNBKT_HIP(launch_splitk_reduce_multi(folds.data() + q0,
+                                            (int32_t)std::min<size_t>(kFoldJobs, folds.size() - q0),
+                                            st));
+  }
   RNNBKT_HIP(mark_join());
   RNNBKT_HIP(wait_join());
   // Weight gradients of every layer, reduced over every valid frame (unless
@@ -1130,25 +1182,11 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
                         s.H, GH, s.H, n, nullptr, 0, s.bf16, side.s, d == 0 ? pf : pr, sk_rec));
       }
-      {
+      if (!persistent) {
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-        if (persistent) {
-          // The recurrence kernel left one partial per row group.
-          const int rgroups = (B + 15) / 16;
-          RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.bpart[ld]), rgroups, 1, GH,
-                                          grads + po.b[ld], GH, nullptr, 0, st));
-          if (gru)
-            RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.bpart_h[ld]), rgroups, 1, GH,
-                                            grads + po.bhh[ld], GH, nullptr, 0, st));
-          if (s.peep)
-            RNNBKT_HIP(launch_splitk_reduce(at<float>(workspace, c.ppart[ld]), rgroups, 1,
-                                            3 * s.H, grads + po.peep[ld], 3 * s.H, nullptr, 0,
-                                            st));
-        } else {
-          RNNBKT_HIP(launch_colsum(dax, N, GH, GH, colsum_rows(N), cs, grads + po.b[ld], st));
-          if (gru)
-            RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, colsum_rows(N), cs, grads + po.bhh[ld], st));
-        }
+        RNNBKT_HIP(launch_colsum(dax, N, GH, GH, colsum_rows(N), cs, grads + po.b[ld], st));
+        if (gru)
+          RNNBKT_HIP(launch_colsum(dahh, N, GH, GH, colsum_rows(N), cs, grads + po.bhh[ld], st));
       }
     }
   }

@@ -75,6 +75,66 @@ __global__ void k_pack(const float* __restrict__ x, const int32_t* __restrict__ 
   prev_rev[f] = (t + 1 < T && b < bs[t + 1]) ? off[t + 1] + b : -1;
 }
 
+struct PrepArgs {
+  int32_t len[kPrepMaxB];
+  int32_t B, T, D;
+  const float* x;
+  const int32_t* labels;
+  int32_t *bs, *off;
+  float* Xp;
+  int32_t *Yp, *pf, *pr;
+  FillJob fill[kFillJobs];
+  int32_t nfill;
+  uint32_t value;
+};
+
+// Packing with the tables written in passing: with lengths non-increasing,
+// frame (t, b) is valid iff len[b] > t, batch_sizes[t] = #{b : len[b] > t}
+// and offsets[t] = sum_b min(len[b], t), so each thread takes them from the
+// lengths directly.  Then the fills, grid-stride, 16 bytes per store.
+__global__ void k_prepare(PrepArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t nth = (int64_t)gridDim.x * blockDim.x;
+  const int64_t frames = (int64_t)a.T * a.B;
+  for (int64_t idx = gid; idx < frames; idx += nth) {
+    const int t = (int)(idx / a.B), b = (int)(idx % a.B);
+    int32_t off_t = 0, off_p = 0, bs_t = 0, bs_n = 0, len_b = 0;
+    for (int q = 0; q < a.B; ++q) {  // uniform index: scalar loads of the lengths
+      const int32_t L = a.len[q];
+      off_t += min(L, t);
+      off_p += min(L, t - 1);
+      bs_t += L > t ? 1 : 0;
+      bs_n += L > t + 1 ? 1 : 0;
+      len_b = q == b ? L : len_b;
+    }
+    if (len_b <= t) continue;
+    if (b == 0) {
+      a.bs[t] = bs_t;
+      a.off[t] = off_t;
+      if (t == a.T - 1) a.off[a.T] = off_t + bs_t;
+    }
+    const int64_t f = off_t + b;
+    const float* src = a.x + idx * a.D;
+    float* dst = a.Xp + f * a.D;
+    for (int k = 0; k < a.D; ++k) dst[k] = src[k];
+    if (a.Yp) a.Yp[f] = a.labels[idx];
+    a.pf[f] = t > 0 ? off_p + b : -1;
+    a.pr[f] = (t + 1 < a.T && b < bs_n) ? off_t + bs_t + b : -1;
+  }
+  const uint4 v4 = make_uint4(a.value, a.value, a.value, a.value);
+  for (int j = 0; j < a.nfill; ++j) {
+    unsigned* p = a.fill[j].p;
+    const int64_t n = a.fill[j].n;
+    for (int64_t i4 = gid * 4; i4 < n; i4 += nth * 4) {
+      if (i4 + 3 < n) {
+        *reinterpret_cast<uint4*>(p + i4) = v4;
+      } else {
+        for (int64_t i = i4; i < n; ++i) p[i] = a.value;
+      }
+    }
+  }
+}
+
 __global__ void k_unpack(const float* __restrict__ H, int W, const int32_t* __restrict__ bs,
                          const int32_t* __restrict__ off, int T, int B,
                          float* __restrict__ out) {
@@ -306,6 +366,39 @@ hipError_t launch_pack(const float* x, const int32_t* labels, const int32_t* bs,
   const int threads = 256;
   hipLaunchKernelGGL(k_pack, dim3((unsigned)((total + threads - 1) / threads)), dim3(threads),
                      0, st, x, labels, bs, off, T, B, D, Xp, Yp, pf, pr);
+  return hipGetLastError();
+}
+
+hipError_t launch_prepare(const int32_t* lengths, int32_t B, int32_t T, const float* x,
+                          const int32_t* labels, int32_t D, int32_t* bs, int32_t* off, float* Xp,
+                          int32_t* Yp, int32_t* pf, int32_t* pr, const FillJob* fills,
+                          int32_t nfill, unsigned value, hipStream_t st) {
+  if (B < 0 || B > kPrepMaxB || nfill < 0 || nfill > kFillJobs) return hipErrorInvalidValue;
+  PrepArgs a{};
+  for (int i = 0; i < B; ++i) a.len[i] = lengths[i];
+  a.B = B;
+  a.T = T;
+  a.D = D;
+  a.x = x;
+  a.labels = labels;
+  a.bs = bs;
+  a.off = off;
+  a.Xp = Xp;
+  a.Yp = Yp;
+  a.pf = pf;
+  a.pr = pr;
+  a.nfill = nfill;
+  a.value = value;
+  int64_t quads = 0;
+  for (int j = 0; j < nfill; ++j) {
+    a.fill[j] = fills[j];
+    quads = std::max<int64_t>(quads, (fills[j].n + 3) / 4);
+  }
+  const int threads = 256;
+  const int64_t want = std::max<int64_t>((int64_t)T * B, std::min<int64_t>(quads, 4096 * threads));
+  if (want == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_prepare, dim3((unsigned)((want + threads - 1) / threads)), dim3(threads), 0,
+                     st, a);
   return hipGetLastError();
 }
 

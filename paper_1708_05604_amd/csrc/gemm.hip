@@ -337,6 +337,37 @@ __global__ void k_splitk_reduce(const float* __restrict__ partial, int S, int M,
   *c = v;
 }
 
+struct FoldArgs {
+  FoldJob job[kFoldJobs];
+  int64_t first[kFoldJobs + 1];  // first element of each job, then the total
+  int32_t njobs;
+};
+
+// One thread per output element of the job its index falls in; the partials
+// are folded in the order of k_splitk_reduce.
+__global__ void k_splitk_reduce_multi(FoldArgs a) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= a.first[a.njobs]) return;
+  int q = 0;
+  while (q + 1 < a.njobs && idx >= a.first[q + 1]) ++q;
+  FoldJob j = a.job[0];
+  for (int r = 1; r < kFoldJobs; ++r)
+    if (r == q) j = a.job[r];
+  const int64_t e = idx - a.first[q];
+  const int64_t MN = (int64_t)j.M * j.N;
+  const int m = (int)(e / j.N), n = (int)(e % j.N);
+  float v0 = 0.f, v1 = 0.f, v2 = 0.f, v3 = 0.f;
+  int s = 0;
+  for (; s + 4 <= j.S; s += 4) {
+    v0 += j.partial[(int64_t)s * MN + e];
+    v1 += j.partial[(int64_t)(s + 1) * MN + e];
+    v2 += j.partial[(int64_t)(s + 2) * MN + e];
+    v3 += j.partial[(int64_t)(s + 3) * MN + e];
+  }
+  for (; s < j.S; ++s) v0 += j.partial[(int64_t)s * MN + e];
+  j.out[(int64_t)m * j.ldc + n] = (v0 + v1) + (v2 + v3);
+}
+
 __global__ void k_colsum_partial(const float* __restrict__ A, int64_t rows, int cols,
                                  int64_t lda, int64_t rows_per_split,
                                  float* __restrict__ partial) {
@@ -388,6 +419,24 @@ hipError_t launch_splitk_reduce(const float* partial, int32_t S, int32_t M, int3
   const int threads = 256;
   hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((total + threads - 1) / threads)),
                      dim3(threads), 0, st, partial, S, M, N, out, ldc, bias, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_splitk_reduce_multi(const FoldJob* jobs, int32_t njobs, hipStream_t st) {
+  if (njobs < 1 || njobs > kFoldJobs) return hipErrorInvalidValue;
+  FoldArgs a{};
+  a.njobs = njobs;
+  int64_t total = 0;
+  for (int q = 0; q < njobs; ++q) {
+    a.job[q] = jobs[q];
+    a.first[q] = total;
+    total += (int64_t)jobs[q].M * jobs[q].N;
+  }
+  a.first[njobs] = total;
+  if (total == 0) return hipSuccess;
+  const int threads = 256;
+  hipLaunchKernelGGL(k_splitk_reduce_multi, dim3((unsigned)((total + threads - 1) / threads)),
+                     dim3(threads), 0, st, a);
   return hipGetLastError();
 }
 

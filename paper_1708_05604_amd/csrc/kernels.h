@@ -51,6 +51,17 @@ hipError_t launch_splitk_reduce(const float* partial, int32_t S, int32_t M, int3
                                 float* out, int64_t ldc, const float* bias, int32_t accumulate,
                                 hipStream_t stream);
 
+// Several folds of the form above (no bias, no accumulation) in one launch:
+// out[m*ldc + n] = sum_s partial[s][m][n], each job its own sizes.
+constexpr int kFoldJobs = 16;
+struct FoldJob {
+  const float* partial;
+  int32_t S, M, N;
+  float* out;
+  int64_t ldc;
+};
+hipError_t launch_splitk_reduce_multi(const FoldJob* jobs, int32_t njobs, hipStream_t stream);
+
 // Column sums of A[rows x cols] (row stride lda), deterministic:
 // partial[s][c] over row slices of `rows_per_split`, then folded into out[c].
 hipError_t launch_colsum(const float* A, int64_t rows, int32_t cols, int64_t lda,
@@ -63,6 +74,22 @@ hipError_t launch_colsum(const float* A, int64_t rows, int32_t cols, int64_t lda
 // offsets[T_max] = n_valid.
 hipError_t launch_batch_tables(const int32_t* lengths_host, int32_t B, int32_t T_max,
                                int32_t* batch_sizes, int32_t* offsets, hipStream_t stream);
+
+// One launch for the start of a batch: what launch_batch_tables and
+// launch_pack do (when B > 0; B <= kPrepMaxB, lengths non-increasing), plus
+// filling fills[0..nfill) with `value` (16-byte aligned buffers).  With B = 0
+// it only fills.
+constexpr int kPrepMaxB = 256;
+constexpr int kFillJobs = 8;
+struct FillJob {
+  unsigned* p;
+  int64_t n;
+};
+hipError_t launch_prepare(const int32_t* lengths_host, int32_t B, int32_t T_max, const float* x,
+                          const int32_t* labels, int32_t D, int32_t* batch_sizes,
+                          int32_t* offsets, float* Xp, int32_t* Yp, int32_t* prev_fwd,
+                          int32_t* prev_rev, const FillJob* fills, int32_t nfill, unsigned value,
+                          hipStream_t stream);
 
 // Padded time-major batch -> packed valid frames (frame of (t, b) = offsets[t] + b):
 // Xp[f][:] = x[t][b][:], Yp[f] = labels[t][b] (labels may be null),

@@ -101,7 +101,10 @@ _SIGNATURES = {
                                                   ctypes.POINTER(ctypes.c_double)]),
 }
 
-KERNEL_KINDS = {"step_fwd": 0, "step_bwd": 1, "gemm": 2, "xent": 3, "sgd": 4, "other": 5}
+KERNEL_KINDS = {"step_fwd": 0, "step_bwd": 1, "gemm": 2, "xent": 3, "sgd": 4, "other": 5,
+                "side": 6}
+# Kinds whose time runs beside the recurrence rather than on the critical path.
+OVERLAPPED_KINDS = ("side",)
 
 _lib = None
 

@@ -309,6 +309,17 @@ def test_wide_batch_many_row_groups():
     H.assert_batch_close(spec, data.params, data, order, label="B=256")
 
 
+def test_batch_beyond_single_launch_tables():
+    """B = 300, more sequences than the one-launch batch preparation takes:
+    tables and packing by the separate kernels."""
+    spec = H.Spec(0, 2, 0, 4, 32, 8)
+    rng = np.random.default_rng(33)
+    lengths = sorted(rng.integers(1, 25, 300).tolist(), reverse=True)
+    data = H.data_from_lengths(spec, lengths, seed=33, scale=0.3)
+    order = H.batch_order(data, range(300))
+    H.assert_batch_close(spec, data.params, data, order, label="B=300")
+
+
 @pytest.mark.parametrize("label,spec,lengths", [
     ("stream-1l", H.Spec(0, 1, 0, 4, 64, 12), [31, 30, 30, 29] + list(range(28, 0, -1))),
     ("stream-2l", H.Spec(0, 2, 0, 8, 32, 8), [70, 64, 40, 33, 17, 17, 3, 1]),
