@@ -178,9 +178,11 @@ int64_t rnnbkt_param_count(const rnnbkt_model_desc* desc);
 
 /*
  * Bytes of the two caller-owned device buffers a batch needs:
- *   reserve   -- written by rnnbkt_lstm_fwd, read by rnnbkt_lstm_bwd of the
- *                same batch (activations kept for backpropagation); must not
- *                be modified in between
+ *   reserve   -- written by rnnbkt_lstm_fwd, used by rnnbkt_lstm_bwd of the
+ *                same batch: activations kept for backpropagation, and the
+ *                backward's gate gradients (the forward prepares them for
+ *                the backward's workgroups to exchange); must not be
+ *                modified in between
  *   workspace -- scratch of either call (no content carried between calls)
  * Depends on (desc, T_max, B, n_valid) only and is non-decreasing in each,
  * so sizing with an epoch's maxima covers every batch of the epoch.
@@ -280,7 +282,7 @@ int32_t rnnbkt_lstm_fwd_ctc(const rnnbkt_model_desc* desc, const float* params, 
  */
 int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
                         const int32_t* lengths, int32_t T_max, int32_t B,
-                        const void* reserve, size_t reserve_bytes, void* workspace,
+                        void* reserve, size_t reserve_bytes, void* workspace,
                         size_t workspace_bytes, float* grads, void* stream);
 
 /* rnnbkt_sgd_apply -- params[i] -= lr * grads[i] for i < n (device fp32). */

@@ -124,18 +124,19 @@ struct Carve {
   // reserve
   size_t bs, off, xp, yp, prev_f, prev_r, dz;
   size_t dhtop;                    // dH of the top layer's output, dZ W_out [N x Htop]
+  std::vector<size_t> da, dah;     // backward gate gradients per layer*dirs [N x G*H]
   std::vector<size_t> hout;        // per layer [N x dirs*H]
   std::vector<size_t> stash, cst;  // per layer*dirs
   size_t reserve;
   // workspace (forward)
   size_t gx[2], loss_part;
+  size_t out_done;  // counter of the output-layer workgroups that finished
   size_t ws_fwd;
   // workspace (backward)
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
   size_t splitk_out, colsum_out;  // output-layer gradients (run beside the recurrence)
   size_t splitk_rec;              // recurrent weight gradients (run beside the input ones)
   size_t wgpart;                  // streamed weight gradients: partial tiles of every layer
-  std::vector<size_t> da, dah;  // per layer*dirs
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
   std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
 
@@ -160,6 +161,12 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   c.prev_r = take(sizeof(int32_t) * N);
   c.dz = take(sizeof(float) * N * s.C);
   c.dhtop = take(sizeof(float) * N * s.Htop);
+  // The backward's gate gradients, exchanged between its workgroups: kept
+  // here so that the forward can set their sentinel beside its recurrence.
+  for (int q = 0; q < s.L * s.dirs; ++q) {
+    c.da.push_back(take(sizeof(float) * N * GH));
+    c.dah.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0);
+  }
   for (int l = 0; l < s.L; ++l) c.hout.push_back(take(sizeof(float) * N * s.dirs * s.H));
   for (int l = 0; l < s.L; ++l)
     for (int d = 0; d < s.dirs; ++d) {
@@ -172,15 +179,12 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   const size_t common = pos;
   for (int d = 0; d < 2; ++d) c.gx[d] = d < s.dirs ? take(sizeof(float) * N * GH) : c.gx[0];
   c.loss_part = take(sizeof(float) * ((N + 15) / 16 + 1));
+  c.out_done = take(sizeof(unsigned));
   c.ws_fwd = pos;
 
   pos = common;
   c.dha = take(sizeof(float) * N * s.Htop);
   c.dhb = take(sizeof(float) * N * s.Htop);
-  for (int q = 0; q < s.L * s.dirs; ++q) {
-    c.da.push_back(take(sizeof(float) * N * GH));
-    c.dah.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0);
-  }
   c.carry = take(sizeof(float) * (size_t)B * s.H);
   c.peep_acc = s.peep ? take(sizeof(float) * (size_t)B * 3 * s.H) : 0;
   size_t sk = 0;
@@ -337,6 +341,27 @@ hipError_t side_for(hipStream_t st, Side* out) {
   g_sides.emplace_back(st, sd);
   *out = sd;
   return hipSuccess;
+}
+
+// Reserve buffers whose backward exchange buffers (dA, GRU dAh) the last
+// forward on them left holding the sentinel; the backward takes the mark, or
+// sets the sentinel itself.
+std::mutex g_pre_mu;
+std::vector<const void*> g_prefilled;
+
+void note_prefilled(const void* reserve, bool yes) {
+  std::lock_guard<std::mutex> lk(g_pre_mu);
+  auto it = std::find(g_prefilled.begin(), g_prefilled.end(), reserve);
+  if (yes && it == g_prefilled.end()) g_prefilled.push_back(reserve);
+  if (!yes && it != g_prefilled.end()) g_prefilled.erase(it);
+}
+
+bool take_prefilled(const void* reserve) {
+  std::lock_guard<std::mutex> lk(g_pre_mu);
+  auto it = std::find(g_prefilled.begin(), g_prefilled.end(), reserve);
+  if (it == g_prefilled.end()) return false;
+  g_prefilled.erase(it);
+  return true;
 }
 
 // Host copy of the batch tables (active rows per step and frame offsets).
@@ -538,6 +563,19 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   // every layer's output: one launch when the batch fits its arguments.
   // The CTC loss has no per-frame labels: nothing to pack (labels are read
   // only when given somewhere to put them).
+  // The backward's exchange buffers, which the forward sets to the
+  // sentinel when the resident kernels run: beside the recurrence (by the
+  // output-layer workgroups) when the output layer runs there, else here.
+  FillJob bwd_fill[kFillJobs];
+  int nbwd = 0;
+  if (persist && s.L * s.dirs * (s.cell == RNNBKT_CELL_GRU ? 2 : 1) <= kFillJobs) {
+    for (int q = 0; q < s.L * s.dirs; ++q) {
+      bwd_fill[nbwd++] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.da[q])), N * GH};
+      if (s.cell == RNNBKT_CELL_GRU)
+        bwd_fill[nbwd++] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.dah[q])), N * GH};
+    }
+  }
+  unsigned* out_done = at<unsigned>(workspace, c.out_done);
   bool prefilled = false;
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
@@ -547,12 +585,14 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       pre[l] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l])), N * ldh};
     if (B <= kPrepMaxB && npre <= kFillJobs) {
       RNNBKT_HIP(launch_prepare(lengths, B, T, x, ctc ? nullptr : labels, s.D, d_bs, d_off, Xp,
-                                ctc ? nullptr : Yp, pf, pr, pre, npre, kPublishSentinel, st));
+                                ctc ? nullptr : Yp, pf, pr, pre, npre, kPublishSentinel, out_done,
+                                st));
       prefilled = true;
     } else {
       RNNBKT_HIP(launch_batch_tables(lengths, B, T, d_bs, d_off, st));
       RNNBKT_HIP(launch_pack(x, ctc ? nullptr : labels, d_bs, d_off, T, B, s.D, Xp,
                              ctc ? nullptr : Yp, pf, pr, st));
+      RNNBKT_HIP(launch_fill_u32(out_done, 1, 0u, st));
     }
   }
 
@@ -658,6 +698,10 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
           oa.dh = at<float>(reserve, c.dhtop);
           oa.partial = lp;
           oa.nblocks = nblk;
+          for (int q = 0; q < nbwd; ++q) oa.fill[q] = bwd_fill[q];
+          oa.nfill = nbwd;
+          oa.done = out_done;
+          oa.loss = loss;
           L.out_blocks = std::min(kOutStreamGrid, nblk);
           if (fwd_persistent_blocks(L, s.cell, s.bf16, B) == 0) L.out_blocks = 0;
         }
@@ -710,11 +754,17 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       }
     }
   }
-  if (streamed_out) {
+  // The loss was summed by the output-layer workgroups, which also set the
+  // backward's sentinels; otherwise they are set here (the separate output
+  // kernels below run after this launch).
+  if (!streamed_out && nbwd > 0) {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-    RNNBKT_HIP(launch_sum(lp, nblk, 1.0f / (float)N, loss, st));
-    return RNNBKT_OK;
+    RNNBKT_HIP(launch_prepare(nullptr, 0, 0, nullptr, nullptr, 0, nullptr, nullptr, nullptr,
+                              nullptr, nullptr, nullptr, bwd_fill, nbwd, kPublishSentinel, nullptr,
+                              st));
   }
+  note_prefilled(reserve, nbwd > 0);
+  if (streamed_out) return RNNBKT_OK;
   // Output layer and loss, then dH of the top layer for the backward.
   const float* top = at<float>(reserve, c.hout[s.L - 1]);
   float* dhtop = at<float>(reserve, c.dhtop);
@@ -810,7 +860,7 @@ extern "C" int32_t rnnbkt_lstm_fwd_ctc(const rnnbkt_model_desc* desc, const floa
 
 extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
                                    const int32_t* lengths, int32_t T, int32_t B,
-                                   const void* reserve, size_t reserve_bytes, void* workspace,
+                                   void* reserve, size_t reserve_bytes, void* workspace,
                                    size_t workspace_bytes, float* grads, void* stream) {
   clear_error();
   Shape s;
@@ -881,10 +931,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   }
   const float* dhtop = at<float>(reserve, c.dhtop);
 
-  auto da_of = [&](int l, int d) { return at<float>(workspace, c.da[l * s.dirs + d]); };
+  auto da_of = [&](int l, int d) { return at<float>(reserve, c.da[l * s.dirs + d]); };
   auto dah_of = [&](int l, int d) {
-    return gru ? at<float>(workspace, c.dah[l * s.dirs + d]) : nullptr;
+    return gru ? at<float>(reserve, c.dah[l * s.dirs + d]) : nullptr;
   };
+  // Whether the forward left the exchange buffers holding the sentinel.
+  const bool prefilled = take_prefilled(reserve);
   const uint64_t rec_b = sizeof(float) * (uint64_t)N * GH;
   const uint32_t rec_bytes = rec_b < 0x7FFFFFF0u ? (uint32_t)rec_b : 0x7FFFFFF0u;
   // Unit (layer l, direction d) of a persistent backward launch.
@@ -982,7 +1034,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         const double kup = (s.dirs == 1 && g.hi - q + 1 < s.L) ? GH : 0;
         for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * (kup + GH) * s.H;
       }
-      {
+      if (!prefilled) {
         // The sentinel in every buffer the launch publishes, in one launch.
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
         FillJob fills[2 * kMaxUnits];
@@ -995,7 +1047,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
         for (int q0 = 0; q0 < nf; q0 += kFillJobs)
           RNNBKT_HIP(launch_prepare(nullptr, 0, 0, nullptr, nullptr, 0, nullptr, nullptr, nullptr,
                                     nullptr, nullptr, nullptr, fills + q0,
-                                    std::min(kFillJobs, nf - q0), kPublishSentinel, st));
+                                    std::min(kFillJobs, nf - q0), kPublishSentinel, nullptr, st));
       }
       if (streamw) {
         // The weight gradients start on the side stream once the published

@@ -86,6 +86,7 @@ struct PrepArgs {
   FillJob fill[kFillJobs];
   int32_t nfill;
   uint32_t value;
+  unsigned* zero;
 };
 
 // Packing with the tables written in passing: with lengths non-increasing,
@@ -96,6 +97,7 @@ __global__ void k_prepare(PrepArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t nth = (int64_t)gridDim.x * blockDim.x;
   const int64_t frames = (int64_t)a.T * a.B;
+  if (gid == 0 && a.zero) *a.zero = 0u;
   for (int64_t idx = gid; idx < frames; idx += nth) {
     const int t = (int)(idx / a.B), b = (int)(idx % a.B);
     int32_t off_t = 0, off_p = 0, bs_t = 0, bs_n = 0, len_b = 0;
@@ -372,7 +374,7 @@ hipError_t launch_pack(const float* x, const int32_t* labels, const int32_t* bs,
 hipError_t launch_prepare(const int32_t* lengths, int32_t B, int32_t T, const float* x,
                           const int32_t* labels, int32_t D, int32_t* bs, int32_t* off, float* Xp,
                           int32_t* Yp, int32_t* pf, int32_t* pr, const FillJob* fills,
-                          int32_t nfill, unsigned value, hipStream_t st) {
+                          int32_t nfill, unsigned value, unsigned* zero_word, hipStream_t st) {
   if (B < 0 || B > kPrepMaxB || nfill < 0 || nfill > kFillJobs) return hipErrorInvalidValue;
   PrepArgs a{};
   for (int i = 0; i < B; ++i) a.len[i] = lengths[i];
@@ -389,13 +391,15 @@ hipError_t launch_prepare(const int32_t* lengths, int32_t B, int32_t T, const fl
   a.pr = pr;
   a.nfill = nfill;
   a.value = value;
+  a.zero = zero_word;
   int64_t quads = 0;
   for (int j = 0; j < nfill; ++j) {
     a.fill[j] = fills[j];
     quads = std::max<int64_t>(quads, (fills[j].n + 3) / 4);
   }
   const int threads = 256;
-  const int64_t want = std::max<int64_t>((int64_t)T * B, std::min<int64_t>(quads, 4096 * threads));
+  const int64_t want = std::max<int64_t>(std::max<int64_t>((int64_t)T * B, zero_word ? 1 : 0),
+                                         std::min<int64_t>(quads, 4096 * threads));
   if (want == 0) return hipSuccess;
   hipLaunchKernelGGL(k_prepare, dim3((unsigned)((want + threads - 1) / threads)), dim3(threads), 0,
                      st, a);

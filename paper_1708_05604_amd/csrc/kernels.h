@@ -10,6 +10,14 @@
 
 namespace rnnbkt {
 
+// A buffer of n 32-bit words to set to one value (16-byte aligned).
+constexpr int kFillJobs = 8;
+struct FillJob {
+  unsigned* p;
+  int64_t n;
+};
+
+
 // Cell nonlinearities of both recurrence implementations (device code):
 // the logistic function from the hardware exp and reciprocal (relative
 // error a few ulp), and tanh x = 2 sigma(2x) - 1 (absolute error a few
@@ -80,16 +88,12 @@ hipError_t launch_batch_tables(const int32_t* lengths_host, int32_t B, int32_t T
 // filling fills[0..nfill) with `value` (16-byte aligned buffers).  With B = 0
 // it only fills.
 constexpr int kPrepMaxB = 256;
-constexpr int kFillJobs = 8;
-struct FillJob {
-  unsigned* p;
-  int64_t n;
-};
+// zero_word (if not null) is set to 0.
 hipError_t launch_prepare(const int32_t* lengths_host, int32_t B, int32_t T_max, const float* x,
                           const int32_t* labels, int32_t D, int32_t* batch_sizes,
                           int32_t* offsets, float* Xp, int32_t* Yp, int32_t* prev_fwd,
                           int32_t* prev_rev, const FillJob* fills, int32_t nfill, unsigned value,
-                          hipStream_t stream);
+                          unsigned* zero_word, hipStream_t stream);
 
 // Padded time-major batch -> packed valid frames (frame of (t, b) = offsets[t] + b):
 // Xp[f][:] = x[t][b][:], Yp[f] = labels[t][b] (labels may be null),
@@ -255,6 +259,14 @@ struct OutStreamArgs {
   float* dh;         // [N x Htop]
   float* partial;    // [nblocks]
   int32_t nblocks;
+  // Before the output layer, these workgroups set fill[0..nfill) to the
+  // publication sentinel (buffers of a later launch).  After it, the last
+  // of them to finish (counted in *done, zero before the launch) writes
+  // loss[0] = inv_n * sum of partial, summed in a fixed order.
+  FillJob fill[kFillJobs];
+  int32_t nfill;
+  unsigned* done;
+  float* loss;
 };
 // Output-layer workgroups of a launch at most.
 constexpr int kOutStreamGrid = 32;

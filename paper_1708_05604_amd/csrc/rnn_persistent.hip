@@ -303,10 +303,37 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lq = lane >> 4;
   for (int i = tid; i < C * Htop; i += 256) Ws[(i / Htop) * WL + i % Htop] = a.W[i];
+  // The sentinel fills are paced by the output blocks: block blk takes
+  // quads [blk * per, (blk + 1) * per) of the fills laid end to end, so the
+  // writes spread over the recurrence instead of contending with its first
+  // steps (non-temporal stores: the lines are next read by another launch).
+  int64_t fill_quads = 0;
+  for (int j = 0; j < a.nfill; ++j) fill_quads += (a.fill[j].n + 3) / 4;
+  const int64_t per = (fill_quads + a.nblocks - 1) / a.nblocks;
+  auto fill_share = [&](int blk) {
+    const u4 v4 = {kSentinel, kSentinel, kSentinel, kSentinel};
+    const int64_t q1 = min(fill_quads, (int64_t)(blk + 1) * per);
+    int64_t base = 0;
+    for (int j = 0; j < a.nfill; ++j) {
+      const int64_t n = a.fill[j].n, nq = (n + 3) / 4;
+      const int64_t lo = max((int64_t)blk * per, base), hi = min(q1, base + nq);
+      unsigned* p = a.fill[j].p;
+      for (int64_t q = lo + tid; q < hi; q += 256) {
+        const int64_t i4 = (q - base) * 4;
+        if (i4 + 3 < n) {
+          __builtin_nontemporal_store(v4, reinterpret_cast<u4*>(p + i4));
+        } else {
+          for (int64_t i = i4; i < n; ++i) p[i] = kSentinel;
+        }
+      }
+      base += nq;
+    }
+  };
   const __amdgpu_buffer_rsrc_t rh = published_rsrc(a.h, a.h_bytes);
   constexpr int RT = kOutRows / 16;
   const int ctiles = (C + 15) / 16, htiles = Htop / 16;
   for (int blk = first; blk < a.nblocks; blk += stride) {
+    if (a.nfill > 0) fill_share(blk);
     const int64_t f0 = (int64_t)blk * kOutRows;
     // this block's h rows, re-read until published
     for (int i = tid; i < kOutRows * Htop / 4; i += 256) {
@@ -390,6 +417,26 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
       }
     }
     __syncthreads();  // Hs, Zs and wsum are rewritten for the next block
+  }
+  // The last workgroup to finish sums the partials (every one of them was
+  // written before its workgroup's count: release fence, counter, acquire
+  // fence in the reader).
+  if (tid == 0) {
+    __threadfence();
+    const unsigned prev = __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    wsum[0] = prev + 1 == (unsigned)stride ? 1.f : 0.f;
+  }
+  __syncthreads();
+  if (wsum[0] != 0.f) {
+    __threadfence();
+    float v = 0.f;
+    for (int i = tid; i < a.nblocks; i += 256) v += a.partial[i];
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    __syncthreads();
+    if (lane == 0) wsum[wave] = v;
+    __syncthreads();
+    if (tid == 0) a.loss[0] = ((wsum[0] + wsum[1]) + (wsum[2] + wsum[3])) * a.inv_n;
   }
 }
 

@@ -339,6 +339,35 @@ def test_streamed_weight_gradients(label, spec, lengths, monkeypatch):
     assert H.normwise_err(a[1], b[1]) < 1e-6
 
 
+
+@pytest.mark.parametrize("label,spec,lengths,env", [
+    ("lstm-streamed", H.Spec(0, 2, 0, 8, 32, 8), [40, 33, 17, 2], {}),
+    ("lstm-output-after", H.Spec(0, 2, 0, 8, 32, 8), [40, 33, 17, 2], {"RNNBKT_OUTPUT": "after"}),
+    ("gru-bf16", H.Spec(1, 2, 0, 8, 32, 8, synth.BF16), [40, 33, 17, 2], {}),
+    ("bilstm", H.Spec(0, 2, 1, 4, 32, 8), [30, 29, 3, 1], {}),
+])
+def test_backward_repeated_without_forward(label, spec, lengths, env, monkeypatch):
+    """The forward leaves the backward's exchange buffers holding the
+    sentinel; a second backward of the same batch (buffers now used) sets it
+    itself, and both give the same gradients bit for bit."""
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    data = H.data_from_lengths(spec, lengths, seed=45, scale=0.3)
+    order = H.batch_order(data, range(len(lengths)))
+    g = H.GpuBatch(spec, data.params, data, order)
+    g.forward()
+    g.backward()
+    g.torch.cuda.synchronize()
+    first = g.grads.cpu().numpy().copy()
+    g.grads.fill_(float("nan"))
+    g.backward()
+    g.torch.cuda.synchronize()
+    lib.sync_check()
+    second = g.grads.cpu().numpy()
+    assert np.isfinite(first).all()
+    assert np.array_equal(first, second), label
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("label,spec,lengths", [
     ("out-1l-c12", H.Spec(0, 1, 0, 4, 64, 12), [31, 30, 30, 29] + list(range(28, 0, -1))),
