@@ -210,10 +210,9 @@ int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_
  * The loss gradient w.r.t. the logits, and its product with W_out (the
  * gradient w.r.t. the top layer's output), are computed here and kept in
  * reserve.  When the top layer runs in a resident launch (fp32, one stream
- * declared), the output layer and loss run beside it on an internal stream,
- * on rows of the top layer as they are published; the call still returns
- * with all of its work ordered on `stream`.  RNNBKT_OUTPUT=after runs them
- * after the recurrence instead.
+ * declared), the output layer and loss are computed by extra workgroups of
+ * that launch, on rows of the top layer as they are published;
+ * RNNBKT_OUTPUT=after runs them as separate kernels after the recurrence.
  * Recurrence kernels (this call and rnnbkt_lstm_bwd): all steps of a layer
  * (or of a unidirectional stack) in one launch whose workgroups stay
  * resident, when the grid fits (see rnnbkt_set_concurrency), else one
@@ -278,6 +277,13 @@ int32_t rnnbkt_lstm_fwd_ctc(const rnnbkt_model_desc* desc, const float* params, 
  *   grads   device fp32[param_count] out: d loss / d params (overwritten
  *           entirely, same layout as params)
  * Other arguments as in rnnbkt_lstm_fwd (labels are not needed again).
+ * For an fp32 unidirectional LSTM stack in one resident launch (one stream
+ * declared), the layer weight gradients are computed by extra workgroups of
+ * that launch as the gate gradients are published (RNNBKT_WGRAD=after:
+ * GEMMs after it).  The
+ * output layer's weight gradients run on an internal stream beside the
+ * recurrence when one stream is declared; the call returns with all of its
+ * work ordered on `stream`.
  * Reductions run in a fixed order: results are bitwise reproducible.
  */
 int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
@@ -375,8 +381,9 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
 #define RNNBKT_KERNEL_SGD 4      /* parameter update (SGD, ADADELTA, eq. 3 aggregation) */
 #define RNNBKT_KERNEL_OTHER 5    /* batch tables, packing, column sums, loss sum */
 #define RNNBKT_KERNEL_SIDE 6     /* any work on the library's internal side stream, which
-                                    runs beside the backward recurrence (output-layer and
-                                    weight gradients, their folds): overlapped time */
+                                    runs beside other work of the backward (output-layer
+                                    weight gradients; recurrent weight gradients when the
+                                    launch does not compute them): overlapped time */
 #define RNNBKT_KERNEL_KINDS 7
 
 int32_t rnnbkt_kernel_timer(int32_t enable);

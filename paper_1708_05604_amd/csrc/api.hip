@@ -313,7 +313,7 @@ class Timed {
 // it and join it back.  Created on first use and kept for the process.
 struct Side {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, mid = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
 };
 std::mutex g_side_mu;
 std::vector<std::pair<hipStream_t, Side>> g_sides;
@@ -335,7 +335,6 @@ hipError_t side_for(hipStream_t st, Side* out) {
   Side sd;
   hipError_t e = hipStreamCreateWithFlags(&sd.s, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.mid, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&sd.join, hipEventDisableTiming);
   if (e != hipSuccess) return e;
   g_sides.emplace_back(st, sd);
@@ -651,10 +650,12 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   // Output layer and loss run by extra workgroups of the launch that holds
   // the top layer, on its rows as they are published: fp32 with per-frame
   // labels, W_out plus a block of rows within a workgroup's LDS, and the
-  // grid still resident with them.  RNNBKT_OUTPUT=after runs them after the
-  // recurrence as separate kernels.
+  // grid still resident with them; one stream declared (several streams
+  // already fill the GPU between them).  RNNBKT_OUTPUT=after runs them after
+  // the recurrence as separate kernels.
   const char* out_env = getenv("RNNBKT_OUTPUT");
-  const bool stream_out_ok = !ctc && !s.bf16 && output_stream_lds(s.C, s.Htop) > 0 &&
+  const bool stream_out_ok = concurrency() == 1 && !ctc && !s.bf16 &&
+                             output_stream_lds(s.C, s.Htop) > 0 &&
                              hout_bytes < 0x7FFFFFF0u &&
                              !(out_env && strcmp(out_env, "after") == 0);
   const int nblk = (int)((N + kOutRows - 1) / kOutRows);
@@ -1005,12 +1006,16 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       hi -= best;
     }
   }
-  // Weight gradients streamed beside the recurrence (k_wgrad_stream): fp32
-  // unidirectional LSTM stacks whose layers all run in one resident launch,
-  // with the side stream in use.  RNNBKT_WGRAD=after computes them after it.
+  // Weight gradients computed beside the recurrence by extra workgroups of
+  // its launch: fp32 unidirectional LSTM stacks whose layers all run in one
+  // resident launch, one stream declared (with several, the other streams'
+  // launches already fill the GPU).  RNNBKT_WGRAD=after computes them after.
   const char* wg_env = getenv("RNNBKT_WGRAD");
   bool streamw = persistent && split && !gru && s.dirs == 1 && !s.bf16 && groups.size() == 1 &&
                  !(wg_env && strcmp(wg_env, "after") == 0);
+  FoldJob wg_folds[kWgJobs];
+  int nwg_folds = 0;
+  double wg_flops = 0;
 
   if (persistent) {
     // Gradient w.r.t. the output of the top layer of the next group; the
@@ -1050,12 +1055,10 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                                     std::min(kFillJobs, nf - q0), kPublishSentinel, nullptr, st));
       }
       if (streamw) {
-        // The weight gradients start on the side stream once the published
-        // buffers hold the sentinel; the grid leaves the recurrence enough
-        // CUs to be resident whatever order the two are dispatched in.
-        const int free_cus = cu_count() - bwd_persistent_blocks(Lc, s.cell, s.bf16, B);
-        WgStreamArgs wa{};
-        float* part = at<float>(workspace, c.wgpart);
+        // As many workgroups per output tile as stay resident with the
+        // recurrence (at least one, else the products run after it).
+        WgStreamArgs& wa = Lc.wg;
+        wa = WgStreamArgs{};
         for (int l = 0; l < s.L; ++l) {
           const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
           WgJob ji{}, jh{};
@@ -1076,39 +1079,31 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
             wa.job[wa.njobs++] = *j;
           }
         }
-        wa.reps = std::min(kWgRepsMax, free_cus / std::max(wa.tiles, 1));
+        wa.off = d_off;
+        wa.T = T;
+        wa.spc = kWgStepsPerChunk;
+        wa.nchunks = (T + kWgStepsPerChunk - 1) / kWgStepsPerChunk;
+        Lc.wg_on = 1;
+        wa.reps = kWgRepsMax;
+        while (wa.reps >= 1 && bwd_persistent_blocks(Lc, s.cell, s.bf16, B) == 0) --wa.reps;
         if (wa.reps < 1) {
+          Lc.wg_on = 0;
           streamw = false;
         } else {
+          float* part = at<float>(workspace, c.wgpart);
           for (int q = 0; q < wa.njobs; ++q) {
             wa.job[q].partial = part;
             part += (size_t)wa.reps * wa.job[q].M * wa.job[q].N;
-          }
-          wa.off = d_off;
-          wa.T = T;
-          wa.spc = kWgStepsPerChunk;
-          wa.nchunks = (T + kWgStepsPerChunk - 1) / kWgStepsPerChunk;
-          RNNBKT_HIP(hipEventRecord(side.mid, st));
-          RNNBKT_HIP(hipStreamWaitEvent(side.s, side.mid, 0));
-          double wfl = 0;
-          for (int l = 0; l < s.L; ++l) wfl += 2.0 * N * GH * (s.din(l) + s.H);
-          {
-            Timed tm(RNNBKT_KERNEL_GEMM, wfl, 0.0, side.s);
-            RNNBKT_HIP(launch_wgrad_stream(wa, side.s));
-          }
-          FoldJob folds[kWgJobs];
-          for (int q = 0; q < wa.njobs; ++q) {
             const int l = q / 2;
-            folds[q] = {wa.job[q].partial, wa.reps, wa.job[q].M, wa.job[q].N,
-                        grads + (q % 2 == 0 ? po.wih[l] : po.whh[l]), wa.job[q].N};
+            wg_folds[nwg_folds++] = {wa.job[q].partial, wa.reps, wa.job[q].M, wa.job[q].N,
+                                     grads + (q % 2 == 0 ? po.wih[l] : po.whh[l]), wa.job[q].N};
           }
-          Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
-          RNNBKT_HIP(launch_splitk_reduce_multi(folds, wa.njobs, side.s));
+          for (int l = 0; l < s.L; ++l) wg_flops += 2.0 * N * GH * (s.din(l) + s.H);
         }
       }
       bool fits = false;
       {
-        Timed tm(RNNBKT_KERNEL_STEP_BWD, fl, 0.0, st);
+        Timed tm(RNNBKT_KERNEL_STEP_BWD, fl + wg_flops, 0.0, st);
         RNNBKT_HIP(launch_bwd_persistent(Lc, s.cell, s.bf16, B, st, &fits));
       }
       RNNBKT_REQUIRE(fits, RNNBKT_EHIP, "lstm_bwd: persistent launch no longer fits");
@@ -1192,10 +1187,11 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
 
   if (persistent) {
     // Bias (GRU: both biases; peephole weights) gradients: the recurrence
-    // kernels left one partial per row group; all folded in one launch,
-    // which only needs this stream's kernels (it runs before the join).
+    // kernels left one partial per row group; folded in one launch with the
+    // partial tiles of the weight gradients computed in the launch, which
+    // only needs this stream's kernels (it runs before the join).
     const int rgroups = (B + 15) / 16;
-    std::vector<FoldJob> folds;
+    std::vector<FoldJob> folds(wg_folds, wg_folds + nwg_folds);
     for (int ld = 0; ld < s.L * s.dirs; ++ld) {
       folds.push_back({at<float>(workspace, c.bpart[ld]), rgroups, 1, GH, grads + po.b[ld], GH});
       if (gru)

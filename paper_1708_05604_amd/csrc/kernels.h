@@ -314,31 +314,16 @@ struct BwdUnit {
   int32_t wg_begin;
 };
 
-struct BwdLaunch {
-  BwdUnit u[kMaxUnits];
-  int32_t nunits;
-  const int32_t* bs;
-  const int32_t* off;
-  int32_t H, ldh, T;
-  int32_t slices, rgroups;  // set by the launcher
-};
-
-// Workgroups a forward launch of these units would need (0 = shape not
-// supported by the persistent kernel).
-int fwd_persistent_blocks(const FwdLaunch& a, int cell, bool bf16, int B);
-hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
-                                 bool* fits);
-int bwd_persistent_blocks(const BwdLaunch& a, int cell, bool bf16, int B);
-hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
-                                 bool* fits);
-// Weight gradients streamed beside the backward recurrence (fp32 LSTM
-// stacks): C = A^T B summed over the valid frames, for every (A, B) job,
-// while the recurrence is still publishing A.  The frames are taken in
-// chunks of `spc` time steps from the last step down (the order the
-// recurrence finishes them); each workgroup owns one 64 x 64 output tile of
-// one job and accumulates every `reps`-th chunk in registers, waiting (with
-// device-scope polls of the sentinel) for the A rows it reads.  It writes
-// one partial tile; partial[r] of job j (r < reps) are then summed in order.
+// Weight gradients computed by extra workgroups of the backward launch of
+// an fp32 LSTM stack: C = A^T B summed over the valid frames, for every
+// (A, B) job, while the recurrence is still publishing A.  The frames are
+// taken in chunks of `spc` time steps from the last step down (the order the
+// recurrence finishes them).  A workgroup of 64*NW threads holds NW/4
+// sub-tiles of 256 threads, each owning one 64 x 64 output tile; all of them
+// accumulate every `reps`-th chunk (the same chunks, so they keep step at
+// the workgroup's barriers) in registers, waiting (device-scope polls of the
+// sentinel) for the A rows they read.  Each writes one partial tile;
+// partial[r] of job j (r < reps) are then summed in order.
 constexpr int kWgJobs = 8;      // two per layer, up to kMaxUnits layers
 constexpr int kWgRepsMax = 8;   // workgroups per output tile, at most
 struct WgJob {
@@ -358,13 +343,37 @@ struct WgStreamArgs {
   const int32_t* off;      // device frame offsets per step [T+1]
   int32_t T, spc, nchunks;
 };
-hipError_t launch_wgrad_stream(const WgStreamArgs& a, hipStream_t stream);
-constexpr int kWgStepsPerChunk = 4;  // short chunks leave little after the recurrence ends
-// Compute units of the current device (0 on error).
-int cu_count();
+// One step per chunk: the last chunk, all that is left once the recurrence
+// ends, is then a single step's frames (measured against 2, 4 and longer
+// chunks, and 4-step chunks ending in single steps).
+constexpr int kWgStepsPerChunk = 1;
 // Output tiles of one job (64 x 64).
 inline int32_t wg_tiles(int32_t M, int32_t N) { return ((M + 63) / 64) * ((N + 63) / 64); }
 
+struct BwdLaunch {
+  BwdUnit u[kMaxUnits];
+  int32_t nunits;
+  const int32_t* bs;
+  const int32_t* off;
+  int32_t H, ldh, T;
+  int32_t slices, rgroups;  // set by the launcher
+  // fp32 LSTM only: wg_on adds the weight-gradient workgroups, ceil(tiles /
+  // (NW/4)) * reps of them after the recurrence ones (wg_blocks: set by the
+  // launcher).
+  WgStreamArgs wg;
+  int32_t wg_on, wg_blocks;
+};
+
+// Workgroups a forward launch of these units would need (0 = shape not
+// supported by the persistent kernel).
+int fwd_persistent_blocks(const FwdLaunch& a, int cell, bool bf16, int B);
+hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
+                                 bool* fits);
+int bwd_persistent_blocks(const BwdLaunch& a, int cell, bool bf16, int B);
+hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStream_t stream,
+                                 bool* fits);
+// Compute units of the current device (0 on error).
+int cu_count();
 
 // Number of waits for published values that gave up (should stay 0).
 // Streams that may run persistent launches at once (each launch then claims

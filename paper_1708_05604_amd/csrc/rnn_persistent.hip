@@ -663,6 +663,184 @@ __device__ inline void store_or_publish(float* p, float v, bool pub) {
     *p = v;
 }
 
+// ---------------------------------------------------------------- weight gradients
+// C = A^T B over the frames of the batch, by workgroups of the backward
+// launch beside the recurrence that publishes A (see WgStreamArgs).  The
+// tile loop of a 256-thread sub-tile is the fp32 TN product of the GEMM
+// kernels: 32-frame K-tiles staged untransposed in LDS ([k][m] and [k][n],
+// rows padded by 16 floats), fed to v_mfma_f32_16x16x4_f32 with 4 waves of
+// 32 x 32 each.  A's K-tile is read with device-scope loads and re-read until
+// no element holds the sentinel.
+constexpr int kWgBK = 32;
+constexpr int kWgLD = 64 + 16;
+
+constexpr size_t kWgSubLds = sizeof(float) * 2 * kWgBK * kWgLD;  // A and B K-tiles
+
+__device__ inline void wg_load_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0, int clim,
+                                 int k0, int klim, int tid) {
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    const unsigned o = (k0 + k < klim && c0 + c < clim)
+                           ? 4u * (unsigned)((int64_t)(k0 + k) * lda + c0 + c)
+                           : kNoRow;
+    v[rep] = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, kDeviceScope);
+  }
+}
+
+__device__ inline bool wg_clear(const u4 (&v)[2]) {
+  bool ok = true;
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ok &= v[rep][e] != kSentinel;
+  return ok;
+}
+
+// Re-reads this thread's part of an A K-tile until it is all published.
+__device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0,
+                                   int clim, int k0, int klim, int tid) {
+  if (wg_clear(v)) return;
+  for (unsigned polls = 1;; ++polls) {
+    // (not on the recurrence's path: polling gently leaves it the memory
+    // system; measured best of sleeps 2..64)
+    __builtin_amdgcn_s_sleep(32);
+    poll_fence();
+    wg_load_a(v, r, lda, c0, clim, k0, klim, tid);
+    if (wg_clear(v)) return;
+    if ((polls & 1023u) == 0 && waits_abandoned()) return;
+    if (polls >= kMaxPolls) {
+      __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+  }
+}
+
+__device__ inline void wg_load_b(f4 (&v)[2], const float* P, int64_t ld, const int32_t* gather,
+                                 int c0, int clim, int k0, int klim, int tid) {
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    f4 x = {0.f, 0.f, 0.f, 0.f};
+    if (k0 + k < klim && c0 + c < clim) {
+      int64_t row = k0 + k;
+      if (gather) row = gather[row];
+      if (row >= 0) x = *reinterpret_cast<const f4*>(P + row * ld + c0 + c);
+    }
+    v[rep] = x;
+  }
+}
+
+__device__ inline void wg_store(float* S, const f4 (&v)[2], int tid) {
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    *reinterpret_cast<f4*>(S + k * kWgLD + c) = v[rep];
+  }
+}
+
+__device__ inline void wg_store(float* S, const u4 (&v)[2], int tid) {
+#pragma unroll
+  for (int rep = 0; rep < 2; ++rep) {
+    const int k = (tid >> 4) + rep * 16;
+    const int c = (tid & 15) * 4;
+    *reinterpret_cast<u4*>(S + k * kWgLD + c) = v[rep];
+  }
+}
+
+__device__ inline WgJob pick_job(const WgStreamArgs& a, int j) {
+  WgJob u = a.job[0];
+#pragma unroll
+  for (int q = 1; q < kWgJobs; ++q)
+    if (j == q) u = a.job[q];
+  return u;
+}
+
+// Role of workgroup wb (of the weight-gradient ones) in a backward launch of
+// 64*NW threads: sub-tile threadIdx.x / 256 takes tile (wb % groups) * NW/4 +
+// sub of repetition wb / groups; past the last tile it repeats the last one
+// without storing, to keep step at the barriers.  LDS: NW/4 * kWgSubLds.
+template <int NW>
+__device__ void wgrad_role(const WgStreamArgs& a, int wb, float* lds) {
+  constexpr int SUBS = NW / 4;
+  const int sub = threadIdx.x >> 8, tid = threadIdx.x & 255;
+  const int groups = (a.tiles + SUBS - 1) / SUBS;
+  const int rep = wb / groups;
+  const int t_raw = (wb % groups) * SUBS + sub;
+  const bool owner = t_raw < a.tiles;
+  const int tile = owner ? t_raw : a.tiles - 1;
+  float* As = lds + (size_t)sub * 2 * kWgBK * kWgLD;
+  float* Bs = As + kWgBK * kWgLD;
+  int j = 0;
+  for (int q = 1; q < a.njobs; ++q)
+    if (tile >= a.job[q].tile_begin) j = q;
+  const WgJob J = pick_job(a, j);
+  const int lt = tile - J.tile_begin;
+  const int mtiles = (J.M + 63) / 64;
+  const int m0 = (lt % mtiles) * 64, n0 = (lt / mtiles) * 64;
+  const __amdgpu_buffer_rsrc_t ra = published_rsrc(J.A, J.a_bytes);
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int lr = lane & 15, lq = lane >> 4;
+  f4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) acc[i][jj] = f4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c = rep; c < a.nchunks; c += a.reps) {
+    // chunk c: steps [t_lo, t_hi), the c-th group of spc steps from the end
+    const int t_hi = a.T - c * a.spc;
+    const int t_lo = t_hi - a.spc > 0 ? t_hi - a.spc : 0;
+    const int kbeg = a.off[t_lo], kend = a.off[t_hi];
+    u4 ua[2];
+    f4 rb[2];
+    wg_load_a(ua, ra, J.lda, m0, J.M, kbeg, kend, tid);
+    wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, kbeg, kend, tid);
+    for (int k0 = kbeg; k0 < kend; k0 += kWgBK) {
+      wg_settle_a(ua, ra, J.lda, m0, J.M, k0, kend, tid);
+      wg_store(As, ua, tid);
+      wg_store(Bs, rb, tid);
+      __syncthreads();
+      if (k0 + kWgBK < kend) {
+        wg_load_a(ua, ra, J.lda, m0, J.M, k0 + kWgBK, kend, tid);
+        wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, k0 + kWgBK, kend, tid);
+      }
+#pragma unroll
+      for (int kk = 0; kk < kWgBK; kk += 4) {
+        const int kr = (kk + lq) * kWgLD;
+        float av[2], bv[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) av[i] = As[kr + wm + i * 16 + lr];
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) bv[jj] = Bs[kr + wn + jj * 16 + lr];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+            acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[jj], acc[i][jj], 0, 0, 0);
+      }
+      __syncthreads();  // the K-tile in LDS is rewritten next
+    }
+  }
+  if (!owner) return;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int n = n0 + wn + jj * 16 + lr;
+      if (n >= J.N) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = m0 + wm + i * 16 + lq * 4 + q;
+        if (m < J.M) J.partial[((int64_t)rep * J.M + m) * J.N + n] = acc[i][jj][q];
+      }
+    }
+}
+
 // Backpropagation through time of the launch's units.  Workgroup = 16 rows
 // x 16 hidden units of one unit; NW waves split each segment's reduction;
 // threads 0..255 then run the gate-gradient algebra of one (row, unit) each,
@@ -676,8 +854,16 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   float* red = reinterpret_cast<float*>(smem);                // [max(NW, 8)][256]
   int32_t* tbs = reinterpret_cast<int32_t*>(red + (NW < 8 ? 8 : NW) * 256);
   int32_t* toff = tbs + a.T;
+  // Weight-gradient workgroups follow the recurrence ones.
+  const int rec_blocks = gridDim.x - a.wg_blocks;
+  if constexpr (G == 4 && !BF16) {
+    if ((int)blockIdx.x >= rec_blocks) {
+      wgrad_role<NW>(a.wg, blockIdx.x - rec_blocks, reinterpret_cast<float*>(smem));
+      return;
+    }
+  }
   load_tables(a.bs, a.off, a.T, tbs, toff);
-  const int bid = logical_block(gridDim.x);
+  const int bid = logical_block(rec_blocks);
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
     if (bid >= a.u[q].wg_begin) ui = q;
@@ -887,178 +1073,6 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
 // Streams that may run persistent launches at the same time (>= 1).
 std::atomic<int> g_concurrency{1};
 
-// ---------------------------------------------------------------- streamed weight gradients
-// C = A^T B over the frames of the batch, beside the backward recurrence that
-// publishes A (see WgStreamArgs).  The tile loop is the fp32 TN product of
-// the GEMM kernels: 32-frame K-tiles staged untransposed in LDS ([k][m] and
-// [k][n], rows padded by 16 floats), double buffered, fed to
-// v_mfma_f32_16x16x4_f32 with 4 waves of 32 x 32 each.  A's K-tile is read
-// with device-scope loads and re-read until no element holds the sentinel.
-constexpr int kWgBK = 32;
-constexpr int kWgLD = 64 + 16;
-
-__device__ inline void wg_load_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0, int clim,
-                                 int k0, int klim) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int rep = 0; rep < 2; ++rep) {
-    const int k = (tid >> 4) + rep * 16;
-    const int c = (tid & 15) * 4;
-    const unsigned o = (k0 + k < klim && c0 + c < clim)
-                           ? 4u * (unsigned)((int64_t)(k0 + k) * lda + c0 + c)
-                           : kNoRow;
-    v[rep] = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, kDeviceScope);
-  }
-}
-
-__device__ inline bool wg_clear(const u4 (&v)[2]) {
-  bool ok = true;
-#pragma unroll
-  for (int rep = 0; rep < 2; ++rep)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) ok &= v[rep][e] != kSentinel;
-  return ok;
-}
-
-// Re-reads this thread's part of an A K-tile until it is all published.
-__device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0,
-                                   int clim, int k0, int klim) {
-  if (wg_clear(v)) return;
-  for (unsigned polls = 1;; ++polls) {
-    // (not on the recurrence's path: polling gently leaves it the memory
-    // system; measured best of sleeps 2..64)
-    __builtin_amdgcn_s_sleep(32);
-    poll_fence();
-    wg_load_a(v, r, lda, c0, clim, k0, klim);
-    if (wg_clear(v)) return;
-    if ((polls & 1023u) == 0 && waits_abandoned()) return;
-    if (polls >= kMaxPolls) {
-      __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-  }
-}
-
-__device__ inline void wg_load_b(f4 (&v)[2], const float* P, int64_t ld, const int32_t* gather,
-                                 int c0, int clim, int k0, int klim) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int rep = 0; rep < 2; ++rep) {
-    const int k = (tid >> 4) + rep * 16;
-    const int c = (tid & 15) * 4;
-    f4 x = {0.f, 0.f, 0.f, 0.f};
-    if (k0 + k < klim && c0 + c < clim) {
-      int64_t row = k0 + k;
-      if (gather) row = gather[row];
-      if (row >= 0) x = *reinterpret_cast<const f4*>(P + row * ld + c0 + c);
-    }
-    v[rep] = x;
-  }
-}
-
-__device__ inline void wg_store(float* S, const f4 (&v)[2]) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int rep = 0; rep < 2; ++rep) {
-    const int k = (tid >> 4) + rep * 16;
-    const int c = (tid & 15) * 4;
-    *reinterpret_cast<f4*>(S + k * kWgLD + c) = v[rep];
-  }
-}
-
-__device__ inline void wg_store(float* S, const u4 (&v)[2]) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int rep = 0; rep < 2; ++rep) {
-    const int k = (tid >> 4) + rep * 16;
-    const int c = (tid & 15) * 4;
-    *reinterpret_cast<u4*>(S + k * kWgLD + c) = v[rep];
-  }
-}
-
-__device__ inline WgJob pick_job(const WgStreamArgs& a, int j) {
-  WgJob u = a.job[0];
-#pragma unroll
-  for (int q = 1; q < kWgJobs; ++q)
-    if (j == q) u = a.job[q];
-  return u;
-}
-
-__global__ __launch_bounds__(256) void k_wgrad_stream(WgStreamArgs a) {
-  __shared__ __attribute__((aligned(16))) float As[2][kWgBK * kWgLD];
-  __shared__ __attribute__((aligned(16))) float Bs[2][kWgBK * kWgLD];
-  const int tile = blockIdx.x % a.tiles;
-  const int rep = blockIdx.x / a.tiles;
-  int j = 0;
-  for (int q = 1; q < a.njobs; ++q)
-    if (tile >= a.job[q].tile_begin) j = q;
-  const WgJob J = pick_job(a, j);
-  const int lt = tile - J.tile_begin;
-  const int mtiles = (J.M + 63) / 64;
-  const int m0 = (lt % mtiles) * 64, n0 = (lt / mtiles) * 64;
-  const __amdgpu_buffer_rsrc_t ra = published_rsrc(J.A, J.a_bytes);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
-  const int lr = lane & 15, lq = lane >> 4;
-  f4 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj) acc[i][jj] = f4{0.f, 0.f, 0.f, 0.f};
-
-  for (int c = rep; c < a.nchunks; c += a.reps) {
-    // chunk c: steps [t_lo, t_hi), the c-th group of spc steps from the end
-    const int t_hi = a.T - c * a.spc;
-    const int t_lo = t_hi - a.spc > 0 ? t_hi - a.spc : 0;
-    const int kbeg = a.off[t_lo], kend = a.off[t_hi];
-    u4 ua[2];
-    f4 rb[2];
-    wg_load_a(ua, ra, J.lda, m0, J.M, kbeg, kend);
-    wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, kbeg, kend);
-    int buf = 0;
-    for (int k0 = kbeg; k0 < kend; k0 += kWgBK) {
-      wg_settle_a(ua, ra, J.lda, m0, J.M, k0, kend);
-      wg_store(As[buf], ua);
-      wg_store(Bs[buf], rb);
-      __syncthreads();
-      if (k0 + kWgBK < kend) {
-        wg_load_a(ua, ra, J.lda, m0, J.M, k0 + kWgBK, kend);
-        wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, k0 + kWgBK, kend);
-      }
-      const float* a_s = As[buf];
-      const float* b_s = Bs[buf];
-#pragma unroll
-      for (int kk = 0; kk < kWgBK; kk += 4) {
-        const int kr = (kk + lq) * kWgLD;
-        float av[2], bv[2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) av[i] = a_s[kr + wm + i * 16 + lr];
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) bv[jj] = b_s[kr + wn + jj * 16 + lr];
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int jj = 0; jj < 2; ++jj)
-            acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[jj], acc[i][jj], 0, 0, 0);
-      }
-      buf ^= 1;
-    }
-    __syncthreads();  // the next chunk's first K-tile reuses buffer 0
-  }
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      const int n = n0 + wn + jj * 16 + lr;
-      if (n >= J.N) continue;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int m = m0 + wm + i * 16 + lq * 4 + q;
-        if (m < J.M) J.partial[((int64_t)rep * J.M + m) * J.N + n] = acc[i][jj][q];
-      }
-    }
-}
-
 // Dynamic LDS above 64 KiB has to be allowed per kernel once.
 hipError_t allow_lds(const void* kernel, size_t shmem) {
   static std::mutex mu;
@@ -1250,7 +1264,7 @@ const void* bwd_kernel(int cell, bool bf16, int nw, int maxc, bool split) {
 
 struct BwdPlan {
   const void* kernel;
-  int nw, maxc, blocks;
+  int nw, maxc, blocks, wg_blocks;
   bool split;
   size_t shmem;
 };
@@ -1261,7 +1275,7 @@ struct BwdPlan {
 // lstm2); more waves cost a little in the barriers.  The cheapest candidate
 // that fits in registers without spilling wins.
 BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
-  BwdPlan p{nullptr, 0, 0, 0, false, 0};
+  BwdPlan p{nullptr, 0, 0, 0, 0, false, 0};
   const int ch = bf16 ? 32 : 16;
   const int G = cell == RNNBKT_CELL_LSTM ? 4 : 3;
   if (a.T > kMaxSteps || a.nunits < 1 || a.nunits > kMaxUnits || a.H % kBwdUnits != 0) return p;
@@ -1304,6 +1318,14 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
   if (p.nw == 0) return p;
   p.blocks = a.nunits * (a.H / kBwdUnits) * ((B + 15) / 16);
   p.shmem = sizeof(float) * std::max(p.nw, 8) * 256 + sizeof(int32_t) * (2 * a.T + 1);
+  p.wg_blocks = 0;
+  if (a.wg_on) {
+    if (bf16 || G != 4 || a.wg.tiles < 1 || a.wg.reps < 1) return p;
+    const int subs = p.nw / 4;
+    p.wg_blocks = (a.wg.tiles + subs - 1) / subs * a.wg.reps;
+    p.blocks += p.wg_blocks;
+    p.shmem = std::max(p.shmem, subs * kWgSubLds);
+  }
   p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc, p.split);
   return p;
 }
@@ -1324,6 +1346,7 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
   if (!p.kernel) return hipSuccess;
   a.slices = a.H / kBwdUnits;
   a.rgroups = (B + 15) / 16;
+  a.wg_blocks = p.wg_blocks;
   const int per_unit = a.slices * a.rgroups;
   for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
   return coop_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
@@ -1344,11 +1367,6 @@ int cu_count() {
   return cus;
 }
 
-hipError_t launch_wgrad_stream(const WgStreamArgs& a, hipStream_t st) {
-  if (a.tiles <= 0 || a.reps <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_wgrad_stream, dim3(a.tiles * a.reps), dim3(256), 0, st, a);
-  return hipGetLastError();
-}
 
 void set_concurrency(int streams) { g_concurrency.store(streams); }
 int concurrency() { return g_concurrency.load(); }
