@@ -579,9 +579,12 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
     FillJob pre[kFillJobs];
-    const int npre = persist ? s.L : 0;
+    int npre = persist ? s.L : 0;
     for (int l = 0; l < npre && l < kFillJobs; ++l)
       pre[l] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l])), N * ldh};
+    // The output-layer workgroups publish their loss partials.
+    if (persist && npre < kFillJobs)
+      pre[npre++] = {reinterpret_cast<unsigned*>(lp), (N + kOutRows - 1) / kOutRows};
     if (B <= kPrepMaxB && npre <= kFillJobs) {
       RNNBKT_HIP(launch_prepare(lengths, B, T, x, ctc ? nullptr : labels, s.D, d_bs, d_off, Xp,
                                 ctc ? nullptr : Yp, pf, pr, pre, npre, kPublishSentinel, out_done,
@@ -592,6 +595,8 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       RNNBKT_HIP(launch_pack(x, ctc ? nullptr : labels, d_bs, d_off, T, B, s.D, Xp,
                              ctc ? nullptr : Yp, pf, pr, st));
       RNNBKT_HIP(launch_fill_u32(out_done, 1, 0u, st));
+      RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(lp), (N + kOutRows - 1) / kOutRows,
+                                 kPublishSentinel, st));
     }
   }
 

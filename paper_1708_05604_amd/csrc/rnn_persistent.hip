@@ -401,7 +401,7 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
       if (lane == 0) wsum[wave] = term;
     }
     __syncthreads();
-    if (tid == 0) a.partial[blk] = (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]);
+    if (tid == 0) publish(a.partial + blk, (wsum[0] + wsum[1]) + (wsum[2] + wsum[3]));
     for (int t = wave; t < RT * htiles; t += 4) {
       const int r0 = (t % RT) * 16, h0 = (t / RT) * 16;
       f4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -422,16 +422,29 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
   // written before its workgroup's count: release fence, counter, acquire
   // fence in the reader).
   if (tid == 0) {
-    __threadfence();
     const unsigned prev = __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_AGENT);
     wsum[0] = prev + 1 == (unsigned)stride ? 1.f : 0.f;
   }
   __syncthreads();
   if (wsum[0] != 0.f) {
-    __threadfence();
+    // The partials are published (sentinel until written): poll them.
+    const __amdgpu_buffer_rsrc_t rp = published_rsrc(a.partial, 4u * (unsigned)a.nblocks);
     float v = 0.f;
-    for (int i = tid; i < a.nblocks; i += 256) v += a.partial[i];
+    for (int i = tid; i < a.nblocks; i += 256) {
+      unsigned x = __builtin_amdgcn_raw_buffer_load_b32(rp, 4u * (unsigned)i, 0, kDeviceScope);
+      for (unsigned polls = 1; x == kSentinel; ++polls) {
+        __builtin_amdgcn_s_sleep(1);
+        poll_fence();
+        x = __builtin_amdgcn_raw_buffer_load_b32(rp, 4u * (unsigned)i, 0, kDeviceScope);
+        if ((polls & 1023u) == 0 && waits_abandoned()) break;
+        if (polls >= kMaxPolls) {
+          __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+      }
+      v += __uint_as_float(x);
+    }
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
     __syncthreads();
     if (lane == 0) wsum[wave] = v;
