@@ -77,6 +77,7 @@ __global__ void k_pack(const float* __restrict__ x, const int32_t* __restrict__ 
 
 struct PrepArgs {
   int32_t len[kPrepMaxB];
+  int32_t lsum[kPrepMaxB + 1];  // lsum[i] = sum of len[0..i)
   int32_t B, T, D;
   const float* x;
   const int32_t* labels;
@@ -89,27 +90,39 @@ struct PrepArgs {
   unsigned* zero;
 };
 
+// #{b : len[b] > t} for non-increasing lengths (binary search).
+__device__ inline int32_t rows_after(const PrepArgs& a, int t) {
+  int lo = 0, hi = a.B;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a.len[mid] > t)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
 // Packing with the tables written in passing: with lengths non-increasing,
-// frame (t, b) is valid iff len[b] > t, batch_sizes[t] = #{b : len[b] > t}
-// and offsets[t] = sum_b min(len[b], t), so each thread takes them from the
-// lengths directly.  Then the fills, grid-stride, 16 bytes per store.
+// frame (t, b) is valid iff b < batch_sizes[t] = #{b : len[b] > t}, and
+// offsets[t] = sum_b min(len[b], t) = t * batch_sizes[t] + sum of the lengths
+// from batch_sizes[t] on, so each thread takes them from the lengths and
+// their prefix sums (a few binary-search steps).  Then the fills,
+// grid-stride, 16 bytes per store.
 __global__ void k_prepare(PrepArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t nth = (int64_t)gridDim.x * blockDim.x;
   const int64_t frames = (int64_t)a.T * a.B;
   if (gid == 0 && a.zero) *a.zero = 0u;
+  const int32_t total = a.lsum[a.B];
   for (int64_t idx = gid; idx < frames; idx += nth) {
     const int t = (int)(idx / a.B), b = (int)(idx % a.B);
-    int32_t off_t = 0, off_p = 0, bs_t = 0, bs_n = 0, len_b = 0;
-    for (int q = 0; q < a.B; ++q) {  // uniform index: scalar loads of the lengths
-      const int32_t L = a.len[q];
-      off_t += min(L, t);
-      off_p += min(L, t - 1);
-      bs_t += L > t ? 1 : 0;
-      bs_n += L > t + 1 ? 1 : 0;
-      len_b = q == b ? L : len_b;
-    }
-    if (len_b <= t) continue;
+    const int32_t bs_t = rows_after(a, t);
+    if (b >= bs_t) continue;
+    const int32_t off_t = t * bs_t + total - a.lsum[bs_t];
+    const int32_t bs_p = t > 0 ? rows_after(a, t - 1) : 0;
+    const int32_t bs_n = t + 1 < a.T ? rows_after(a, t + 1) : 0;
+    const int32_t off_p = off_t - bs_p;  // offsets[t - 1]
     if (b == 0) {
       a.bs[t] = bs_t;
       a.off[t] = off_t;
@@ -377,7 +390,10 @@ hipError_t launch_prepare(const int32_t* lengths, int32_t B, int32_t T, const fl
                           int32_t nfill, unsigned value, unsigned* zero_word, hipStream_t st) {
   if (B < 0 || B > kPrepMaxB || nfill < 0 || nfill > kFillJobs) return hipErrorInvalidValue;
   PrepArgs a{};
-  for (int i = 0; i < B; ++i) a.len[i] = lengths[i];
+  for (int i = 0; i < B; ++i) {
+    a.len[i] = lengths[i];
+    a.lsum[i + 1] = a.lsum[i] + lengths[i];
+  }
   a.B = B;
   a.T = T;
   a.D = D;
