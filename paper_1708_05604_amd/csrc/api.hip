@@ -575,6 +575,9 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     }
   }
   unsigned* out_done = at<unsigned>(workspace, c.out_done);
+  // Set again below once this call has enqueued the fills: a call that
+  // fails part-way leaves no mark behind.
+  note_prefilled(reserve, false);
   bool prefilled = false;
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
