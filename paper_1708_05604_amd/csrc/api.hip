@@ -1218,7 +1218,7 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   RNNBKT_HIP(mark_join());
   RNNBKT_HIP(wait_join());
   // Weight gradients of every layer, reduced over every valid frame (unless
-  // they were streamed beside the recurrence).  The input and recurrent
+  // the recurrence launch computed them).  The input and recurrent
   // products of a layer read the same dA and are independent: the recurrent
   // ones run on the side stream (own split-K buffer), overlapping the other
   // stream's products and reductions.

@@ -380,7 +380,7 @@ def test_backward_repeated_without_forward(label, spec, lengths, env, monkeypatc
 ])
 def test_streamed_output_layer(label, spec, lengths, monkeypatch):
     """The output layer and loss computed beside the forward recurrence
-    (k_output_stream, blocks of 32 frames, grid-stride over more blocks than
+    (output-layer workgroups of the forward launch, blocks of 32 frames, more blocks than
     workgroups) match the oracle and the separate kernels run after it (to
     rounding: logits and loss are summed in another order)."""
     data = H.data_from_lengths(spec, lengths, seed=43, scale=0.3)
