@@ -146,6 +146,37 @@ def test_epoch_sgd_under_feeding_order(ordering):
         assert err < 1e-4
 
 
+def test_resume_at_epoch_boundary_is_exact(tmp_path):
+    """Checkpoint / resume: the epoch's shuffle is derived from (seed, epoch)
+    and every reduction runs in a fixed order, so two SGD epochs in a row equal
+    one epoch, the flat parameter vector saved to a file and loaded back, and
+    the second epoch -- bit for bit."""
+    w = synth.WORKLOADS["tiny"]
+    spec = H.Spec.of(w)
+    data = synth.make_workload(w, 0, param_count=orn.param_count(spec.model()))
+    _, bof, keff, _ = lib.bucket_plan(data.lengths, 2)
+    lr = 0.2
+
+    def epoch(params, e):
+        keys = synth.shuffle_keys(0, e, w.n)
+        cur = params
+        for order in lib.epoch_schedule(data.lengths, bof, keff, keys, w.batch):
+            gb = H.GpuBatch(spec, cur, data, order)
+            gb.run()
+            gb.sgd(lr)
+            cur = gb.params.cpu().numpy()
+        return cur
+
+    p0 = data.params.astype(np.float32)
+    straight = epoch(epoch(p0, 0), 1)
+    ckpt = tmp_path / "params_epoch1.npy"
+    np.save(ckpt, epoch(p0, 0))
+    resumed = epoch(np.load(ckpt), 1)
+    assert np.isfinite(straight).all()
+    assert np.array_equal(straight, resumed)
+    assert not np.array_equal(straight, p0)
+
+
 def test_sgd_apply_exact():
     import torch
     rng = np.random.default_rng(0)
