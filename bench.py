@@ -83,25 +83,26 @@ def flops_per_useful_step(w: synth.Workload) -> int:
     return total
 
 
-def describe(w: synth.Workload, K: int) -> str:
+def describe(w: synth.Workload, K: int, seed: int = 0) -> str:
     cell = {synth.LSTM: "LSTM", synth.GRU: "GRU", synth.LSTM_PEEPHOLE: "peephole LSTM"}[w.cell]
     bi = "bidirectional " if w.bidirectional else ""
     return (f"{w.name}: {w.num_layers}-layer {bi}{cell} D={w.input_dim} H={w.hidden} "
             f"C={w.num_classes}, {w.n} sequences {w.law}{w.law_args}, B={w.batch}, K={K}, "
-            f"{'bf16' if w.gemm_dtype == synth.BF16 else 'fp32'} GEMMs, seed 0")
+            f"{'bf16' if w.gemm_dtype == synth.BF16 else 'fp32'} GEMMs, seed {seed}")
 
 
 class Epoch:
     """One epoch's batches staged on the GPU."""
 
-    def __init__(self, w, data, K, epoch, torch, dev, targets=None, ordering="ascending"):
+    def __init__(self, w, data, K, epoch, torch, dev, targets=None, ordering="ascending",
+                 seed=0):
         t0 = time.perf_counter()
         self.upper, bof, self.keff, self.p_bucket = lib.bucket_plan(data.lengths, K)
         self.plan_ms = (time.perf_counter() - t0) * 1e3
         t0 = time.perf_counter()
         self.batches = lib.epoch_schedule(data.lengths, bof, self.keff,
-                                          synth.shuffle_keys(0, epoch, w.n), w.batch,
-                                          ordering, synth.order_keys(0, epoch, w.n))
+                                          synth.shuffle_keys(seed, epoch, w.n), w.batch,
+                                          ordering, synth.order_keys(seed, epoch, w.n))
         self.sched_ms = (time.perf_counter() - t0) * 1e3
         self.lens, self.x, self.y, self.useful = [], [], [], []
         self.p_batch = 0
@@ -287,6 +288,11 @@ def main(argv=None):
     ap.add_argument("--workload", default="lstm2", choices=list(synth.WORKLOADS))
     ap.add_argument("--K", type=int, default=0, help="buckets (0 = largest of the workload)")
     ap.add_argument("--lr", type=float, default=0.1, help="SGD step size")
+    ap.add_argument("--seed", type=int, default=0,
+                    help="seed of the synthetic workload (lengths, data, parameters, shuffles)")
+    ap.add_argument("--recurrence", default="resident", choices=("resident", "steps"),
+                    help="resident kernels (default) or one launch per step "
+                         "(the library's RNNBKT_RECURRENCE=steps)")
     ap.add_argument("--loss", default="frame", choices=("frame", "ctc"),
                     help="per-frame cross-entropy, or CTC over synthetic label strings "
                          "(one label per 8 frames)")
@@ -314,6 +320,8 @@ def main(argv=None):
               "its parallel scheme runs as concurrent replicas on the one GPU (--replicas).",
               file=sys.stderr)
         return 2
+    if args.recurrence == "steps":
+        os.environ["RNNBKT_RECURRENCE"] = "steps"  # read by the library at each call
 
     import torch
     dev = torch.device("cuda", 0)
@@ -324,7 +332,7 @@ def main(argv=None):
     desc = lib.ModelDesc.of(w.cell, w.num_layers, w.input_dim, w.hidden, w.num_classes,
                             w.bidirectional, w.gemm_dtype)
     P = lib.param_count(desc)
-    data = synth.make_workload(w, 0, param_count=P)
+    data = synth.make_workload(w, args.seed, param_count=P)
 
     if args.calibrate:
         nf = args.calibrate * (1 << 20) // 4
@@ -334,9 +342,11 @@ def main(argv=None):
         torch.cuda.synchronize()
         del cp, cg
 
-    targets = synth.ctc_targets(data.lengths, w.num_classes, 0) if args.loss == "ctc" else None
-    ep = Epoch(w, data, K, 0, torch, dev, targets, args.ordering)
-    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev, targets, args.ordering)
+    targets = (synth.ctc_targets(data.lengths, w.num_classes, args.seed) if args.loss == "ctc"
+               else None)
+    ep = Epoch(w, data, K, 0, torch, dev, targets, args.ordering, args.seed)
+    ep1 = None if args.no_k1 else Epoch(w, data, 1, 0, torch, dev, targets, args.ordering,
+                                        args.seed)
     eps = [e for e in (ep, ep1) if e is not None]
     rb, wb = lib.buffer_sizes(desc, max(e.max_T for e in eps), max(e.max_B for e in eps),
                               max(e.max_N for e in eps))
@@ -396,8 +406,9 @@ def main(argv=None):
         "warmup": warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if w.gemm_dtype == synth.BF16 else "f32", "data": "synthetic",
-        "config": {"workload": describe(w, K), "loss": args.loss, "optimizer": args.optimizer,
-                   "ordering": args.ordering,
+        "config": {"workload": describe(w, K, args.seed), "loss": args.loss,
+                   "optimizer": args.optimizer,
+                   "ordering": args.ordering, "recurrence": args.recurrence,
                    "batches_per_epoch": nb,
                    "useful_timesteps_per_epoch": ep.U,
                    "parallelism": "single GPU" if args.replicas == 1 else
