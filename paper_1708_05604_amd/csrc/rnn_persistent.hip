@@ -262,14 +262,26 @@ __device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
 }
 
 // Workgroups are dispatched to the 8 XCDs in turn (block b on XCD b mod 8),
-// each XCD with its own L2.  Renumbering so that consecutive logical ids
-// share an XCD keeps each unit's row groups, which exchange values every
-// step, on one XCD.
+// each XCD with its own L2.  The S workgroups of one (unit, row group)
+// cluster exchange values every step, so each cluster is kept on one XCD.
+// With a cluster count nc that is a multiple of 8, consecutive logical ids
+// share an XCD (nc / 8 whole clusters each: logical_block).  Otherwise the
+// GRU backward pads its grid to ceil(nc / 8) cluster places per XCD
+// (rec_grid, cluster_block): XCD x takes clusters x, x + 8, ..., and the
+// workgroups of the empty places exit at once (-1).  The forward keeps the
+// plain numbering: padded, gru2's 48-workgroup clusters put two workgroups on
+// half the CUs of an XCD and its step got slower (14.1 -> 18.4 us).
 constexpr int kXcds = 8;
 __device__ inline int logical_block(int n) {
   const int b = blockIdx.x;
   if (n % kXcds != 0) return b;
   return (b % kXcds) * (n / kXcds) + b / kXcds;
+}
+__device__ inline int cluster_block(int rec_blocks, int nc, int S) {
+  if (nc % kXcds == 0) return logical_block(rec_blocks);
+  const int b = blockIdx.x;
+  const int c = b % kXcds + kXcds * (b / kXcds / S);
+  return c < nc ? c * S + b / kXcds % S : -1;
 }
 
 // ---------------------------------------------------------------- output layer
@@ -876,7 +888,13 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     }
   }
   load_tables(a.bs, a.off, a.T, tbs, toff);
-  const int bid = logical_block(rec_blocks);
+  int bid;
+  if constexpr (G == 3) {
+    bid = cluster_block(rec_blocks, a.nunits * a.rgroups, a.slices);
+    if (bid < 0) return;
+  } else {
+    bid = logical_block(rec_blocks);
+  }
   int ui = 0;
   for (int q = 1; q < a.nunits; ++q)
     if (bid >= a.u[q].wg_begin) ui = q;
@@ -1173,6 +1191,11 @@ const void* fwd_kernel(int cell, bool bf16, int nt, int maxc) {
   return nt == 1 ? fwd_kernel_nt<3, false, 1>(maxc) : fwd_kernel_nt<3, false, 2>(maxc);
 }
 
+// Workgroups of a recurrence grid of nc clusters of S (see cluster_block).
+int rec_grid(int nc, int S) {
+  return nc % kXcds == 0 ? nc * S : kXcds * ((nc + kXcds - 1) / kXcds) * S;
+}
+
 struct FwdPlan {
   const void* kernel;
   int nt, maxc, blocks;
@@ -1240,7 +1263,8 @@ constexpr int bwd_maxc_cap(int nw, bool bf16) {
 
 template <int G, bool BF16, int NW, int M, bool SP>
 const void* bwd_kernel_m() {
-  if constexpr (M <= bwd_maxc_cap(NW, BF16) && (!SP || NW >= 8) && (SP || NW != 8))
+  if constexpr (M <= bwd_maxc_cap(NW, BF16) && (!SP || NW >= 8) && (SP || NW != 8) &&
+                (M != 5 || (NW == 16 && !SP)))
     return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, M, SP>);
   return nullptr;
 }
@@ -1252,6 +1276,7 @@ const void* bwd_kernel_nw(int maxc) {
     case 2: return bwd_kernel_m<G, BF16, NW, 2, SP>();
     case 3: return bwd_kernel_m<G, BF16, NW, 3, SP>();
     case 4: return bwd_kernel_m<G, BF16, NW, 4, SP>();
+    case 5: return bwd_kernel_m<G, BF16, NW, 5, SP>();
     case 8: return bwd_kernel_m<G, BF16, NW, 8, SP>();
     case 16: return bwd_kernel_m<G, BF16, NW, 16, SP>();
   }
@@ -1319,9 +1344,11 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     }
   }
   if (p.nw == 0) {
-    // Very wide layers: 16 polling waves with spilled registers.
-    int m = 1;
-    while (m < (nch + 15) / 16) m *= 2;
+    // Very wide layers: 16 polling waves with spilled registers (5 slots
+    // spill far less than 8, e.g. for 72 chunks).
+    const int per = (nch + 15) / 16;
+    int m = per == 5 ? 5 : 1;
+    while (m < per) m *= 2;
     if (m <= bwd_maxc_cap(16, bf16)) {
       p.nw = 16;
       p.maxc = m;
@@ -1329,7 +1356,8 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     }
   }
   if (p.nw == 0) return p;
-  p.blocks = a.nunits * (a.H / kBwdUnits) * ((B + 15) / 16);
+  const int nc = a.nunits * ((B + 15) / 16);
+  p.blocks = G == 3 ? rec_grid(nc, a.H / kBwdUnits) : nc * (a.H / kBwdUnits);
   p.shmem = sizeof(float) * std::max(p.nw, 8) * 256 + sizeof(int32_t) * (2 * a.T + 1);
   p.wg_blocks = 0;
   if (a.wg_on) {

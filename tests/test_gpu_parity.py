@@ -321,6 +321,19 @@ def test_workload_sampled_first_bucket(name, K):
     H.assert_batch_close(spec, data.params, data, order, label=f"{name} bucket 0")
 
 
+def test_gru_wide_layer_five_slots_padded_grid():
+    """GRU with H = 352: the backward's reduction over the 3H = 1056 gate
+    gradients is 66 chunks of 16, 5 per wave of 16 (the wide-layer variant),
+    and B = 40 is 3 row groups, so the backward grid is padded to whole
+    clusters per XCD with workgroups that exit at once."""
+    spec = H.Spec(1, 2, 0, 8, 352, 8)
+    rng = np.random.default_rng(37)
+    lengths = sorted(rng.integers(1, 24, 40).tolist(), reverse=True)
+    data = H.data_from_lengths(spec, lengths, seed=37, scale=0.3)
+    order = H.batch_order(data, range(40))
+    H.assert_batch_close(spec, data.params, data, order, label="GRU H=352 B=40")
+
+
 def test_sequence_longer_than_resident_limit():
     """T_max above the 6144 steps whose batch tables the resident kernels keep
     in LDS: the recurrences fall back to one launch per step."""
