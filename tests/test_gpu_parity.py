@@ -334,6 +334,19 @@ def test_gru_wide_layer_five_slots_padded_grid():
     H.assert_batch_close(spec, data.params, data, order, label="GRU H=352 B=40")
 
 
+def test_gru_forward_twelve_units_per_workgroup():
+    """fp32 GRU with H = 192 and B = 176 (11 row groups): 8 units per
+    workgroup would need more workgroups than the GPU has CUs, so the
+    forward takes 12 per workgroup on a grid padded to whole row-group
+    clusters per XCD."""
+    spec = H.Spec(1, 2, 0, 8, 192, 8)
+    rng = np.random.default_rng(43)
+    lengths = sorted(rng.integers(1, 21, 176).tolist(), reverse=True)
+    data = H.data_from_lengths(spec, lengths, seed=43, scale=0.3)
+    order = H.batch_order(data, range(176))
+    H.assert_batch_close(spec, data.params, data, order, label="GRU H=192 B=176")
+
+
 def test_sequence_longer_than_resident_limit():
     """T_max above the 6144 steps whose batch tables the resident kernels keep
     in LDS: the recurrences fall back to one launch per step."""
