@@ -268,8 +268,8 @@ __device__ inline FwdUnit pick_unit(const FwdLaunch& a, int ui) {
 // share an XCD (nc / 8 whole clusters each: logical_block).  Otherwise the
 // GRU backward pads its grid to ceil(nc / 8) cluster places per XCD
 // (rec_grid, cluster_block): XCD x takes clusters x, x + 8, ..., and the
-// workgroups of the empty places exit at once (-1), and so does the GRU
-// forward with 12 units per workgroup.  The 8-unit forward keeps the plain
+// workgroups of the empty places exit at once (-1), and so does the forward
+// with 12 or 16 units per workgroup.  The 8-unit forward keeps the plain
 // numbering: padded, gru2's 48-workgroup clusters put two workgroups on half
 // the CUs of an XCD and its step got slower (14.1 -> 18.4 us).
 constexpr int kXcds = 8;
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   }
   load_tables(a.bs, a.off, a.T, tbs, toff);
   int bid;
-  if constexpr (NT == 3) {
+  if constexpr (NT >= 3) {
     bid = cluster_block(rec_blocks, a.nunits * a.rgroups, a.slices);
     if (bid < 0) return;
   } else {
@@ -1192,10 +1192,11 @@ const void* fwd_kernel_nt(int maxc) {
 const void* fwd_kernel(int cell, bool bf16, int nt, int maxc) {
   if (cell == RNNBKT_CELL_LSTM) {
     if (nt == 3) return nullptr;
+    if (nt == 4) return bf16 ? fwd_kernel_nt<4, true, 4>(maxc) : nullptr;
     if (bf16) return nt == 1 ? fwd_kernel_nt<4, true, 1>(maxc) : fwd_kernel_nt<4, true, 2>(maxc);
     return nt == 1 ? fwd_kernel_nt<4, false, 1>(maxc) : fwd_kernel_nt<4, false, 2>(maxc);
   }
-  if (nt == 3) return bf16 ? nullptr : fwd_kernel_nt<3, false, 3>(maxc);
+  if (nt >= 3) return bf16 || nt == 4 ? nullptr : fwd_kernel_nt<3, false, 3>(maxc);
   if (bf16) return nt == 1 ? fwd_kernel_nt<3, true, 1>(maxc) : fwd_kernel_nt<3, true, 2>(maxc);
   return nt == 1 ? fwd_kernel_nt<3, false, 1>(maxc) : fwd_kernel_nt<3, false, 2>(maxc);
 }
@@ -1213,9 +1214,10 @@ struct FwdPlan {
 
 // Column blocks per workgroup: 2 (8 units) for wide layers, else 1 (4 units).
 // An fp32 GRU whose 8-unit grid has more workgroups than the GPU has CUs
-// takes 3 (12 units) when H allows: each workgroup then has a CU of its own
-// (gru2: 192 workgroups instead of 288, 32 of them sharing a CU), and its
-// row-group clusters of 32 are kept whole on one XCD (rec_grid).
+// takes 3 (12 units) when H allows, a bf16 LSTM 4 (16 units): each
+// workgroup then has a CU of its own (gru2: 192 workgroups instead of 288,
+// 32 of them sharing a CU), and the row-group clusters are kept whole on
+// one XCD (rec_grid).
 FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
   FwdPlan p{nullptr, 0, 0, 0, 0};
   const int ch = bf16 ? 32 : 16;
@@ -1239,16 +1241,18 @@ FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
     p.shmem = std::max(p.shmem, out_lds);
   }
   p.kernel = fwd_kernel(cell, bf16, p.nt, p.maxc);
-  if (cell == RNNBKT_CELL_GRU && !bf16 && p.nt == 2 && a.H % 12 == 0 && p.blocks > cu_count()) {
-    const void* k3 = fwd_kernel(cell, bf16, 3, p.maxc);
-    const int b3 = rec_grid(a.nunits * ((B + 15) / 16), a.H / 12) + a.out_blocks;
-    const size_t sh3 =
-        std::max(sizeof(float) * 4 * 3 * 256 + sizeof(int32_t) * (2 * a.T + 1), out_lds);
-    if (k3 && b3 <= max_coresident(k3, 256, sh3)) {
-      p.nt = 3;
-      p.blocks = b3;
-      p.shmem = sh3;
-      p.kernel = k3;
+  // Wider workgroups: 12 units for an fp32 GRU, 16 for a bf16 LSTM.
+  const int wide = cell == RNNBKT_CELL_GRU ? (bf16 ? 0 : 3) : (bf16 ? 4 : 0);
+  if (wide > 0 && p.nt == 2 && a.H % (4 * wide) == 0 && p.blocks > cu_count()) {
+    const void* kw = fwd_kernel(cell, bf16, wide, p.maxc);
+    const int bw = rec_grid(a.nunits * ((B + 15) / 16), a.H / (4 * wide)) + a.out_blocks;
+    const size_t shw =
+        std::max(sizeof(float) * 4 * wide * 256 + sizeof(int32_t) * (2 * a.T + 1), out_lds);
+    if (kw && bw <= max_coresident(kw, 256, shw)) {
+      p.nt = wide;
+      p.blocks = bw;
+      p.shmem = shw;
+      p.kernel = kw;
     }
   }
   return p;

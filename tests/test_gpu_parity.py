@@ -347,6 +347,21 @@ def test_gru_forward_twelve_units_per_workgroup():
     H.assert_batch_close(spec, data.params, data, order, label="GRU H=192 B=176")
 
 
+def test_bf16_lstm_forward_sixteen_units_per_workgroup():
+    """bf16 LSTM with H = 256 and B = 80 (5 row groups): the two layers with
+    8 units per workgroup would need more workgroups than the GPU has CUs,
+    so the forward takes 16 per workgroup on a padded grid.  Weights at the
+    workloads' scale (U(-0.1, 0.1)): at 0.3 a 256-wide recurrence amplifies
+    the bf16 operand rounding past the bound with 8 units per workgroup too
+    (identical results)."""
+    spec = H.Spec(0, 2, 0, 8, 256, 8, synth.BF16)
+    rng = np.random.default_rng(47)
+    lengths = sorted(rng.integers(1, 15, 80).tolist(), reverse=True)
+    data = H.data_from_lengths(spec, lengths, seed=47, scale=0.1)
+    order = H.batch_order(data, range(80))
+    H.assert_batch_close(spec, data.params, data, order, label="bf16 LSTM H=256 B=80")
+
+
 def test_sequence_longer_than_resident_limit():
     """T_max above the 6144 steps whose batch tables the resident kernels keep
     in LDS: the recurrences fall back to one launch per step."""
