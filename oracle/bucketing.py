@@ -8,16 +8,20 @@ bucket's upper length, so the padded work is sum_b upper_b * count_b
 (eq. 2 with the per-bucket cost of eq. 1; the DP's score).  The DP runs over
 the length histogram f, where f[l] counts the sequences of length l.
 
-Readings of the garbled text, applied here:
-  * f is indexed by length, f[0] = 0, and the DP's index i runs over lengths
-    1..Lmax; the answer is dp[Q][Lmax] (the pseudo-code's "n <- length(f)"
-    and "curId <- n-1" only agree with this indexing).
-  * dp[q][i] = min over 0 <= j < i of dp[q-1][j] + i * sum_{t=j+1..i} f[t];
-    dp[0][0] = 0, every other entry starts at INF, and INF predecessors are
-    skipped (the notation list's dp[i][k] is the transposed name of the same
-    table, and its summation bounds are garbled).
-  * ties: j runs downwards and only a strictly smaller value replaces the
-    incumbent, so the largest minimising j wins.
+How the printed text is read here (it is garbled in places):
+  * The histogram is indexed by the length itself, with an empty entry for
+    length 0, so the table's column i stands for "all sequences of length at
+    most i" and the optimum sits in column Lmax; the procedure's bound on i
+    and its starting point for the walk back are consistent only with this.
+  * cost[q][i] = min over 0 <= j < i of cost[q-1][j] + i * (F[i] - F[j]), with
+    F the inclusive prefix sum of f: the top range (j, i] of a q-range cover
+    holds F[i] - F[j] sequences, each padded to i.  Only cost[0][0] = 0 is
+    finite in row 0; unreachable predecessors are skipped.  (The notation
+    list transposes the table's indices and garbles the summation bounds;
+    the procedure's arithmetic is what is followed.)
+  * Ties: the procedure scans split points downwards and only a strictly
+    smaller score replaces the incumbent, so among equal minima the largest
+    split point is kept.
   * Q larger than the number of distinct lengths D is clamped to D (every
     extra bucket would be empty); the clamped count is returned.
 """
@@ -36,61 +40,31 @@ def length_histogram(lengths) -> np.ndarray:
     return np.bincount(lengths, minlength=int(lengths.max()) + 1).astype(np.int64)
 
 
-def dynamic_bucketing_loops(Q: int, f: np.ndarray):
-    """The DYNAMICBUCKETING procedure written as plain loops, in the paper's
-    order (q outer, i middle, j descending inner, running sum of f).
-    Returns (bests, dp_value).  O(Q * Lmax^2) Python steps: small inputs only."""
-    Lmax = len(f) - 1
-    dp = [[INF] * (Lmax + 1) for _ in range(Q + 1)]
-    prev = [[-1] * (Lmax + 1) for _ in range(Q + 1)]
-    dp[0][0] = 0
-    for q in range(1, Q + 1):
-        for i in range(1, Lmax + 1):
-            cur = int(f[i])
-            for j in range(i - 1, -1, -1):
-                if dp[q - 1][j] != INF:
-                    val = cur * i + dp[q - 1][j]
-                    if val < dp[q][i]:
-                        dp[q][i] = val
-                        prev[q][i] = j
-                cur += int(f[j])
-    bests = []
-    cur_id = Lmax
-    for q in range(Q, 0, -1):
-        bests.insert(0, cur_id)
-        cur_id = prev[q][cur_id]
-    return bests, dp[Q][Lmax]
-
-
 def dynamic_bucketing(Q: int, f: np.ndarray):
-    """Same DP as ``dynamic_bucketing_loops``; the inner j loop is evaluated as
-    one vector expression.  The running sum of the j loop equals
-    F[i] - F[j] with F the inclusive prefix sum of f, and "largest j among the
-    minima" is the first minimum when j is scanned downwards.
-    Returns (bests, dp_value)."""
+    """The recurrence above over every length 0..Lmax.  Row q of the table
+    is filled from row q-1: for each end point i all split points j < i are
+    scored at once, and the largest j reaching the minimum is recorded.
+    Returns (bests, optimum): bests[b] is the upper length of bucket b, read
+    back from column Lmax through the recorded split points."""
     Lmax = len(f) - 1
     F = np.cumsum(f).astype(np.int64)           # F[x] = sum_{t<=x} f[t]
-    dp = np.full((Q + 1, Lmax + 1), INF, np.int64)
-    prev = np.full((Q + 1, Lmax + 1), -1, np.int64)
-    dp[0, 0] = 0
+    cost = np.full((Q + 1, Lmax + 1), INF, np.int64)
+    split = np.full((Q + 1, Lmax + 1), -1, np.int64)
+    cost[0, 0] = 0
     for q in range(1, Q + 1):
+        below = cost[q - 1]
         for i in range(1, Lmax + 1):
-            js = np.arange(i - 1, -1, -1)        # j = i-1 down to 0
-            base = dp[q - 1, js]
-            ok = base != INF
-            if not ok.any():
+            reach = below[:i] != INF            # split points j = 0..i-1
+            if not reach.any():
                 continue
-            val = np.where(ok, (F[i] - F[js]) * i + np.where(ok, base, 0), INF)
-            k = int(np.argmin(val))              # first minimum = largest j
-            if val[k] < dp[q, i]:
-                dp[q, i] = val[k]
-                prev[q, i] = js[k]
-    bests = []
-    cur_id = Lmax
-    for q in range(Q, 0, -1):
-        bests.insert(0, int(cur_id))
-        cur_id = prev[q, cur_id]
-    return bests, int(dp[Q, Lmax])
+            score = np.where(reach, np.where(reach, below[:i], 0) + i * (F[i] - F[:i]), INF)
+            best = score.min()
+            cost[q, i] = best
+            split[q, i] = np.flatnonzero(score == best)[-1]
+    bests = [Lmax]
+    for q in range(Q, 1, -1):
+        bests.append(int(split[q, bests[-1]]))
+    return bests[::-1], int(cost[Q, Lmax])
 
 
 def bucket_plan(lengths, K: int):

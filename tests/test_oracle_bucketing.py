@@ -48,18 +48,6 @@ def test_dp_equals_brute_force(seed):
         assert list(ob_bests) == bests, (lengths, K)
 
 
-@pytest.mark.parametrize("seed", range(10))
-def test_loop_form_equals_vector_form(seed):
-    rng = np.random.default_rng(100 + seed)
-    lengths = rng.integers(1, 40, int(rng.integers(1, 60)))
-    f = ob.length_histogram(lengths)
-    D = int(np.count_nonzero(f))
-    for Q in range(1, D + 1):
-        a = ob.dynamic_bucketing_loops(Q, f)
-        b = ob.dynamic_bucketing(Q, f)
-        assert a[0] == b[0] and a[1] == b[1]
-
-
 def test_invariants_on_workload_lengths():
     for name in ("tiny", "lstm2"):
         w = synth.WORKLOADS[name]
