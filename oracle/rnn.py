@@ -165,8 +165,6 @@ def lstm_dir_backward(W_ih, W_hh, X, cache, dH, d, peep=None):
     dA = np.zeros((L, 4 * H))
     dh_rec = np.zeros(H)      # gradient reaching h_t through the next step's W_hh
     dc_rec = np.zeros(H)      # gradient reaching c_t through the next step's gates
-    dW_hh = np.zeros_like(W_hh)
-    dp = np.zeros((3, H))
     for t in reversed(list(_time_order(L, d))):
         i, f, g, o = cache["i"][t], cache["f"][t], cache["g"][t], cache["o"][t]
         c, c_prev, h_prev = cache["c"][t], cache["c_prev"][t], cache["h_prev"][t]
@@ -181,15 +179,20 @@ def lstm_dir_backward(W_ih, W_hh, X, cache, dH, d, peep=None):
         da_g = dc * i * (1.0 - g * g)        # cell candidate
         da = np.concatenate([da_i, da_f, da_g, da_o])
         dA[t] = da
-        dW_hh += np.outer(da, h_prev)
-        dp += np.stack([da_i * c_prev, da_f * c_prev, da_o * c])
         dh_rec = W_hh.T @ da
         # c_{t-1} reaches the loss through the forget path and the two peepholes
         dc_rec = dc * f + da_i * p_i + da_f * p_f
+    # Sums over the steps, each written as one product over the stored steps:
+    # dW_hh = sum_t da_t h_{t-1}^T, dW_ih = sum_t da_t x_t^T, and the
+    # peephole gradients sum_t da_i c_{t-1}, da_f c_{t-1}, da_o c_t.
+    dW_hh = dA.T @ cache["h_prev"]
     dW_ih = dA.T @ X
     db = dA.sum(axis=0)
     dX = dA @ W_ih
-    return dW_ih, dW_hh, db, dX, dp.reshape(-1)
+    dp = np.concatenate([(dA[:, 0:H] * cache["c_prev"]).sum(axis=0),
+                         (dA[:, H:2 * H] * cache["c_prev"]).sum(axis=0),
+                         (dA[:, 3 * H:4 * H] * cache["c"]).sum(axis=0)])
+    return dW_ih, dW_hh, db, dX, dp
 
 
 def gru_dir_forward(W_ih, W_hh, b_ih, b_hh, X, d):
@@ -219,7 +222,6 @@ def gru_dir_backward(W_ih, W_hh, X, cache, dH, d):
     dAx = np.zeros((L, 3 * H))   # gradient of the input pre-activations
     dAh = np.zeros((L, 3 * H))   # gradient of W_hh h + b_hh
     dh_rec = np.zeros(H)
-    dW_hh = np.zeros_like(W_hh)
     for t in reversed(list(_time_order(L, d))):
         r, z, n = cache["r"][t], cache["z"][t], cache["n"][t]
         ahn, h_prev = cache["ahn"][t], cache["h_prev"][t]
@@ -231,8 +233,8 @@ def gru_dir_backward(W_ih, W_hh, X, cache, dH, d):
         daz = dz * z * (1.0 - z)
         dAx[t] = np.concatenate([dar, daz, dan])
         dAh[t] = np.concatenate([dar, daz, dan * r])
-        dW_hh += np.outer(dAh[t], h_prev)
         dh_rec = W_hh.T @ dAh[t] + dh * z
+    dW_hh = dAh.T @ cache["h_prev"]        # sum_t dAh_t h_{t-1}^T
     dW_ih = dAx.T @ X
     return dW_ih, dW_hh, dAx.sum(axis=0), dAh.sum(axis=0), dAx @ W_ih
 
