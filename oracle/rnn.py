@@ -29,7 +29,10 @@ next layer (and the output layer) reads that concatenation.
 Output: z_t = W_out h_t + b_out over the top layer, log-softmax, and the loss
 is the mean over all valid frames of the batch of -log p_t[y_t] (the paper's
 CTC loss is replaced by per-frame cross-entropy with one label per frame).
-Pad frames do not exist here: every sequence is processed at its own length.
+The sequences of a batch run side by side, each over its own length: at
+step k every sequence longer than k advances one frame (frame k, or its
+frame L - 1 - k in the reverse direction) from its own state.  Frames past
+a sequence's length are padding that takes no part in anything.
 
 Flat parameter layout (float32 on the wire, float64 inside), row-major:
   for each layer, for each direction (forward first):
@@ -121,122 +124,143 @@ def _sig(x):
     return 1.0 / (1.0 + np.exp(-x))
 
 
-def _time_order(L: int, d: int):
-    return range(L) if d == 0 else range(L - 1, -1, -1)
+def _steps(lengths, d: int):
+    """The recurrence's steps over a batch of sequences run side by side:
+    at step k (k = 0 .. max length - 1) every sequence still running
+    (k < L_b) advances by one frame -- frame k forward, frame L_b - 1 - k in
+    the reverse direction.  Yields (rows, frames) per step."""
+    lengths = np.asarray(lengths)
+    for k in range(int(lengths.max())):
+        rows = np.nonzero(lengths > k)[0]
+        yield rows, (np.full(rows.size, k) if d == 0 else lengths[rows] - 1 - k)
 
 
-def lstm_dir_forward(W_ih, W_hh, b, X, d, peep=None):
-    """One direction of one LSTM layer over one sequence X [L, D_in];
-    `peep` = [p_i ; p_f ; p_o] (3H) for the peephole cell, else None.
-    Returns (Hseq [L, H], cache)."""
-    L = X.shape[0]
+def valid_mask(lengths, T: int) -> np.ndarray:
+    """[B, T] booleans: frame t of sequence b exists (t < L_b)."""
+    return np.arange(T)[None, :] < np.asarray(lengths)[:, None]
+
+
+def lstm_dir_forward(W_ih, W_hh, b, X, lengths, d, peep=None):
+    """One direction of one LSTM layer over a batch of sequences given as a
+    padded array X [B, T, D_in] (frames t >= L_b are never used) with
+    lengths [B]; every sequence runs its own recurrence from a zero state
+    (see _steps).  `peep` = [p_i ; p_f ; p_o] (3H) for the peephole cell,
+    else None.  Returns (Hseq [B, T, H] with zero pad frames, cache)."""
+    B, T = X.shape[0], X.shape[1]
     H = W_hh.shape[1]
     p_i, p_f, p_o = (np.zeros(H),) * 3 if peep is None else np.reshape(peep, (3, H))
-    ax = X @ W_ih.T + b                           # input part of a_t, all t
-    Hs = np.zeros((L, H))
-    cache = {"i": np.zeros((L, H)), "f": np.zeros((L, H)), "g": np.zeros((L, H)),
-             "o": np.zeros((L, H)), "c": np.zeros((L, H)), "c_prev": np.zeros((L, H)),
-             "h_prev": np.zeros((L, H))}
-    h = np.zeros(H)
-    c = np.zeros(H)
-    for t in _time_order(L, d):
-        a = ax[t] + W_hh @ h
-        i = _sig(a[0:H] + p_i * c)
-        f = _sig(a[H:2 * H] + p_f * c)
-        g = np.tanh(a[2 * H:3 * H])
-        cache["h_prev"][t] = h
-        cache["c_prev"][t] = c
-        c = f * c + i * g
-        o = _sig(a[3 * H:4 * H] + p_o * c)
-        h = o * np.tanh(c)
-        Hs[t] = h
-        for k, v in (("i", i), ("f", f), ("g", g), ("o", o), ("c", c)):
-            cache[k][t] = v
+    Hs = np.zeros((B, T, H))
+    cache = {k: np.zeros((B, T, H)) for k in ("i", "f", "g", "o", "c", "c_prev", "h_prev")}
+    h = np.zeros((B, H))
+    c = np.zeros((B, H))
+    for rows, fr in _steps(lengths, d):
+        a = X[rows, fr] @ W_ih.T + b + h[rows] @ W_hh.T
+        cp = c[rows]
+        i = _sig(a[:, 0:H] + p_i * cp)
+        f = _sig(a[:, H:2 * H] + p_f * cp)
+        g = np.tanh(a[:, 2 * H:3 * H])
+        cache["h_prev"][rows, fr] = h[rows]
+        cache["c_prev"][rows, fr] = cp
+        cn = f * cp + i * g
+        o = _sig(a[:, 3 * H:4 * H] + p_o * cn)
+        hn = o * np.tanh(cn)
+        c[rows] = cn
+        h[rows] = hn
+        Hs[rows, fr] = hn
+        for k, v in (("i", i), ("f", f), ("g", g), ("o", o), ("c", cn)):
+            cache[k][rows, fr] = v
     return Hs, cache
 
 
-def lstm_dir_backward(W_ih, W_hh, X, cache, dH, d, peep=None):
-    """Reverse-mode pass of ``lstm_dir_forward`` given dLoss/dh_t = dH [L, H].
-    Returns (dW_ih, dW_hh, db, dX, dpeep); dpeep (3H) is zero without
-    peepholes."""
-    L = X.shape[0]
+def lstm_dir_backward(W_ih, W_hh, X, lengths, cache, dH, d, peep=None):
+    """Reverse-mode pass of ``lstm_dir_forward`` given dLoss/dh = dH
+    [B, T, H] (zero on pad frames).  Returns (dW_ih, dW_hh, db, dX
+    [B, T, D_in], dpeep); dpeep (3H) is zero without peepholes."""
+    B, T = X.shape[0], X.shape[1]
     H = W_hh.shape[1]
     p_i, p_f, p_o = (np.zeros(H),) * 3 if peep is None else np.reshape(peep, (3, H))
-    dA = np.zeros((L, 4 * H))
-    dh_rec = np.zeros(H)      # gradient reaching h_t through the next step's W_hh
-    dc_rec = np.zeros(H)      # gradient reaching c_t through the next step's gates
-    for t in reversed(list(_time_order(L, d))):
-        i, f, g, o = cache["i"][t], cache["f"][t], cache["g"][t], cache["o"][t]
-        c, c_prev, h_prev = cache["c"][t], cache["c_prev"][t], cache["h_prev"][t]
-        dh = dH[t] + dh_rec
+    dA = np.zeros((B, T, 4 * H))
+    dh_rec = np.zeros((B, H))  # gradient reaching h_t through the next step's W_hh
+    dc_rec = np.zeros((B, H))  # gradient reaching c_t through the next step's gates
+    for rows, fr in reversed(list(_steps(lengths, d))):
+        i, f, g, o = (cache[k][rows, fr] for k in ("i", "f", "g", "o"))
+        c, c_prev = cache["c"][rows, fr], cache["c_prev"][rows, fr]
+        dh = dH[rows, fr] + dh_rec[rows]
         tc = np.tanh(c)
         da_o = dh * tc * o * (1.0 - o)       # output gate
         # c_t reaches the loss through h_t, the output gate's peephole and
         # (dc_rec) the next step
-        dc = dh * o * (1.0 - tc * tc) + da_o * p_o + dc_rec
+        dc = dh * o * (1.0 - tc * tc) + da_o * p_o + dc_rec[rows]
         da_i = dc * g * i * (1.0 - i)        # input gate
         da_f = dc * c_prev * f * (1.0 - f)   # forget gate
         da_g = dc * i * (1.0 - g * g)        # cell candidate
-        da = np.concatenate([da_i, da_f, da_g, da_o])
-        dA[t] = da
-        dh_rec = W_hh.T @ da
+        da = np.concatenate([da_i, da_f, da_g, da_o], axis=1)
+        dA[rows, fr] = da
+        dh_rec[rows] = da @ W_hh
         # c_{t-1} reaches the loss through the forget path and the two peepholes
-        dc_rec = dc * f + da_i * p_i + da_f * p_f
-    # Sums over the steps, each written as one product over the stored steps:
-    # dW_hh = sum_t da_t h_{t-1}^T, dW_ih = sum_t da_t x_t^T, and the
-    # peephole gradients sum_t da_i c_{t-1}, da_f c_{t-1}, da_o c_t.
-    dW_hh = dA.T @ cache["h_prev"]
-    dW_ih = dA.T @ X
-    db = dA.sum(axis=0)
+        dc_rec[rows] = dc * f + da_i * p_i + da_f * p_f
+    # Sums over every valid frame, each written as one product:
+    # dW_hh = sum da_t h_{t-1}^T, dW_ih = sum da_t x_t^T, and the peephole
+    # gradients sum da_i c_{t-1}, da_f c_{t-1}, da_o c_t.
+    M = valid_mask(lengths, T)
+    dAv = dA[M]
+    dW_hh = dAv.T @ cache["h_prev"][M]
+    dW_ih = dAv.T @ X[M]
+    db = dAv.sum(axis=0)
     dX = dA @ W_ih
-    dp = np.concatenate([(dA[:, 0:H] * cache["c_prev"]).sum(axis=0),
-                         (dA[:, H:2 * H] * cache["c_prev"]).sum(axis=0),
-                         (dA[:, 3 * H:4 * H] * cache["c"]).sum(axis=0)])
+    dp = np.concatenate([(dAv[:, 0:H] * cache["c_prev"][M]).sum(axis=0),
+                         (dAv[:, H:2 * H] * cache["c_prev"][M]).sum(axis=0),
+                         (dAv[:, 3 * H:4 * H] * cache["c"][M]).sum(axis=0)])
     return dW_ih, dW_hh, db, dX, dp
 
 
-def gru_dir_forward(W_ih, W_hh, b_ih, b_hh, X, d):
-    L = X.shape[0]
+def gru_dir_forward(W_ih, W_hh, b_ih, b_hh, X, lengths, d):
+    """As lstm_dir_forward for the GRU cell."""
+    B, T = X.shape[0], X.shape[1]
     H = W_hh.shape[1]
-    ax = X @ W_ih.T + b_ih
-    Hs = np.zeros((L, H))
-    cache = {k: np.zeros((L, H)) for k in ("r", "z", "n", "ahn", "h_prev")}
-    h = np.zeros(H)
-    for t in _time_order(L, d):
-        ah = W_hh @ h + b_hh
-        r = _sig(ax[t, 0:H] + ah[0:H])
-        z = _sig(ax[t, H:2 * H] + ah[H:2 * H])
-        n = np.tanh(ax[t, 2 * H:3 * H] + r * ah[2 * H:3 * H])
-        cache["h_prev"][t] = h
-        h = (1.0 - z) * n + z * h
-        Hs[t] = h
-        for k, v in (("r", r), ("z", z), ("n", n), ("ahn", ah[2 * H:3 * H])):
-            cache[k][t] = v
+    Hs = np.zeros((B, T, H))
+    cache = {k: np.zeros((B, T, H)) for k in ("r", "z", "n", "ahn", "h_prev")}
+    h = np.zeros((B, H))
+    for rows, fr in _steps(lengths, d):
+        hp = h[rows]
+        ax = X[rows, fr] @ W_ih.T + b_ih
+        ah = hp @ W_hh.T + b_hh
+        r = _sig(ax[:, 0:H] + ah[:, 0:H])
+        z = _sig(ax[:, H:2 * H] + ah[:, H:2 * H])
+        n = np.tanh(ax[:, 2 * H:3 * H] + r * ah[:, 2 * H:3 * H])
+        cache["h_prev"][rows, fr] = hp
+        hn = (1.0 - z) * n + z * hp
+        h[rows] = hn
+        Hs[rows, fr] = hn
+        for k, v in (("r", r), ("z", z), ("n", n), ("ahn", ah[:, 2 * H:3 * H])):
+            cache[k][rows, fr] = v
     return Hs, cache
 
 
-def gru_dir_backward(W_ih, W_hh, X, cache, dH, d):
-    """Returns (dW_ih, dW_hh, db_ih, db_hh, dX)."""
-    L = X.shape[0]
+def gru_dir_backward(W_ih, W_hh, X, lengths, cache, dH, d):
+    """Returns (dW_ih, dW_hh, db_ih, db_hh, dX [B, T, D_in])."""
+    B, T = X.shape[0], X.shape[1]
     H = W_hh.shape[1]
-    dAx = np.zeros((L, 3 * H))   # gradient of the input pre-activations
-    dAh = np.zeros((L, 3 * H))   # gradient of W_hh h + b_hh
-    dh_rec = np.zeros(H)
-    for t in reversed(list(_time_order(L, d))):
-        r, z, n = cache["r"][t], cache["z"][t], cache["n"][t]
-        ahn, h_prev = cache["ahn"][t], cache["h_prev"][t]
-        dh = dH[t] + dh_rec
+    dAx = np.zeros((B, T, 3 * H))   # gradient of the input pre-activations
+    dAh = np.zeros((B, T, 3 * H))   # gradient of W_hh h + b_hh
+    dh_rec = np.zeros((B, H))
+    for rows, fr in reversed(list(_steps(lengths, d))):
+        r, z, n = cache["r"][rows, fr], cache["z"][rows, fr], cache["n"][rows, fr]
+        ahn, h_prev = cache["ahn"][rows, fr], cache["h_prev"][rows, fr]
+        dh = dH[rows, fr] + dh_rec[rows]
         dn = dh * (1.0 - z)
         dz = dh * (h_prev - n)
         dan = dn * (1.0 - n * n)
         dar = dan * ahn * r * (1.0 - r)
         daz = dz * z * (1.0 - z)
-        dAx[t] = np.concatenate([dar, daz, dan])
-        dAh[t] = np.concatenate([dar, daz, dan * r])
-        dh_rec = W_hh.T @ dAh[t] + dh * z
-    dW_hh = dAh.T @ cache["h_prev"]        # sum_t dAh_t h_{t-1}^T
-    dW_ih = dAx.T @ X
-    return dW_ih, dW_hh, dAx.sum(axis=0), dAh.sum(axis=0), dAx @ W_ih
+        dAx[rows, fr] = np.concatenate([dar, daz, dan], axis=1)
+        dah = np.concatenate([dar, daz, dan * r], axis=1)
+        dAh[rows, fr] = dah
+        dh_rec[rows] = dah @ W_hh + dh * z
+    M = valid_mask(lengths, T)
+    dW_hh = dAh[M].T @ cache["h_prev"][M]        # sum dAh_t h_{t-1}^T
+    dW_ih = dAx[M].T @ X[M]
+    return dW_ih, dW_hh, dAx[M].sum(axis=0), dAh[M].sum(axis=0), dAx @ W_ih
 
 
 def log_softmax(z):
@@ -247,8 +271,10 @@ def log_softmax(z):
 def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True, ctc_targets=None):
     """Loss and flat gradient for one mini-batch given as lists of per-sequence
     features [L_s, D] and labels [L_s].  Returns (loss, grad or None, outputs)
-    where outputs holds the per-sequence top-layer activations.
+    where outputs holds the per-sequence top-layer activations [L_s, H_top].
 
+    The sequences run side by side, each over its own length (see _steps);
+    frames past a sequence's length take no part in anything.
     Per-frame loss: the mean over the batch's valid frames of the softmax
     cross-entropy of the frame's label.  With ctc_targets (one label string
     per sequence, classes 1..C-1; seqs_y is then not used): the mean over
@@ -256,74 +282,80 @@ def forward_backward(m: Model, theta, seqs_x, seqs_y, need_grad=True, ctc_target
     from oracle import ctc
     p = unpack(m, theta)
     n_seq = len(seqs_x)
-    G, H, dirs = m.gates, m.hidden, m.dirs
-    n_valid = sum(int(len(y)) for y in seqs_y)
+    H, dirs = m.hidden, m.dirs
+    lengths = np.array([len(x) for x in seqs_x], np.int64)
+    if n_seq == 0 or lengths.min() < 1:
+        raise ValueError("every sequence needs at least one frame")
+    T = int(lengths.max())
+    X0 = np.zeros((n_seq, T, m.input_dim))
+    for b, x in enumerate(seqs_x):
+        X0[b, :lengths[b]] = np.asarray(x, np.float64)
+    M = valid_mask(lengths, T)
+    n_valid = int(lengths.sum())
     grads = {k: np.zeros_like(v) for k, v in p.items()}
-    loss = 0.0
-    tops = []
-    for X0, Y in zip(seqs_x, seqs_y):
-        X0 = np.asarray(X0, np.float64)
-        Y = np.asarray(Y, np.int64)
-        L = X0.shape[0]
-        inputs, caches = [X0], []
-        for l in range(m.num_layers):
-            outs = []
-            for d in range(dirs):
-                if m.is_lstm:
-                    Hs, cache = lstm_dir_forward(p[("W_ih", l, d)], p[("W_hh", l, d)],
-                                                 p[("b", l, d)], inputs[-1], d,
-                                                 p.get(("p", l, d)))
-                else:
-                    Hs, cache = gru_dir_forward(p[("W_ih", l, d)], p[("W_hh", l, d)],
-                                                p[("b_ih", l, d)], p[("b_hh", l, d)],
-                                                inputs[-1], d)
-                outs.append(Hs)
-                caches.append(cache)
-            inputs.append(np.concatenate(outs, axis=1))
-        top = inputs[-1]
-        tops.append(top)
-        z = top @ p[("W_out", 0, 0)].T + p[("b_out", 0, 0)]
-        if ctc_targets is not None:
-            lc, gc = ctc.ctc_loss_grad(z, ctc_targets[len(tops) - 1])
+    inputs, caches = [X0], []
+    for l in range(m.num_layers):
+        outs = []
+        for d in range(dirs):
+            if m.is_lstm:
+                Hs, cache = lstm_dir_forward(p[("W_ih", l, d)], p[("W_hh", l, d)],
+                                             p[("b", l, d)], inputs[-1], lengths, d,
+                                             p.get(("p", l, d)))
+            else:
+                Hs, cache = gru_dir_forward(p[("W_ih", l, d)], p[("W_hh", l, d)],
+                                            p[("b_ih", l, d)], p[("b_hh", l, d)],
+                                            inputs[-1], lengths, d)
+            outs.append(Hs)
+            caches.append(cache)
+        inputs.append(np.concatenate(outs, axis=2))
+    top = inputs[-1]
+    tops = [top[b, :lengths[b]] for b in range(n_seq)]
+    z = top @ p[("W_out", 0, 0)].T + p[("b_out", 0, 0)]       # [B, T, C]
+    dz = np.zeros_like(z)
+    if ctc_targets is not None:
+        loss = 0.0
+        for b in range(n_seq):
+            lc, gc = ctc.ctc_loss_grad(z[b, :lengths[b]], ctc_targets[b])
             loss += lc / n_seq
-            if not need_grad:
-                continue
-            dz = gc / n_seq
-        else:
-            logp = log_softmax(z)
-            loss -= logp[np.arange(L), Y].sum() / n_valid
-            if not need_grad:
-                continue
-            dz = np.exp(logp)
-            dz[np.arange(L), Y] -= 1.0
-            dz /= n_valid
-        grads[("W_out", 0, 0)] += dz.T @ top
-        grads[("b_out", 0, 0)] += dz.sum(axis=0)
-        dIn = dz @ p[("W_out", 0, 0)]
-        for l in range(m.num_layers - 1, -1, -1):
-            X = inputs[l]
-            dX = np.zeros_like(X)
-            for d in range(dirs):
-                cache = caches[l * dirs + d]
-                dH = dIn[:, d * H:(d + 1) * H]
-                if m.is_lstm:
-                    gWi, gWh, gb, gX, gp = lstm_dir_backward(p[("W_ih", l, d)],
-                                                             p[("W_hh", l, d)], X, cache, dH, d,
-                                                             p.get(("p", l, d)))
-                    grads[("b", l, d)] += gb
-                    if m.cell == LSTM_PEEPHOLE:
-                        grads[("p", l, d)] += gp
-                else:
-                    gWi, gWh, gbi, gbh, gX = gru_dir_backward(p[("W_ih", l, d)], p[("W_hh", l, d)],
-                                                              X, cache, dH, d)
-                    grads[("b_ih", l, d)] += gbi
-                    grads[("b_hh", l, d)] += gbh
-                grads[("W_ih", l, d)] += gWi
-                grads[("W_hh", l, d)] += gWh
-                dX += gX
-            dIn = dX
-    grad = pack(m, grads) if need_grad else None
-    return float(loss), grad, tops
+            dz[b, :lengths[b]] = gc / n_seq
+    else:
+        Y = np.zeros((n_seq, T), np.int64)
+        for b, y in enumerate(seqs_y):
+            Y[b, :lengths[b]] = np.asarray(y, np.int64)
+        logp = log_softmax(z[M])                                  # valid frames only
+        picked = logp[np.arange(n_valid), Y[M]]
+        loss = -picked.sum() / n_valid
+        g = np.exp(logp)
+        g[np.arange(n_valid), Y[M]] -= 1.0
+        dz[M] = g / n_valid
+    if not need_grad:
+        return float(loss), None, tops
+    grads[("W_out", 0, 0)] += dz[M].T @ top[M]
+    grads[("b_out", 0, 0)] += dz[M].sum(axis=0)
+    dIn = dz @ p[("W_out", 0, 0)]                                  # zero on pad frames
+    for l in range(m.num_layers - 1, -1, -1):
+        X = inputs[l]
+        dX = np.zeros_like(X)
+        for d in range(dirs):
+            cache = caches[l * dirs + d]
+            dH = dIn[:, :, d * H:(d + 1) * H]
+            if m.is_lstm:
+                gWi, gWh, gb, gX, gp = lstm_dir_backward(p[("W_ih", l, d)], p[("W_hh", l, d)],
+                                                         X, lengths, cache, dH, d,
+                                                         p.get(("p", l, d)))
+                grads[("b", l, d)] += gb
+                if m.cell == LSTM_PEEPHOLE:
+                    grads[("p", l, d)] += gp
+            else:
+                gWi, gWh, gbi, gbh, gX = gru_dir_backward(p[("W_ih", l, d)], p[("W_hh", l, d)],
+                                                          X, lengths, cache, dH, d)
+                grads[("b_ih", l, d)] += gbi
+                grads[("b_hh", l, d)] += gbh
+            grads[("W_ih", l, d)] += gWi
+            grads[("W_hh", l, d)] += gWh
+            dX += gX
+        dIn = dX * M[:, :, None]
+    return float(loss), pack(m, grads), tops
 
 
 def sgd(theta, grad, lr):
