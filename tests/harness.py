@@ -1,5 +1,8 @@
 """Runs one mini-batch through the library (GPU) and through the oracle (CPU)
-on the same seeded inputs, and compares them normwise."""
+on the same seeded inputs, and compares them: per tensor and per parameter
+block, ||gpu - ref||_inf <= rtol * ||ref||_inf (the bar), and, logged beside
+it, the largest element-wise relative error over the elements with
+|ref| >= 1e-3 ||ref||_inf."""
 from __future__ import annotations
 
 import dataclasses
@@ -148,6 +151,31 @@ def normwise_err(gpu, ref) -> float:
     return num / den
 
 
+def elementwise_rel(gpu, ref, floor=1e-3):
+    """(max, 99th percentile) of |gpu - ref| / |ref| over the elements with
+    |ref| >= floor * ||ref||_inf."""
+    gpu = np.asarray(gpu, np.float64).reshape(-1)
+    ref = np.asarray(ref, np.float64).reshape(-1)
+    if ref.size == 0:
+        return 0.0, 0.0
+    m = np.max(np.abs(ref))
+    if m == 0.0:
+        return 0.0, 0.0
+    sel = np.abs(ref) >= floor * m
+    rel = np.abs(gpu[sel] - ref[sel]) / np.abs(ref[sel])
+    return float(rel.max()), float(np.percentile(rel, 99))
+
+
+def block_elementwise(spec: Spec, g_gpu, g_ref):
+    out = {}
+    pos = 0
+    for name, shape in orn.param_layout(spec.model()):
+        size = int(np.prod(shape))
+        out[name] = elementwise_rel(g_gpu[pos:pos + size], g_ref[pos:pos + size])
+        pos += size
+    return out
+
+
 def block_errors(spec: Spec, g_gpu, g_ref):
     """Normwise error of every parameter block of the flat gradient."""
     out = {}
@@ -175,13 +203,59 @@ def assert_batch_close(spec: Spec, params, data, order, rtol=None, label="", tar
                   f"hold {top_g[L + bad[0], b, :4].tolist()}", flush=True)
         assert bad.size == 0, "pad frames of the top-layer output are not zero"
     e_top = normwise_err(top_g, top_r)
+    check_results(spec, label, rtol, loss_g, grad_g, loss_r, grad_r, e_top,
+                  elementwise_rel(top_g, top_r))
+    return gb, (loss_r, grad_r, top_r)
+
+
+def check_results(spec: Spec, label, rtol, loss_g, grad_g, loss_r, grad_r, e_top, el_top):
+    """Asserts the bar on the loss, the top layer and every gradient block,
+    after logging the normwise and element-wise errors."""
     e_loss = abs(loss_g - loss_r) / abs(loss_r)
     errs = block_errors(spec, grad_g, grad_r)
     worst = max(errs.values())
+    el = block_elementwise(spec, grad_g, grad_r)
     print(f"[case] {label} loss {loss_g:.7f} vs {loss_r:.7f} err {e_loss:.2e} top {e_top:.2e} "
-          f"grad-max {worst:.2e}", flush=True)
+          f"(elementwise max {el_top[0]:.2e} p99 {el_top[1]:.2e}) grad-max {worst:.2e}",
+          flush=True)
+    for name, e in errs.items():
+        print(f"[case] {label}   {name[0]}[{name[1]},{name[2]}] normwise {e:.2e} "
+              f"elementwise max {el[name][0]:.2e} p99 {el[name][1]:.2e}", flush=True)
     assert e_loss <= rtol, (e_loss, rtol)
     assert e_top <= rtol, (e_top, rtol)
     bad = {k: v for k, v in errs.items() if v > rtol}
     assert not bad, bad
-    return gb, (loss_r, grad_r, top_r)
+
+
+def assert_long_batch_close(spec: Spec, params, data, order, job, rtol=None, label=""):
+    """assert_batch_close for batches too long for one oracle process: `job`
+    is the oracle's batch job (oracle/pool.py), running in worker processes
+    while the GPU computes; the top layer is compared sequence by sequence."""
+    rtol = RTOL[spec.gemm_dtype] if rtol is None else rtol
+    lens = data.lengths[order]
+    print(f"[case] {label} spec={spec} B={len(order)} T={int(lens.max())} N={int(lens.sum())}",
+          flush=True)
+    gb = GpuBatch(spec, params, data, order)
+    gb.forward()
+    gb.backward()
+    gb.torch.cuda.synchronize()
+    lib.sync_check()
+    loss_g = float(gb.loss.cpu()[0])
+    grad_g = gb.grads.cpu().numpy().astype(np.float64)
+    top_g = gb.top.cpu().numpy()  # float32 [T, B, Htop]
+    del gb
+    assert np.all(np.isfinite(grad_g)), "non-finite gradient (unwritten entries?)"
+    for b, L in enumerate(lens):
+        assert not np.any(top_g[L:, b] != 0.0), f"pad frames of row {b} are not zero"
+    print(f"[case] {label} GPU done; waiting for the oracle", flush=True)
+    loss_r, grad_r, tops_r = job.result(log=lambda m: print(m, flush=True))
+    num = max(float(np.max(np.abs(top_g[:L, b].astype(np.float64) - tops_r[b])))
+              for b, L in enumerate(lens))
+    den = max(float(np.max(np.abs(t))) for t in tops_r)
+    e_top = num / den if den > 0 else num
+    # element-wise figure of the top layer over three rows (memory)
+    rows = sorted({0, len(lens) // 2, len(lens) - 1})
+    el_top = elementwise_rel(np.concatenate([top_g[:lens[b], b].reshape(-1) for b in rows]),
+                             np.concatenate([tops_r[b].reshape(-1) for b in rows]))
+    check_results(spec, label, rtol, loss_g, grad_g, loss_r, grad_r, e_top, el_top)
+    return loss_r, grad_r
