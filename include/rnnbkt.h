@@ -55,7 +55,14 @@ const char* rnnbkt_version(void);
 /* Message of the last error on this thread ("" if none). */
 const char* rnnbkt_last_error(void);
 
-/* Waits for `stream` and reports any asynchronous HIP error as RNNBKT_EHIP. */
+/* Waits for `stream` and reports any asynchronous HIP error as RNNBKT_EHIP.
+ * Also RNNBKT_EHIP when a wait of a resident recurrence launch (see
+ * rnnbkt_lstm_fwd) gave up since the last report: the results of the launch
+ * it belonged to are invalid.  Such a launch still runs to its end (its
+ * later waits return at once) and other launches are not affected; the
+ * report clears the count, so a later call returns RNNBKT_OK unless new
+ * waits gave up.  The count is per device and process: call this while no
+ * other stream runs the library's launches, or the report may name them. */
 int32_t rnnbkt_sync_check(void* stream);
 
 /*
@@ -217,8 +224,9 @@ int32_t rnnbkt_buffer_sizes(const rnnbkt_model_desc* desc, int32_t T_max, int32_
  * (or of a unidirectional stack) in one launch whose workgroups stay
  * resident, when the grid fits (see rnnbkt_set_concurrency), else one
  * launch per step.  Environment: RNNBKT_RECURRENCE=steps forces the
- * per-step kernels; RNNBKT_LAUNCH=cooperative launches the resident grids
- * through the runtime's cooperative launch (alone on the device).
+ * per-step kernels; RNNBKT_MAX_POLLS=n sets the poll budget of one wait of
+ * a resident launch (default 2^20; a test hook: 0 makes every wait give up
+ * at its first miss, which rnnbkt_sync_check then reports).
  * Errors: EINVAL (null pointer, bad lengths, buffers too small),
  * EUNSUPPORTED (hidden % 32 != 0, input_dim % 4 != 0, num_classes % 4 != 0
  * or > 1024), EHIP.
@@ -365,7 +373,7 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
  * their products (forward x.W_ih and h.W_hh, backward dA.W_hh and, where a
  * launch takes a stack of layers, the upper layer's dA.W_ih), GEMMs 2*M*N*K,
  * the loss kernel 8*C+4 bytes per frame, SGD 12 and ADADELTA 28 bytes per
- * parameter.
+ * parameter, the batch preparation the bytes it moves.
  * Kinds: see RNNBKT_KERNEL_*.  The events add a small gap between launches,
  * so time a run with the timer off and use the timer in a separate pass.
  *   rnnbkt_kernel_timer(1) clears the records and starts recording,
@@ -384,7 +392,10 @@ int32_t rnnbkt_top_hidden(const rnnbkt_model_desc* desc, const int32_t* lengths,
                                     runs beside other work of the backward (output-layer
                                     weight gradients; recurrent weight gradients when the
                                     launch does not compute them): overlapped time */
-#define RNNBKT_KERNEL_KINDS 7
+#define RNNBKT_KERNEL_PREPARE 7  /* start of a forward: batch tables, packing of the padded
+                                    batch into valid frames and the sentinel fills of the
+                                    resident launches (bytes: everything the launch moves) */
+#define RNNBKT_KERNEL_KINDS 8
 
 int32_t rnnbkt_kernel_timer(int32_t enable);
 int32_t rnnbkt_kernel_timer_read(int32_t kind, double* total_ms, int64_t* launches,

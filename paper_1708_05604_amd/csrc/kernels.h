@@ -37,6 +37,9 @@ __device__ inline float act_tanh(float x) { return 2.f * act_sigmoid(2.f * x) - 
 // With splits > 1 the K range is cut into `splits` slices of k_per_split
 // (a multiple of 32); each slice writes partial[s][M][N] and
 // splitk_reduce() folds them in slice order (deterministic).
+// A second term (K2 > 0): C = op(A) op(B) + op(A2) op(B2), A2 and B2 in the
+// layouts of A and B with strides lda2, ldb2 and reduction length K2 (no
+// gather, no split-K; K % 32 == 0).
 struct GemmArgs {
   const float* A;
   const float* B;
@@ -49,7 +52,15 @@ struct GemmArgs {
   int32_t k_per_split;
   int32_t splits;
   int32_t accumulate;
+  const float* A2;
+  const float* B2;
+  int64_t lda2, ldb2;
+  int32_t K2;
 };
+
+// Output tile of the GEMM kernels, rows x columns: 64 x 64 (fp32), 128 x 128
+// (bf16).  Split-K counts are chosen per tile size.
+inline int32_t gemm_tile(bool bf16) { return bf16 ? 128 : 64; }
 
 hipError_t launch_gemm(const GemmArgs& g, bool a_kcontig, bool b_kcontig, bool bf16,
                        hipStream_t stream);
@@ -215,6 +226,15 @@ hipError_t launch_step_bwd(const StepBwdArgs& a, int cell, bool bf16, hipStream_
 // resident at once and the shape is supported; if not, nothing is launched.
 constexpr int kMaxUnits = 4;
 
+// Bounded waits of one resident launch.  `gen` identifies the launch: a wait
+// that gives up marks its own launch, whose later waits then return at once
+// (so it still ends), while other launches keep waiting normally.
+// `max_polls` is the poll budget of one wait.  Both are set by the launcher.
+struct WaitCtl {
+  uint32_t gen;
+  uint32_t max_polls;
+};
+
 // One (layer, direction) recurrence inside a forward launch.  The input
 // projection is done per step inside the kernel: the reduction operand of
 // a step is [input row (kin floats, zero-padded to a chunk multiple) ;
@@ -284,6 +304,7 @@ struct FwdLaunch {
   // the recurrence ones, reading the last unit's published output.
   OutStreamArgs out;
   int32_t out_blocks;
+  WaitCtl wait;  // set by the launcher
 };
 
 // One (layer, direction) recurrence inside a backward launch.  The
@@ -362,6 +383,7 @@ struct BwdLaunch {
   // launcher).
   WgStreamArgs wg;
   int32_t wg_on, wg_blocks;
+  WaitCtl wait;  // set by the launcher
 };
 
 // Workgroups a forward launch of these units would need (0 = shape not
@@ -375,12 +397,14 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
 // Compute units of the current device (0 on error).
 int cu_count();
 
-// Number of waits for published values that gave up (should stay 0).
 // Streams that may run persistent launches at once (each launch then claims
 // at most 1/streams of the GPU's co-resident capacity).
 void set_concurrency(int streams);
 int concurrency();
+// Number of waits for published values that gave up since the last reset
+// (0 unless something went wrong), and its reset to 0 (device synchronous).
 hipError_t read_wait_timeouts(unsigned* count);
+hipError_t reset_wait_timeouts();
 constexpr unsigned kPublishSentinel = 0xFFFFFFFFu;
 
 // Fills n 32-bit words with `value` (a kernel, so it may sit in a captured graph).

@@ -53,21 +53,21 @@ extern "C" int32_t rnnbkt_bucket_plan(const int32_t* lengths, int64_t n, int32_t
                  RNNBKT_EINVAL, "bucket_plan: null pointer");
   RNNBKT_REQUIRE(n >= 1, RNNBKT_EINVAL, "bucket_plan: n must be >= 1 (got %lld)", (long long)n);
   RNNBKT_REQUIRE(K >= 1, RNNBKT_EINVAL, "bucket_plan: K must be >= 1 (got %d)", K);
-  int32_t lmax = 0;
-  for (int64_t s = 0; s < n; ++s) {
+  for (int64_t s = 0; s < n; ++s)
     RNNBKT_REQUIRE(lengths[s] >= 1, RNNBKT_EINVAL,
                    "bucket_plan: lengths[%lld] = %d < 1", (long long)s, lengths[s]);
-    lmax = std::max(lmax, lengths[s]);
-  }
-  // Length histogram f (Sec. III.A) compressed to the distinct lengths.
-  std::vector<int64_t> f(static_cast<size_t>(lmax) + 1, 0);
-  for (int64_t s = 0; s < n; ++s) f[lengths[s]]++;
+  // Length histogram f (Sec. III.A) restricted to the distinct lengths, from
+  // a sorted copy: O(n) memory whatever the largest length is.
+  std::vector<int32_t> sorted(lengths, lengths + n);
+  std::sort(sorted.begin(), sorted.end());
   std::vector<int64_t> v, F(1, 0);
-  for (int32_t l = 1; l <= lmax; ++l)
-    if (f[l]) {
-      v.push_back(l);
-      F.push_back(F.back() + f[l]);
-    }
+  for (int64_t s = 0; s < n;) {
+    int64_t e = s + 1;
+    while (e < n && sorted[e] == sorted[s]) ++e;
+    v.push_back(sorted[s]);
+    F.push_back(F.back() + (e - s));
+    s = e;
+  }
   const int D = static_cast<int>(v.size());
   const int Q = std::min<int>(K, D);
   const int64_t INF = std::numeric_limits<int64_t>::max() / 4;

@@ -27,8 +27,9 @@
 // sentinel.  Single-location coherence of atomics is all this
 // needs: no fence, no cache write-back or invalidation, and a workgroup
 // waits only for the rows it reads (sequences are independent).  Polls are
-// bounded; after a timeout the wait gives up, counts it (reported by
-// rnnbkt_sync_check) and later waits return at once, so a launch always ends.
+// bounded; after a timeout the wait gives up, counts it (reported, then
+// cleared, by rnnbkt_sync_check) and the later waits of the same launch
+// return at once, so a launch always ends; other launches are not affected.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -43,7 +44,10 @@
 
 namespace rnnbkt {
 
+// Waits that gave up since the host last cleared the count, and the
+// generation of the last launch that had one (launch generations start at 1).
 __device__ unsigned g_wait_timeouts = 0;
+__device__ unsigned g_abandoned_gen = 0;
 
 namespace {
 
@@ -166,15 +170,20 @@ __device__ inline bool segment_clear(const unsigned (&u)[NE]) {
   return __all(ready);
 }
 
-// True once some wait of any launch has given up: later waits return at
-// once, so the launch still ends.
-__device__ inline bool waits_abandoned() {
-  return __hip_atomic_load(&g_wait_timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+// True once some wait of this launch has given up: its later waits return
+// at once, so the launch still ends.
+__device__ inline bool waits_abandoned(const WaitCtl& w) {
+  return __hip_atomic_load(&g_abandoned_gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == w.gen;
 }
 
-__device__ inline void report_timeout() {
-  if ((threadIdx.x & 63) == 0)
-    __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Counts a wait that gave up and marks the launch (one thread per call).
+__device__ inline void note_timeout(const WaitCtl& w) {
+  __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(&g_abandoned_gen, w.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline void report_timeout(const WaitCtl& w) {
+  if ((threadIdx.x & 63) == 0) note_timeout(w);
 }
 
 // The buffer loads are pure reads to the compiler: between two polls of the
@@ -182,6 +191,7 @@ __device__ inline void report_timeout() {
 // the polls into one (no code is emitted for this).
 __device__ inline void poll_fence() { __asm__ __volatile__("" ::: "memory"); }
 
+// Poll budget of one wait unless RNNBKT_MAX_POLLS sets another.
 constexpr unsigned kMaxPolls = 1u << 20;
 
 // Re-reads the segment until no element holds the sentinel (wave-uniform).
@@ -190,7 +200,8 @@ constexpr unsigned kMaxPolls = 1u << 20;
 // costs more than it saves.
 template <bool BF16, int MAXC>
 __device__ inline void settle_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
-                                      int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC]) {
+                                      int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC],
+                                      const WaitCtl& w) {
   if (segment_clear(u)) return;
   for (unsigned polls = 1;; ++polls) {
     __builtin_amdgcn_s_sleep(1);
@@ -201,9 +212,9 @@ __device__ inline void settle_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off
     // 1024 polls keeps its round trip off the path of a wait that is about
     // to succeed (checked at every wait's first miss, it cost a round trip
     // per step).
-    if ((polls & 1023u) == 0 && waits_abandoned()) return;
-    if (polls >= kMaxPolls) {
-      report_timeout();
+    if ((polls & 1023u) == 0 && waits_abandoned(w)) return;
+    if (polls >= w.max_polls) {
+      report_timeout(w);
       return;
     }
   }
@@ -305,7 +316,8 @@ __device__ inline float out_group_sum(float v) {
   return v;
 }
 
-__device__ void output_consumer(const OutStreamArgs& a, int first, int stride, char* out_smem) {
+__device__ void output_consumer(const OutStreamArgs& a, int first, int stride, char* out_smem,
+                                const WaitCtl& w) {
   const int Htop = a.Htop, C = a.C;
   const int WL = Htop + 1, ZL = C + 1;
   float* Ws = reinterpret_cast<float*>(out_smem);  // [C][WL]
@@ -360,10 +372,9 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
         __builtin_amdgcn_s_sleep(32);
         poll_fence();
         v = __builtin_amdgcn_raw_buffer_load_b128(rh, o, 0, kDeviceScope);
-        if ((polls & 1023u) == 0 && waits_abandoned()) break;
-        if (polls >= kMaxPolls) {
-          __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
+        if ((polls & 1023u) == 0 && waits_abandoned(w)) break;
+        if (polls >= w.max_polls) {
+          note_timeout(w);
           break;
         }
       }
@@ -431,9 +442,9 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
     }
     __syncthreads();  // Hs, Zs and wsum are rewritten for the next block
   }
-  // The last workgroup to finish sums the partials (every one of them was
-  // written before its workgroup's count: release fence, counter, acquire
-  // fence in the reader).
+  // The last workgroup to finish sums the partials.  The counter is a
+  // relaxed atomic and orders nothing: the partials are published values
+  // (sentinel until written), so the last workgroup polls each of them.
   if (tid == 0) {
     const unsigned prev = __hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_AGENT);
@@ -450,9 +461,9 @@ __device__ void output_consumer(const OutStreamArgs& a, int first, int stride, c
         __builtin_amdgcn_s_sleep(1);
         poll_fence();
         x = __builtin_amdgcn_raw_buffer_load_b32(rp, 4u * (unsigned)i, 0, kDeviceScope);
-        if ((polls & 1023u) == 0 && waits_abandoned()) break;
-        if (polls >= kMaxPolls) {
-          __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((polls & 1023u) == 0 && waits_abandoned(w)) break;
+        if (polls >= w.max_polls) {
+          note_timeout(w);
           break;
         }
       }
@@ -494,7 +505,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   const int rec_blocks = gridDim.x - a.out_blocks;
   if constexpr (!BF16) {
     if ((int)blockIdx.x >= rec_blocks) {
-      output_consumer(a.out, blockIdx.x - rec_blocks, a.out_blocks, smem);
+      output_consumer(a.out, blockIdx.x - rec_blocks, a.out_blocks, smem, a.wait);
       return;
     }
   }
@@ -585,7 +596,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
       for (int nt = 0; nt < NT; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
       // Input part (fetched one step ahead; a published input may still be
       // arriving).
-      if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin);
+      if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin, a.wait);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
       // Recurrent part.
@@ -593,7 +604,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
           r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + U.hcol) : kNoRow;
       unsigned urec[CPL * MAXC];
       issue_segment<BF16, MAXC>(rout, roff, srec, H, urec);
-      settle_segment<BF16, MAXC>(rout, roff, srec, H, urec);
+      settle_segment<BF16, MAXC>(rout, roff, srec, H, urec, a.wait);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         mma_segment<BF16, MAXC>(acc[nt], urec, wrec[nt], srec);
@@ -732,7 +743,7 @@ __device__ inline bool wg_clear(const u4 (&v)[2]) {
 
 // Re-reads this thread's part of an A K-tile until it is all published.
 __device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0,
-                                   int clim, int k0, int klim, int tid) {
+                                   int clim, int k0, int klim, int tid, const WaitCtl& w) {
   if (wg_clear(v)) return;
   for (unsigned polls = 1;; ++polls) {
     // (not on the recurrence's path: polling gently leaves it the memory
@@ -741,9 +752,9 @@ __device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda
     poll_fence();
     wg_load_a(v, r, lda, c0, clim, k0, klim, tid);
     if (wg_clear(v)) return;
-    if ((polls & 1023u) == 0 && waits_abandoned()) return;
-    if (polls >= kMaxPolls) {
-      __hip_atomic_fetch_add(&g_wait_timeouts, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((polls & 1023u) == 0 && waits_abandoned(w)) return;
+    if (polls >= w.max_polls) {
+      note_timeout(w);
       return;
     }
   }
@@ -796,7 +807,7 @@ __device__ inline WgJob pick_job(const WgStreamArgs& a, int j) {
 // sub of repetition wb / groups; past the last tile it repeats the last one
 // without storing, to keep step at the barriers.  LDS: NW/4 * kWgSubLds.
 template <int NW>
-__device__ void wgrad_role(const WgStreamArgs& a, int wb, float* lds) {
+__device__ void wgrad_role(const WgStreamArgs& a, int wb, float* lds, const WaitCtl& w) {
   constexpr int SUBS = NW / 4;
   const int sub = threadIdx.x >> 8, tid = threadIdx.x & 255;
   const int groups = (a.tiles + SUBS - 1) / SUBS;
@@ -833,7 +844,7 @@ __device__ void wgrad_role(const WgStreamArgs& a, int wb, float* lds) {
     wg_load_a(ua, ra, J.lda, m0, J.M, kbeg, kend, tid);
     wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, kbeg, kend, tid);
     for (int k0 = kbeg; k0 < kend; k0 += kWgBK) {
-      wg_settle_a(ua, ra, J.lda, m0, J.M, k0, kend, tid);
+      wg_settle_a(ua, ra, J.lda, m0, J.M, k0, kend, tid, w);
       wg_store(As, ua, tid);
       wg_store(Bs, rb, tid);
       __syncthreads();
@@ -890,7 +901,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   const int rec_blocks = gridDim.x - a.wg_blocks;
   if constexpr (G == 4 && !BF16) {
     if ((int)blockIdx.x >= rec_blocks) {
-      wgrad_role<NW>(a.wg, blockIdx.x - rec_blocks, reinterpret_cast<float*>(smem));
+      wgrad_role<NW>(a.wg, blockIdx.x - rec_blocks, reinterpret_cast<float*>(smem), a.wait);
       return;
     }
   }
@@ -1003,14 +1014,14 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     if (active && mma_wave) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       // Gradient arriving from the layer above (fetched one step ahead).
-      if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
+      if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup, a.wait);
       mma_segment<BF16, MAXC>(acc, uup, wup, sup);
       // Recurrent part.
       const unsigned roff =
           r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
       unsigned urec[CPL * MAXC];
       issue_segment<BF16, MAXC>(rrec, roff, srec, GH, urec);
-      settle_segment<BF16, MAXC>(rrec, roff, srec, GH, urec);
+      settle_segment<BF16, MAXC>(rrec, roff, srec, GH, urec, a.wait);
       mma_segment<BF16, MAXC>(acc, urec, wrec, srec);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[mw * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
@@ -1138,29 +1149,41 @@ int max_coresident(const void* kernel, int threads, size_t shmem) {
   return cus * per_cu / g_concurrency.load();
 }
 
-// Launches a grid that must be resident all at once.  By default an
-// ordinary launch: the grid fits in its share of the GPU (the check above),
-// so every workgroup is dispatched once the work already running drains --
-// kernels of other streams that do not wait on this one.  Several streams
-// may each run a persistent launch at once provided rnnbkt_set_concurrency
-// declared them (each then claims at most its share).  Waits stay bounded
-// either way: a launch whose grid could not all be resident ends with
-// timeouts that rnnbkt_sync_check reports.  RNNBKT_LAUNCH=cooperative uses
-// the runtime's cooperative launch instead, which guarantees residency by
-// running the grid alone on the device (measured about 25 us slower per
-// launch, and it serialises launches from different streams).
-hipError_t coop_launch(const void* kernel, int blocks, int threads, size_t shmem, void* args,
-                       hipStream_t st, bool* fits) {
+// Launches a grid that must be resident all at once, as an ordinary launch:
+// the grid fits in its share of the GPU (the check above), so every
+// workgroup is dispatched once the work already running drains -- kernels
+// of other streams that do not wait on this one.  Several streams may each
+// run a persistent launch at once provided rnnbkt_set_concurrency declared
+// them (each then claims at most its share).  Waits stay bounded: a launch
+// whose grid could not all be resident ends with timeouts that
+// rnnbkt_sync_check reports.
+hipError_t resident_launch(const void* kernel, int blocks, int threads, size_t shmem, void* args,
+                           hipStream_t st, bool* fits) {
   if (blocks > max_coresident(kernel, threads, shmem)) {
     *fits = false;
     return hipSuccess;
   }
   *fits = true;
   void* argv[] = {args};
-  const char* mode = getenv("RNNBKT_LAUNCH");
-  if (mode && strcmp(mode, "cooperative") == 0)
-    return hipLaunchCooperativeKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
   return hipLaunchKernel(kernel, dim3(blocks), dim3(threads), argv, shmem, st);
+}
+
+// Wait control of the next launch: a fresh generation (never 0, the value
+// the device flag starts from) and the poll budget, RNNBKT_MAX_POLLS when set
+// (0: a wait gives up at its first miss -- used to test the reporting path).
+std::atomic<uint32_t> g_launch_gen{0};
+WaitCtl next_wait_ctl() {
+  WaitCtl w;
+  do {
+    w.gen = g_launch_gen.fetch_add(1) + 1;
+  } while (w.gen == 0);
+  w.max_polls = kMaxPolls;
+  if (const char* e = getenv("RNNBKT_MAX_POLLS")) {
+    char* end = nullptr;
+    const unsigned long v = strtoul(e, &end, 10);
+    if (end != e && v <= 0xFFFFFFFFul) w.max_polls = (uint32_t)v;
+  }
+  return w;
 }
 
 }  // namespace
@@ -1276,7 +1299,8 @@ hipError_t launch_fwd_persistent(FwdLaunch a, int cell, bool bf16, int B, hipStr
   a.rgroups = (B + 15) / 16;
   const int per_unit = a.slices * a.rgroups;
   for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
-  return coop_launch(p.kernel, p.blocks, 256, p.shmem, &a, st, fits);
+  a.wait = next_wait_ctl();
+  return resident_launch(p.kernel, p.blocks, 256, p.shmem, &a, st, fits);
 }
 
 namespace {
@@ -1420,7 +1444,8 @@ hipError_t launch_bwd_persistent(BwdLaunch a, int cell, bool bf16, int B, hipStr
   a.wg_blocks = p.wg_blocks;
   const int per_unit = a.slices * a.rgroups;
   for (int q = 0; q < a.nunits; ++q) a.u[q].wg_begin = q * per_unit;
-  return coop_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
+  a.wait = next_wait_ctl();
+  return resident_launch(p.kernel, p.blocks, 64 * p.nw, p.shmem, &a, st, fits);
 }
 
 size_t output_stream_lds(int32_t C, int32_t Htop) {
@@ -1445,6 +1470,12 @@ int concurrency() { return g_concurrency.load(); }
 hipError_t read_wait_timeouts(unsigned* count) {
   return hipMemcpyFromSymbol(count, HIP_SYMBOL(g_wait_timeouts), sizeof(unsigned), 0,
                              hipMemcpyDeviceToHost);
+}
+
+hipError_t reset_wait_timeouts() {
+  const unsigned zero = 0;
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_wait_timeouts), &zero, sizeof(unsigned), 0,
+                           hipMemcpyHostToDevice);
 }
 
 }  // namespace rnnbkt

@@ -74,6 +74,12 @@ def test_planner_edge_cases():
     assert keff == 1 and padded == 300
     big = np.full(10, 2_000_000_000 // 10, np.int32)
     assert lib.bucket_plan(big, 1)[3] == int(big.sum())
+    # The histogram covers the distinct lengths only: a length at the int32
+    # limit costs no memory proportional to it; costs are summed in int64.
+    top = np.iinfo(np.int32).max
+    up, bof, keff, padded = lib.bucket_plan(np.array([top, 1, 5, top], np.int32), 2)
+    assert keff == 2 and list(up) == [5, top] and list(bof) == [1, 0, 0, 1]
+    assert padded == 2 * 5 + 2 * top
     with pytest.raises(lib.RnnbktError) as e:
         lib.bucket_plan([1, 0, 2], 2)
     assert e.value.code == lib.EINVAL
