@@ -105,8 +105,10 @@ struct SplitK {
   int kps;
 };
 
-SplitK choose_splitk(int64_t M, int64_t N, int64_t K) {
-  const int64_t tiles = ((M + 63) / 64) * ((N + 63) / 64);
+// Slices of the reduction so that a GEMM launches about 512 workgroups (two
+// per CU), each slice at least 256 deep, for output tiles of `tile` x `tile`.
+SplitK choose_splitk(int64_t M, int64_t N, int64_t K, int tile) {
+  const int64_t tiles = ((M + tile - 1) / tile) * ((N + tile - 1) / tile);
   int64_t S = std::max<int64_t>(1, (512 + tiles - 1) / tiles);
   S = std::min<int64_t>(S, std::max<int64_t>(1, K / 256));
   int64_t kps = (K + S - 1) / S;
@@ -140,6 +142,7 @@ struct Carve {
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
   std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
 
+  size_t ws_bwd_resident_uni;  // the first bytes, all a resident unidirectional plan uses
   size_t ws_bwd;
   size_t workspace;
 };
@@ -183,22 +186,22 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   c.ws_fwd = pos;
 
   pos = common;
-  c.dha = take(sizeof(float) * N * s.Htop);
-  c.dhb = take(sizeof(float) * N * s.Htop);
-  c.carry = take(sizeof(float) * (size_t)B * s.H);
-  c.peep_acc = s.peep ? take(sizeof(float) * (size_t)B * 3 * s.H) : 0;
+  // Backward, first what every resident (persistent) launch plan of a
+  // unidirectional stack uses: the output layer's split-K partials and
+  // column sums, the weight-gradient partials, the bias partials.
+  const int tile = gemm_tile(s.bf16);
   size_t sk = 0;
   auto need = [&](int64_t M, int64_t Nn, int64_t K) {
-    const SplitK p = choose_splitk(M, Nn, K);
+    const SplitK p = choose_splitk(M, Nn, K, tile);
     if (p.S > 1) sk = std::max(sk, (size_t)p.S * M * Nn);
   };
   {
-    const SplitK p = choose_splitk(s.C, s.Htop, N);
+    const SplitK p = choose_splitk(s.C, s.Htop, N, tile);
     c.splitk_out = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * s.C * s.Htop : 1));
   }
   c.colsum_out = take(sizeof(float) * kColsumSplits * s.C);
   {
-    const SplitK p = choose_splitk(GH, s.H, N);
+    const SplitK p = choose_splitk(GH, s.H, N, tile);
     c.splitk_rec = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * GH * s.H : 1));
   }
   {
@@ -212,15 +215,23 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
     need(GH, s.H, N);
   }
   c.splitk = take(sizeof(float) * std::max<size_t>(sk, 1));
-  // Column sums run over N frames (bias gradients) or B rows (peephole
-  // running sums): at most kColsumSplits partial rows either way.
-  c.colsum = take(sizeof(float) * kColsumSplits * std::max<int64_t>(GH, s.C));
   const int rgroups = (B + 15) / 16;
   for (int q = 0; q < s.L * s.dirs; ++q) {
     c.bpart.push_back(take(sizeof(float) * rgroups * GH));
     c.bpart_h.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * rgroups * GH) : 0);
     c.ppart.push_back(s.peep ? take(sizeof(float) * rgroups * 3 * s.H) : 0);
   }
+  c.ws_bwd_resident_uni = pos;
+  // Then what only the per-step kernels or bidirectional layers use: the
+  // gradient w.r.t. a layer's input between layer launches (ping-pong), the
+  // per-step carries and running sums, column-sum partials.
+  c.dha = take(sizeof(float) * N * s.Htop);
+  c.dhb = take(sizeof(float) * N * s.Htop);
+  c.carry = take(sizeof(float) * (size_t)B * s.H);
+  c.peep_acc = s.peep ? take(sizeof(float) * (size_t)B * 3 * s.H) : 0;
+  // Column sums run over N frames (bias gradients) or B rows (peephole
+  // running sums): at most kColsumSplits partial rows either way.
+  c.colsum = take(sizeof(float) * kColsumSplits * std::max<int64_t>(GH, s.C));
   c.ws_bwd = pos;
   c.workspace = std::max(c.ws_fwd, c.ws_bwd);
   return c;
@@ -388,11 +399,27 @@ const P* at(const void* base, size_t off) {
   return reinterpret_cast<const P*>(static_cast<const char*>(base) + off);
 }
 
+// Second reduction term of a GEMM: C += op(A2) op(B2) over K2 (see GemmArgs).
+struct Term2 {
+  const float* A2;
+  int64_t lda2;
+  const float* B2;
+  int64_t ldb2;
+  int K2;
+};
+
 hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t ldb, bool b_kc,
                 float* C, int64_t ldc, int M, int N, int K, const float* bias, int accumulate,
                 bool bf16, hipStream_t st, const int32_t* gather = nullptr,
-                float* splitk_buf = nullptr) {
+                float* splitk_buf = nullptr, const Term2* t2 = nullptr) {
   GemmArgs g{};
+  if (t2) {
+    g.A2 = t2->A2;
+    g.lda2 = t2->lda2;
+    g.B2 = t2->B2;
+    g.ldb2 = t2->ldb2;
+    g.K2 = t2->K2;
+  }
   g.A = A;
   g.B = Bm;
   g.C = C;
@@ -407,14 +434,14 @@ hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t
   g.accumulate = accumulate;
   g.splits = 1;
   g.k_per_split = (K + 31) / 32 * 32;
-  if (splitk_buf) {
-    const SplitK p = choose_splitk(M, N, K);
+  if (splitk_buf && !t2) {
+    const SplitK p = choose_splitk(M, N, K, gemm_tile(bf16));
     g.splits = p.S;
     g.k_per_split = p.kps;
     g.partial = splitk_buf;
   }
   if (M == 0 || N == 0) return hipSuccess;
-  Timed tm(RNNBKT_KERNEL_GEMM, 2.0 * M * N * K, 0.0, st);
+  Timed tm(RNNBKT_KERNEL_GEMM, 2.0 * M * N * (K + (t2 ? t2->K2 : 0)), 0.0, st);
   hipError_t e = launch_gemm(g, a_kc, b_kc, bf16, st);
   if (e != hipSuccess || g.splits == 1) return e;
   return launch_splitk_reduce(splitk_buf, g.splits, M, N, C, ldc, bias, accumulate, st);
@@ -434,9 +461,15 @@ extern "C" int32_t rnnbkt_sync_check(void* stream) {
   RNNBKT_HIP(hipGetLastError());
   unsigned timeouts = 0;
   RNNBKT_HIP(read_wait_timeouts(&timeouts));
-  RNNBKT_REQUIRE(timeouts == 0, RNNBKT_EHIP,
-                 "%u waits for values published by other workgroups timed out: results of the affected launches are invalid",
-                 timeouts);
+  if (timeouts != 0) {
+    // Reported once: the count restarts, and later launches were never
+    // affected (each launch only abandons its own waits).
+    RNNBKT_HIP(reset_wait_timeouts());
+    RNNBKT_REQUIRE(false, RNNBKT_EHIP,
+                   "%u waits for values published by other workgroups timed out: results of the "
+                   "affected launches are invalid",
+                   timeouts);
+  }
   return RNNBKT_OK;
 }
 
@@ -580,7 +613,6 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   note_prefilled(reserve, false);
   bool prefilled = false;
   {
-    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
     FillJob pre[kFillJobs];
     int npre = persist ? s.L : 0;
     for (int l = 0; l < npre && l < kFillJobs; ++l)
@@ -588,6 +620,11 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     // The output-layer workgroups publish their loss partials.
     if (persist && npre < kFillJobs)
       pre[npre++] = {reinterpret_cast<unsigned*>(lp), (N + kOutRows - 1) / kOutRows};
+    // Bytes moved: each valid frame's features and label read and written
+    // packed, its two neighbour indices written, the tables, the fills.
+    double moved = (double)N * (8.0 * s.D + (ctc ? 0.0 : 8.0) + 8.0) + 8.0 * (T + 1);
+    for (int q = 0; q < npre; ++q) moved += 4.0 * (double)pre[q].n;
+    Timed tm(RNNBKT_KERNEL_PREPARE, 0.0, moved, st);
     if (B <= kPrepMaxB && npre <= kFillJobs) {
       RNNBKT_HIP(launch_prepare(lengths, B, T, x, ctc ? nullptr : labels, s.D, d_bs, d_off, Xp,
                                 ctc ? nullptr : Yp, pf, pr, pre, npre, kPublishSentinel, out_done,
@@ -867,11 +904,14 @@ extern "C" int32_t rnnbkt_lstm_fwd_ctc(const rnnbkt_model_desc* desc, const floa
                  workspace_bytes, loss, stream);
 }
 
-extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
-                                   const int32_t* lengths, int32_t T, int32_t B,
-                                   void* reserve, size_t reserve_bytes, void* workspace,
-                                   size_t workspace_bytes, float* grads, void* stream) {
-  clear_error();
+namespace {
+
+// The backward of rnnbkt_lstm_bwd.  noalloc: the workspace is the library's
+// per-device scratch array (workspace_bytes = its size), only the part the
+// launch plan uses must fit, and all work stays on the caller's stream.
+int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32_t* lengths,
+                 int32_t T, int32_t B, void* reserve, size_t reserve_bytes, void* workspace,
+                 size_t workspace_bytes, float* grads, void* stream, bool noalloc) {
   Shape s;
   int32_t rc = check_desc(desc, &s);
   if (rc != RNNBKT_OK) return rc;
@@ -884,7 +924,8 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
                      aligned16(grads),
                  RNNBKT_EINVAL, "lstm_bwd: params, reserve, workspace and grads must be 16-byte aligned");
   const Carve c = carve(s, T, B, N);
-  RNNBKT_REQUIRE(reserve_bytes >= c.reserve && workspace_bytes >= c.workspace, RNNBKT_EINVAL,
+  RNNBKT_REQUIRE(reserve_bytes >= c.reserve && (noalloc || workspace_bytes >= c.workspace),
+                 RNNBKT_EINVAL,
                  "lstm_bwd: buffers too small (reserve %zu < %zu or workspace %zu < %zu)",
                  reserve_bytes, c.reserve, workspace_bytes, c.workspace);
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -908,44 +949,12 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   const int n = (int)N;
   const bool gru = s.cell == RNNBKT_CELL_GRU;
 
-  // Output layer: dW_out = dZ^T H_top, db_out = colsum dZ (dH_top = dZ W_out
-  // was left in the reserve by the forward).
-  // dW_out and db_out need nothing the recurrence produces: they run on a
-  // side stream beside it (the resident recurrence grids leave most CUs
-  // idle), into buffers of their own, and are joined before the layer weight
-  // gradients.  With several streams declared (rnnbkt_set_concurrency) the
-  // caller's streams already share the GPU and more queues would only
-  // contend: the side work then stays on the caller's stream.
-  const float* top = at<float>(reserve, c.hout[s.L - 1]);
-  Side side;
-  const bool split = concurrency() == 1;
-  if (split)
-    RNNBKT_HIP(side_for(st, &side));
-  else
-    side.s = st;
-  auto fork = [&]() -> hipError_t {
-    if (!split) return hipSuccess;
-    const hipError_t e = hipEventRecord(side.fork, st);
-    return e != hipSuccess ? e : hipStreamWaitEvent(side.s, side.fork, 0);
-  };
-  auto mark_join = [&]() { return split ? hipEventRecord(side.join, side.s) : hipSuccess; };
-  auto wait_join = [&]() { return split ? hipStreamWaitEvent(st, side.join, 0) : hipSuccess; };
-  RNNBKT_HIP(fork());
-  RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
-                  nullptr, 0, s.bf16, side.s, nullptr, at<float>(workspace, c.splitk_out)));
-  {
-    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
-    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
-                             grads + po.bout, side.s));
-  }
   const float* dhtop = at<float>(reserve, c.dhtop);
 
   auto da_of = [&](int l, int d) { return at<float>(reserve, c.da[l * s.dirs + d]); };
   auto dah_of = [&](int l, int d) {
     return gru ? at<float>(reserve, c.dah[l * s.dirs + d]) : nullptr;
   };
-  // Whether the forward left the exchange buffers holding the sentinel.
-  const bool prefilled = take_prefilled(reserve);
   const uint64_t rec_b = sizeof(float) * (uint64_t)N * GH;
   const uint32_t rec_bytes = rec_b < 0x7FFFFFF0u ? (uint32_t)rec_b : 0x7FFFFFF0u;
   // Unit (layer l, direction d) of a persistent backward launch.
@@ -1014,12 +1023,54 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       hi -= best;
     }
   }
+  if (noalloc) {
+    // A resident plan of a unidirectional stack uses only the first bytes.
+    const size_t need = (persistent && s.dirs == 1) ? c.ws_bwd_resident_uni : c.ws_bwd;
+    RNNBKT_REQUIRE(need <= workspace_bytes, RNNBKT_EUNSUPPORTED,
+                   "lstm_bwd_noalloc: this batch needs %zu bytes of scratch, above the %zu "
+                   "the library holds",
+                   need, workspace_bytes);
+  }
+  // Whether the forward left the exchange buffers holding the sentinel.
+  const bool prefilled = take_prefilled(reserve);
+
+  // Output layer: dW_out = dZ^T H_top, db_out = colsum dZ (dH_top = dZ W_out
+  // was left in the reserve by the forward).
+  // dW_out and db_out need nothing the recurrence produces: they run on a
+  // side stream beside it (the resident recurrence grids leave most CUs
+  // idle), into buffers of their own, and are joined before the layer weight
+  // gradients.  With several streams declared (rnnbkt_set_concurrency) the
+  // caller's streams already share the GPU and more queues would only
+  // contend: the side work then stays on the caller's stream.
+  const float* top = at<float>(reserve, c.hout[s.L - 1]);
+  Side side;
+  const bool one_stream = concurrency() == 1;
+  const bool split = one_stream && !noalloc;
+  if (split)
+    RNNBKT_HIP(side_for(st, &side));
+  else
+    side.s = st;
+  auto fork = [&]() -> hipError_t {
+    if (!split) return hipSuccess;
+    const hipError_t e = hipEventRecord(side.fork, st);
+    return e != hipSuccess ? e : hipStreamWaitEvent(side.s, side.fork, 0);
+  };
+  auto mark_join = [&]() { return split ? hipEventRecord(side.join, side.s) : hipSuccess; };
+  auto wait_join = [&]() { return split ? hipStreamWaitEvent(st, side.join, 0) : hipSuccess; };
+  RNNBKT_HIP(fork());
+  RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
+                  nullptr, 0, s.bf16, side.s, nullptr, at<float>(workspace, c.splitk_out)));
+  {
+    Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
+    RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
+                             grads + po.bout, side.s));
+  }
   // Weight gradients computed beside the recurrence by extra workgroups of
   // its launch: fp32 unidirectional LSTM stacks whose layers all run in one
   // resident launch, one stream declared (with several, the other streams'
   // launches already fill the GPU).  RNNBKT_WGRAD=after computes them after.
   const char* wg_env = getenv("RNNBKT_WGRAD");
-  bool streamw = persistent && split && !gru && s.dirs == 1 && !s.bf16 && groups.size() == 1 &&
+  bool streamw = persistent && one_stream && !gru && s.dirs == 1 && !s.bf16 && groups.size() == 1 &&
                  !(wg_env && strcmp(wg_env, "after") == 0);
   FoldJob wg_folds[kWgJobs];
   int nwg_folds = 0;
@@ -1118,11 +1169,11 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
       // Bidirectional: gradient w.r.t. the layer below's output, both directions.
       const int lo = g.hi - g.n + 1;
       if (s.dirs == 2 && lo > 0) {
-        for (int d = 0; d < 2; ++d) {
-          const int ld = lo * 2 + d;
-          RNNBKT_HIP(gemm(da_of(lo, d), GH, true, params + po.wih[ld], s.din(lo), false, dx,
-                          s.din(lo), n, s.din(lo), GH, nullptr, d > 0 ? 1 : 0, s.bf16, st));
-        }
+        // dX = dA_fwd W_ih,fwd + dA_bwd W_ih,bwd: one GEMM with two terms.
+        const Term2 t2{da_of(lo, 1), GH, params + po.wih[lo * 2 + 1], s.din(lo), GH};
+        RNNBKT_HIP(gemm(da_of(lo, 0), GH, true, params + po.wih[lo * 2], s.din(lo), false, dx,
+                        s.din(lo), n, s.din(lo), GH, nullptr, 0, s.bf16, st, nullptr, nullptr,
+                        &t2));
         dh_in = dx;
         std::swap(dx, spare);
       }
@@ -1251,6 +1302,17 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
     RNNBKT_HIP(wait_join());
   }
   return RNNBKT_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
+                                   const int32_t* lengths, int32_t T, int32_t B,
+                                   void* reserve, size_t reserve_bytes, void* workspace,
+                                   size_t workspace_bytes, float* grads, void* stream) {
+  clear_error();
+  return backward(desc, params, lengths, T, B, reserve, reserve_bytes, workspace,
+                  workspace_bytes, grads, stream, false);
 }
 
 extern "C" int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,

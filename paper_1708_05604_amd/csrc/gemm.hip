@@ -3,12 +3,20 @@
 // the backward products (dZ W_out, dA W_ih, and the weight gradients
 // dA^T X, dA^T H_prev, dZ^T H, reduced over all valid frames).
 //
-// Tile 64 x 64 x 32 per 256-thread workgroup (4 wave64s in a 2 x 2 grid,
-// each wave owning a 32 x 32 block = 2 x 2 MFMA 16x16 tiles).  Operands are
-// staged through LDS with K contiguous per row, so every lane feeds the
-// matrix core from one 16-byte LDS read per MFMA group.  fp32 uses
-// v_mfma_f32_16x16x4_f32; bf16 rounds to nearest-even when writing LDS and
-// uses v_mfma_f32_16x16x32_bf16, always accumulating in fp32.
+// fp32: tile 64 x 64 x 32 per 256-thread workgroup (4 wave64s in a 2 x 2
+// grid, each wave owning a 32 x 32 block = 2 x 2 MFMA 16x16 tiles) on
+// v_mfma_f32_16x16x4_f32.  Operands are staged through LDS with K contiguous
+// per row, so every lane feeds the matrix core from one 16-byte LDS read per
+// MFMA group.
+//
+// bf16 (k_gemm_bf16): tile 128 x 128 x 32 per 256-thread workgroup, each
+// wave owning 64 x 64 = 4 x 4 tiles of v_mfma_f32_16x16x32_bf16 with fp32
+// accumulators.  fp32 operands are rounded to bf16 (nearest-even) between
+// their 16-byte global loads and LDS, where both operands sit as [row][k]
+// bf16 (K-tiles double buffered, one barrier per K-tile); an operand stored
+// K-outer in memory is transposed in registers on the way (each thread
+// loads four k-rows of four columns and writes four 4-k pieces).  Workgroups
+// are renumbered so that the ones sharing an A row block run on one XCD.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -19,50 +27,14 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 64, BN = 64, BK = 32;
-constexpr int PAD32 = 4;   // fp32 LDS row padding (floats)
-constexpr int PAD16 = 8;   // bf16 LDS row padding (elements)
-
-template <bool BF16>
-struct Lds;
-template <>
-struct Lds<false> {
-  using T = float;
-  static constexpr int LD = BK + PAD32;
-};
-template <>
-struct Lds<true> {
-  using T = __bf16;
-  static constexpr int LD = BK + PAD16;
-};
-
-template <bool BF16>
-__device__ inline void store4(typename Lds<BF16>::T* dst, f4 v) {
-  if constexpr (BF16) {
-    bf4 b = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-    *reinterpret_cast<bf4*>(dst) = b;
-  } else {
-    *reinterpret_cast<f4*>(dst) = v;
-  }
-}
-
-template <bool BF16>
-__device__ inline void store1(typename Lds<BF16>::T* dst, float v) {
-  if constexpr (BF16) {
-    *dst = (__bf16)v;
-  } else {
-    *dst = v;
-  }
-}
+constexpr int LD32 = BK + 4;  // fp32 LDS row (floats), padded
 
 // Loads the BM x BK tile of an operand whose element (row r, k) lives at
 // P[r*ld + k] (K contiguous) into S[r][k].
-template <bool BF16>
-__device__ inline void load_kcontig(typename Lds<BF16>::T* S, const float* P, int64_t ld,
-                                    int r0, int rlim, int k0, int klim) {
-  constexpr int LD = Lds<BF16>::LD;
+__device__ inline void load_kcontig(float* S, const float* P, int64_t ld, int r0, int rlim,
+                                    int k0, int klim) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int rep = 0; rep < 2; ++rep) {
@@ -72,17 +44,14 @@ __device__ inline void load_kcontig(typename Lds<BF16>::T* S, const float* P, in
     f4 v = {0.f, 0.f, 0.f, 0.f};
     if (r0 + r < rlim && k0 + kq < klim)
       v = *reinterpret_cast<const f4*>(P + (int64_t)(r0 + r) * ld + k0 + kq);
-    store4<BF16>(S + r * LD + kq, v);
+    *reinterpret_cast<f4*>(S + r * LD32 + kq) = v;
   }
 }
 
 // Loads the BK x BM tile of an operand whose element (row r, k) lives at
 // P[row(k)*ld + r] (rows contiguous) into S[r][k] (transposed on the way).
-template <bool BF16>
-__device__ inline void load_rcontig(typename Lds<BF16>::T* S, const float* P, int64_t ld,
-                                    const int32_t* gather, int r0, int rlim, int k0,
-                                    int klim) {
-  constexpr int LD = Lds<BF16>::LD;
+__device__ inline void load_rcontig(float* S, const float* P, int64_t ld, const int32_t* gather,
+                                    int r0, int rlim, int k0, int klim) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int rep = 0; rep < 2; ++rep) {
@@ -96,16 +65,15 @@ __device__ inline void load_rcontig(typename Lds<BF16>::T* S, const float* P, in
       if (row >= 0) v = *reinterpret_cast<const f4*>(P + row * ld + r0 + rq);
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) store1<BF16>(S + (rq + e) * LD + k, v[e]);
+    for (int e = 0; e < 4; ++e) S[(rq + e) * LD32 + k] = v[e];
   }
 }
 
-template <bool A_KC, bool B_KC, bool BF16>
+// fp32 C = op(A) op(B) with A K-contiguous (B either way).
+template <bool A_KC, bool B_KC>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
-  using T = typename Lds<BF16>::T;
-  constexpr int LD = Lds<BF16>::LD;
-  __shared__ __attribute__((aligned(16))) T As[BM * LD];
-  __shared__ __attribute__((aligned(16))) T Bs[BN * LD];
+  __shared__ __attribute__((aligned(16))) float As[BM * LD32];
+  __shared__ __attribute__((aligned(16))) float Bs[BN * LD32];
 
   const int m0 = blockIdx.x * BM;
   const int n0 = blockIdx.y * BN;
@@ -128,48 +96,31 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 
   for (int k0 = kbeg; k0 < kend; k0 += BK) {
     if constexpr (A_KC)
-      load_kcontig<BF16>(As, g.A, g.lda, m0, g.M, k0, kend);
+      load_kcontig(As, g.A, g.lda, m0, g.M, k0, kend);
     else
-      load_rcontig<BF16>(As, g.A, g.lda, nullptr, m0, g.M, k0, kend);
+      load_rcontig(As, g.A, g.lda, nullptr, m0, g.M, k0, kend);
     if constexpr (B_KC)
-      load_kcontig<BF16>(Bs, g.B, g.ldb, n0, g.N, k0, kend);
+      load_kcontig(Bs, g.B, g.ldb, n0, g.N, k0, kend);
     else
-      load_rcontig<BF16>(Bs, g.B, g.ldb, g.gather_b, n0, g.N, k0, kend);
+      load_rcontig(Bs, g.B, g.ldb, g.gather_b, n0, g.N, k0, kend);
     __syncthreads();
-    if constexpr (BF16) {
-      const int kk = lq * 8;
-      bf8 a[2], b[2];
+#pragma unroll
+    for (int kc = 0; kc < BK; kc += 16) {
+      const int kk = kc + lq * 4;
+      f4 a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const bf8*>(As + (wm + i * 16 + lr) * LD + kk);
+        a[i] = *reinterpret_cast<const f4*>(As + (wm + i * 16 + lr) * LD32 + kk);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const bf8*>(Bs + (wn + j * 16 + lr) * LD + kk);
+        b[j] = *reinterpret_cast<const f4*>(Bs + (wn + j * 16 + lr) * LD32 + kk);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    } else {
-#pragma unroll
-      for (int kc = 0; kc < BK; kc += 16) {
-        const int kk = kc + lq * 4;
-        f4 a[2], b[2];
+      for (int e = 0; e < 4; ++e)
 #pragma unroll
         for (int i = 0; i < 2; ++i)
-          a[i] = *reinterpret_cast<const f4*>(As + (wm + i * 16 + lr) * LD + kk);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          b[j] = *reinterpret_cast<const f4*>(Bs + (wn + j * 16 + lr) * LD + kk);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-              acc[i][j] =
-                  __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
-      }
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][e], b[j][e], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
@@ -388,25 +339,222 @@ __global__ void k_colsum_partial(const float* __restrict__ A, int64_t rows, int 
   partial[(int64_t)s * cols + c] = (v0 + v1) + (v2 + v3);
 }
 
+// ---------------------------------------------------------------- bf16
+constexpr int TBM = 128, TBK = 32;
+constexpr int TB_LD = TBK + 8;  // bf16 per LDS row: 80 bytes, so the 16-byte
+                                // reads of 16 consecutive rows hit distinct banks
+typedef __bf16 bf4v __attribute__((ext_vector_type(4)));
+
+__device__ inline bf4v to_bf4(float a, float b, float c, float d) {
+  return bf4v{(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+}
+
+// One operand's K-tile of 128 rows x 32 k in registers, as loaded (fp32).
+struct TileRegs {
+  f4 v[4];
+};
+
+// Element (r, k) of an operand: KC at P[r*ld + k], else at P[row(k)*ld + r]
+// with row(k) = gather ? gather[k] : k (negative = a zero row).
+// KC: thread t loads rows (t >> 3) + 32 i, k = 4 (t & 7) .. + 3.
+// RC: thread t loads k-rows 4 (t >> 5) + i, columns 4 (t & 31) .. + 3.
+template <bool KC>
+__device__ inline void tb_fetch(TileRegs& R, const float* P, int64_t ld, const int32_t* gather,
+                                int r0, int rlim, int k0, int klim, int tid) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f4 x = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (KC) {
+      const int r = (tid >> 3) + 32 * i, k = k0 + (tid & 7) * 4;
+      if (r0 + r < rlim) {
+        const float* q = P + (int64_t)(r0 + r) * ld + k;
+        if (k + 4 <= klim) {
+          x = *reinterpret_cast<const f4*>(q);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (k + e < klim) x[e] = q[e];
+        }
+      }
+    } else {
+      const int k = k0 + 4 * (tid >> 5) + i, r = r0 + 4 * (tid & 31);
+      if (k < klim && r < rlim) {
+        int64_t row = k;
+        if (gather) row = gather[k];
+        if (row >= 0) {
+          const float* q = P + row * ld + r;
+          if (r + 4 <= rlim) {
+            x = *reinterpret_cast<const f4*>(q);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (r + e < rlim) x[e] = q[e];
+          }
+        }
+      }
+    }
+    R.v[i] = x;
+  }
+}
+
+// Writes the registers of tb_fetch into S[row][k] (bf16, row pitch TB_LD).
+template <bool KC>
+__device__ inline void tb_store(__bf16* S, const TileRegs& R, int tid) {
+  if constexpr (KC) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = (tid >> 3) + 32 * i, k = (tid & 7) * 4;
+      *reinterpret_cast<bf4v*>(S + r * TB_LD + k) =
+          to_bf4(R.v[i][0], R.v[i][1], R.v[i][2], R.v[i][3]);
+    }
+  } else {
+    const int k = 4 * (tid >> 5), r = 4 * (tid & 31);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      *reinterpret_cast<bf4v*>(S + (r + e) * TB_LD + k) =
+          to_bf4(R.v[0][e], R.v[1][e], R.v[2][e], R.v[3][e]);
+  }
+}
+
+// Workgroup b of n -> logical index such that consecutive logical indices
+// run on one XCD (workgroups are dispatched to the 8 XCDs in turn).
+__device__ inline int xcd_logical(int b, int n) {
+  const int per = n / 8, rem = n % 8, x = b % 8;
+  return x * per + min(x, rem) + b / 8;
+}
+
+template <bool A_KC, bool B_KC>
+__global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) __bf16 As[2][TBM * TB_LD];
+  __shared__ __attribute__((aligned(16))) __bf16 Bs[2][TBM * TB_LD];
+  const int mt = (g.M + TBM - 1) / TBM, nt = (g.N + TBM - 1) / TBM;
+  const int l = xcd_logical(blockIdx.x, gridDim.x);
+  const int n_i = l % nt, m_i = (l / nt) % mt, split = l / (nt * mt);
+  const int m0 = m_i * TBM, n0 = n_i * TBM;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int lr = lane & 15, lq = lane >> 4;
+
+  f4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+  int buf = 0;
+  // One reduction term: A (lda) x B (ldb, gather) over k in [kbeg, kend).
+  auto term = [&](const float* A, int64_t lda, const float* B, int64_t ldb,
+                  const int32_t* gather, int kbeg, int kend) {
+    if (kbeg >= kend) return;
+    TileRegs ra, rb;
+    tb_fetch<A_KC>(ra, A, lda, nullptr, m0, g.M, kbeg, kend, tid);
+    tb_fetch<B_KC>(rb, B, ldb, gather, n0, g.N, kbeg, kend, tid);
+    for (int k0 = kbeg; k0 < kend; k0 += TBK) {
+      tb_store<A_KC>(As[buf], ra, tid);
+      tb_store<B_KC>(Bs[buf], rb, tid);
+      __syncthreads();
+      if (k0 + TBK < kend) {
+        tb_fetch<A_KC>(ra, A, lda, nullptr, m0, g.M, k0 + TBK, kend, tid);
+        tb_fetch<B_KC>(rb, B, ldb, gather, n0, g.N, k0 + TBK, kend, tid);
+      }
+      const __bf16* a_s = As[buf];
+      const __bf16* b_s = Bs[buf];
+      bf8 a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        a[i] = *reinterpret_cast<const bf8*>(a_s + (wm + 16 * i + lr) * TB_LD + 8 * lq);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        b[j] = *reinterpret_cast<const bf8*>(b_s + (wn + 16 * j + lr) * TB_LD + 8 * lq);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      buf ^= 1;
+    }
+  };
+  const int kbeg = split * g.k_per_split;
+  term(g.A, g.lda, g.B, g.ldb, g.gather_b, kbeg, min(g.K, kbeg + g.k_per_split));
+  if (g.K2 > 0) term(g.A2, g.lda2, g.B2, g.ldb2, nullptr, 0, g.K2);
+
+  // Accumulator layout of a 16x16 MFMA tile: lane holds column (lane & 15),
+  // rows 4*(lane >> 4) + r for r = 0..3.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + wn + 16 * j + lr;
+      if (n >= g.N) continue;
+      const float bv = (g.splits == 1 && g.bias) ? g.bias[n] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm + 16 * i + 4 * lq + r;
+        if (m >= g.M) continue;
+        float v = acc[i][j][r];
+        if (g.splits > 1) {
+          g.partial[((int64_t)split * g.M + m) * g.N + n] = v;
+        } else {
+          float* c = g.C + (int64_t)m * g.ldc + n;
+          v += bv;
+          if (g.accumulate) v += *c;
+          *c = v;
+        }
+      }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& g, bool a_kc, bool b_kc, bool bf16, hipStream_t st) {
+  if (g.K2 > 0 && (g.splits > 1 || g.K % 32 != 0 || g.gather_b)) return hipErrorInvalidValue;
+  if (bf16) {
+    const int64_t blocks = (int64_t)((g.M + TBM - 1) / TBM) * ((g.N + TBM - 1) / TBM) *
+                           (g.splits > 1 ? g.splits : 1);
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)blocks), block(256);
+#define RNNBKT_GEMM_BF16(AK, BKC)                                            \
+  if (a_kc == AK && b_kc == BKC) {                                           \
+    hipLaunchKernelGGL((k_gemm_bf16<AK, BKC>), grid, block, 0, st, g);      \
+    return hipGetLastError();                                                \
+  }
+    RNNBKT_GEMM_BF16(true, true)
+    RNNBKT_GEMM_BF16(true, false)
+    RNNBKT_GEMM_BF16(false, false)
+    RNNBKT_GEMM_BF16(false, true)
+#undef RNNBKT_GEMM_BF16
+    return hipErrorInvalidValue;
+  }
+  if (g.K2 > 0) {
+    // fp32: the second term as a second launch accumulating into C.
+    GemmArgs g1 = g, g2 = g;
+    g1.K2 = 0;
+    g2.A = g.A2;
+    g2.B = g.B2;
+    g2.lda = g.lda2;
+    g2.ldb = g.ldb2;
+    g2.K = g.K2;
+    g2.k_per_split = (g.K2 + 31) / 32 * 32;
+    g2.K2 = 0;
+    g2.bias = nullptr;
+    g2.accumulate = 1;
+    hipError_t e = launch_gemm(g1, a_kc, b_kc, false, st);
+    return e != hipSuccess ? e : launch_gemm(g2, a_kc, b_kc, false, st);
+  }
   dim3 grid((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, g.splits > 1 ? g.splits : 1);
   dim3 block(256);
-#define RNNBKT_GEMM_CASE(AK, BKC, BF)                                      \
-  if (a_kc == AK && b_kc == BKC && bf16 == BF) {                           \
-    hipLaunchKernelGGL((k_gemm<AK, BKC, BF>), grid, block, 0, st, g);     \
+#define RNNBKT_GEMM_CASE(AK, BKC)                                          \
+  if (a_kc == AK && b_kc == BKC) {                                         \
+    hipLaunchKernelGGL((k_gemm<AK, BKC>), grid, block, 0, st, g);         \
     return hipGetLastError();                                              \
   }
-  RNNBKT_GEMM_CASE(true, true, false)
-  RNNBKT_GEMM_CASE(true, true, true)
-  RNNBKT_GEMM_CASE(true, false, false)
-  RNNBKT_GEMM_CASE(true, false, true)
-  if (!a_kc && !b_kc && !bf16) {
+  RNNBKT_GEMM_CASE(true, true)
+  RNNBKT_GEMM_CASE(true, false)
+  if (!a_kc && !b_kc) {
     hipLaunchKernelGGL(k_gemm_tn_f32, grid, block, 0, st, g);
     return hipGetLastError();
   }
-  RNNBKT_GEMM_CASE(false, false, true)
 #undef RNNBKT_GEMM_CASE
   return hipErrorInvalidValue;
 }

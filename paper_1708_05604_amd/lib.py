@@ -102,7 +102,7 @@ _SIGNATURES = {
 }
 
 KERNEL_KINDS = {"step_fwd": 0, "step_bwd": 1, "gemm": 2, "xent": 3, "sgd": 4, "other": 5,
-                "side": 6}
+                "side": 6, "prepare": 7}
 # Kinds whose time runs beside the recurrence rather than on the critical path.
 OVERLAPPED_KINDS = ("side",)
 
