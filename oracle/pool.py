@@ -33,6 +33,17 @@ def _work(model_args, theta, xs, ys, need_tops):
     return n_part, loss * n_part, grad * n_part, tops, time.perf_counter() - t0
 
 
+def _worker_init(nice):
+    if nice > 0:
+        os.nice(nice)
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(limits=1)  # also set by the environment at start
+
+
+def _ready():
+    return os.getpid()
+
+
 def default_workers() -> int:
     """The CPUs this process may run on, at most 16 (the CPU share of a
     one-GPU machine, whatever the host reports)."""
@@ -47,18 +58,22 @@ class Pool:
     """Worker processes (started fresh, not forked) shared by any number of
     batches; submit() returns a BatchJob whose result() waits for it."""
 
-    def __init__(self, workers: int | None = None):
+    def __init__(self, workers: int | None = None, nice: int = 0):
+        """nice > 0 lowers the workers' scheduling priority (work running
+        beside them in the parent keeps precedence)."""
         self.workers = default_workers() if workers is None else max(1, int(workers))
-        # One BLAS thread per worker; large arrays from the heap and freed
-        # memory kept, so that a worker's pages are faulted in once and then
-        # reused (fresh pages are expensive in some sandboxes).
-        env = {"OMP_NUM_THREADS": "1", "OPENBLAS_NUM_THREADS": "1",
-               "MALLOC_MMAP_THRESHOLD_": str(1 << 40), "MALLOC_TRIM_THRESHOLD_": str(1 << 42)}
+        # One BLAS thread per worker (the work is split by processes).
+        env = {"OMP_NUM_THREADS": "1", "OPENBLAS_NUM_THREADS": "1"}
         saved = {k: os.environ.get(k) for k in env}
         os.environ.update(env)
         try:
             self.ex = concurrent.futures.ProcessPoolExecutor(
-                max_workers=self.workers, mp_context=multiprocessing.get_context("spawn"))
+                max_workers=self.workers, mp_context=multiprocessing.get_context("spawn"),
+                initializer=_worker_init, initargs=(nice,))
+            # The workers start on demand: start them all now, while the
+            # environment above is in place.
+            for f in [self.ex.submit(_ready) for _ in range(self.workers)]:
+                f.result()
         finally:
             for k, v in saved.items():
                 if v is None:

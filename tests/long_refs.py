@@ -37,6 +37,7 @@ def case_id(name, K):
 BY_ID = {case_id(c[0], c[1]): c for c in CASES}
 
 _pool = None
+_blas_limit = None
 _jobs = {}
 
 
@@ -71,8 +72,13 @@ def start(ids):
     chosen = [(cid, longest_batch(*BY_ID[cid][:2])) for cid in todo]
     if _pool is None:
         # Four CPUs stay with the rest of the suite, which runs meanwhile
-        # (and has oracle work of its own).
-        _pool = opool.Pool(max(1, opool.default_workers() - 4))
+        # (and has oracle work of its own): the workers get a lower priority,
+        # and BLAS in this process is held to four threads while they run.
+        global _blas_limit
+        free = 4
+        _pool = opool.Pool(max(1, opool.default_workers() - free), nice=10)
+        from threadpoolctl import threadpool_limits
+        _blas_limit = threadpool_limits(limits=free)
     for cid, (data, order) in chosen:
         w = synth.WORKLOADS[BY_ID[cid][0]]
         _jobs[cid] = (data, order,
@@ -88,8 +94,11 @@ def get(cid):
 
 
 def stop():
-    global _pool
+    global _pool, _blas_limit
     if _pool is not None:
         _pool.close(kill=True)
         _pool = None
+    if _blas_limit is not None:
+        _blas_limit.restore_original_limits()
+        _blas_limit = None
     _jobs.clear()
