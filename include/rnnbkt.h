@@ -299,6 +299,28 @@ int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
                         void* reserve, size_t reserve_bytes, void* workspace,
                         size_t workspace_bytes, float* grads, void* stream);
 
+/*
+ * rnnbkt_lstm_bwd_noalloc -- rnnbkt_lstm_bwd for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): no workspace argument, no allocation,
+ * no stream or event creation.  Its scratch is a 128 MiB array the library
+ * holds on each device it runs on (from its first use there until the
+ * process ends).  A batch whose backward needs more is refused with
+ * RNNBKT_EUNSUPPORTED before anything is enqueued: a unidirectional stack
+ * on the resident kernels needs only its split-K, weight-gradient and bias
+ * partials (every batch of a 2-layer H=512 LSTM with B=128 and 4000 steps
+ * fits), other plans the full backward workspace of rnnbkt_buffer_sizes.
+ * Everything runs on `stream` (no internal side stream); results equal
+ * rnnbkt_lstm_bwd's bit for bit.  All calls on one device share its scratch:
+ * calls that overlap on one device (different streams or threads) race, so
+ * serialise them.  Nothing in the scratch needs clearing between calls.
+ * Arguments and errors otherwise as rnnbkt_lstm_bwd.
+ */
+int32_t rnnbkt_lstm_bwd_noalloc(const rnnbkt_model_desc* desc, const float* params,
+                                const int32_t* lengths, int32_t T_max, int32_t B,
+                                void* reserve, size_t reserve_bytes, float* grads,
+                                void* stream);
+
 /* rnnbkt_sgd_apply -- params[i] -= lr * grads[i] for i < n (device fp32). */
 int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,
                          void* stream);

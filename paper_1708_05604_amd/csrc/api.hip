@@ -1304,6 +1304,34 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   return RNNBKT_OK;
 }
 
+// Scratch of rnnbkt_lstm_bwd_noalloc: one array per device, held from the
+// library's first use on that device until the process ends.  Host code must
+// not use the array's name as an address: it stands for the array on the
+// host side only.  Its device address comes from hipGetSymbolAddress, once
+// per device, and is kept in g_scratch_ptr.
+constexpr size_t kScratchBytes = size_t(128) << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int32_t scratch_of_current_device(void** out) {
+  int dev = 0;
+  RNNBKT_HIP(hipGetDevice(&dev));
+  RNNBKT_REQUIRE(dev >= 0 && dev < kMaxDevices, RNNBKT_EUNSUPPORTED,
+                 "lstm_bwd_noalloc: device index %d above %d", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    RNNBKT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    RNNBKT_REQUIRE(p != nullptr, RNNBKT_EHIP, "lstm_bwd_noalloc: no address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RNNBKT_OK;
+}
+
 }  // namespace
 
 extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* params,
@@ -1313,6 +1341,18 @@ extern "C" int32_t rnnbkt_lstm_bwd(const rnnbkt_model_desc* desc, const float* p
   clear_error();
   return backward(desc, params, lengths, T, B, reserve, reserve_bytes, workspace,
                   workspace_bytes, grads, stream, false);
+}
+
+extern "C" int32_t rnnbkt_lstm_bwd_noalloc(const rnnbkt_model_desc* desc, const float* params,
+                                           const int32_t* lengths, int32_t T, int32_t B,
+                                           void* reserve, size_t reserve_bytes, float* grads,
+                                           void* stream) {
+  clear_error();
+  void* ws = nullptr;
+  const int32_t rc = scratch_of_current_device(&ws);
+  if (rc != RNNBKT_OK) return rc;
+  return backward(desc, params, lengths, T, B, reserve, reserve_bytes, ws, kScratchBytes, grads,
+                  stream, true);
 }
 
 extern "C" int32_t rnnbkt_sgd_apply(float* params, const float* grads, int64_t n, float lr,

@@ -86,6 +86,8 @@ _SIGNATURES = {
                                              _vp]),
     "rnnbkt_lstm_bwd": (ctypes.c_int32, [_descp, _vp, _i32p, ctypes.c_int32, ctypes.c_int32,
                                          _vp, ctypes.c_size_t, _vp, ctypes.c_size_t, _vp, _vp]),
+    "rnnbkt_lstm_bwd_noalloc": (ctypes.c_int32, [_descp, _vp, _i32p, ctypes.c_int32,
+                                                 ctypes.c_int32, _vp, ctypes.c_size_t, _vp, _vp]),
     "rnnbkt_sgd_apply": (ctypes.c_int32, [_vp, _vp, ctypes.c_int64, ctypes.c_float, _vp]),
     "rnnbkt_epoch_aggregate": (ctypes.c_int32, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
                                                 ctypes.c_int64, ctypes.c_void_p, ctypes.c_float,
@@ -310,6 +312,17 @@ def lstm_bwd(desc, params, lengths, reserve, workspace, grads, stream=None):
                                   int(L[0]), int(L.size), _dev(reserve), _nbytes(reserve),
                                   _dev(workspace), _nbytes(workspace), _dev(grads, "float32"),
                                   _stream(stream)))
+
+
+def lstm_bwd_noalloc(desc, params, lengths, reserve, grads, stream=None):
+    """rnnbkt_lstm_bwd on the library's own scratch (no workspace)."""
+    L = _i32(lengths)
+    _need(params, param_count(desc), "params")
+    _need(grads, param_count(desc), "grads")
+    _check(load().rnnbkt_lstm_bwd_noalloc(ctypes.byref(desc), _dev(params, "float32"),
+                                          _ptr(L, _i32p), int(L[0]), int(L.size), _dev(reserve),
+                                          _nbytes(reserve), _dev(grads, "float32"),
+                                          _stream(stream)))
 
 
 def sgd_apply(params, grads, lr: float, stream=None, n: Optional[int] = None):
