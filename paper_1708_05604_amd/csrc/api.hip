@@ -137,7 +137,7 @@ struct Carve {
   // workspace (backward)
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
   size_t splitk_out, colsum_out;  // output-layer gradients (run beside the recurrence)
-  size_t splitk_rec;              // recurrent weight gradients (run beside the input ones)
+  size_t splitk_rec;              // weight gradients on the side stream
   size_t wgpart;                  // streamed weight gradients: partial tiles of every layer
   std::vector<size_t> bpart, bpart_h;  // bias-gradient partials per layer*dirs
   std::vector<size_t> ppart;           // peephole-gradient partials per layer*dirs
@@ -201,8 +201,15 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   }
   c.colsum_out = take(sizeof(float) * kColsumSplits * s.C);
   {
-    const SplitK p = choose_splitk(GH, s.H, N, tile);
-    c.splitk_rec = take(sizeof(float) * (p.S > 1 ? (size_t)p.S * GH * s.H : 1));
+    // Products on the side stream: dW_hh, and dW_ih of layers whose weight
+    // gradients run beside the recurrence of the layers below.
+    size_t rec = 1;
+    for (int l = 0; l < s.L; ++l)
+      for (const int64_t cols : {(int64_t)s.H, (int64_t)s.din(l)}) {
+        const SplitK p = choose_splitk(GH, cols, N, tile);
+        if (p.S > 1) rec = std::max(rec, (size_t)p.S * GH * cols);
+      }
+    c.splitk_rec = take(sizeof(float) * rec);
   }
   {
     size_t wg = 0;  // kWgRepsMax partial copies of dW_ih and dW_hh of every layer
@@ -1076,6 +1083,31 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   int nwg_folds = 0;
   double wg_flops = 0;
 
+  // Weight gradients dW_ih and dW_hh of layer l (both directions), reduced
+  // over every valid frame: dW_ih on s_ih with split-K buffer buf_ih, dW_hh
+  // on s_hh with the buffer of its own stream's products.
+  float* sk_rec = at<float>(workspace, c.splitk_rec);
+  auto layer_wgrad = [&](int l, hipStream_t s_ih, float* buf_ih, hipStream_t s_hh) -> hipError_t {
+    const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
+    const int din = s.din(l);
+    const float* hout = at<float>(reserve, c.hout[l]);
+    for (int d = 0; d < s.dirs; ++d) {
+      const int ld = l * s.dirs + d;
+      const float* dax = da_of(l, d);
+      const float* dahh = gru ? dah_of(l, d) : dax;
+      hipError_t e = gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
+                          nullptr, 0, s.bf16, s_ih, nullptr, buf_ih);
+      if (e != hipSuccess) return e;
+      e = gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld], s.H, GH,
+               s.H, n, nullptr, 0, s.bf16, s_hh, d == 0 ? pf : pr, sk_rec);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  };
+  // Layers whose weight gradients are already enqueued (on the side stream,
+  // beside the recurrence of the layers below).
+  std::vector<char> wg_done(s.L, 0);
+
   if (persistent) {
     // Gradient w.r.t. the output of the top layer of the next group; the
     // dX GEMMs of bidirectional layers alternate between dha and dhb.
@@ -1177,6 +1209,17 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
         dh_in = dx;
         std::swap(dx, spare);
       }
+      // The group's gate gradients are complete: its weight gradients run on
+      // the side stream beside the recurrence of the groups below (which
+      // leave most CUs idle).  The last group's run after it, split over
+      // both streams.
+      if (split && !streamw && &g != &groups.back()) {
+        RNNBKT_HIP(fork());
+        for (int q = 0; q < g.n; ++q) {
+          RNNBKT_HIP(layer_wgrad(g.hi - q, side.s, sk_rec, side.s));
+          wg_done[g.hi - q] = 1;
+        }
+      }
     }
   } else {
     // One launch per time step: each layer needs the full gradient from above.
@@ -1266,29 +1309,17 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
                                             (int32_t)std::min<size_t>(kFoldJobs, folds.size() - q0),
                                             st));
   }
-  RNNBKT_HIP(mark_join());
-  RNNBKT_HIP(wait_join());
-  // Weight gradients of every layer, reduced over every valid frame (unless
-  // the recurrence launch computed them).  The input and recurrent
-  // products of a layer read the same dA and are independent: the recurrent
-  // ones run on the side stream (own split-K buffer), overlapping the other
-  // stream's products and reductions.
+  // Weight gradients of the layers not enqueued yet (unless the recurrence
+  // launch computed them).  The input and recurrent products of a layer read
+  // the same dA and are independent: the recurrent ones run on the side
+  // stream (own split-K buffer), overlapping the other stream's products.
   if (!streamw) RNNBKT_HIP(fork());
-  float* sk_rec = at<float>(workspace, c.splitk_rec);
   for (int l = 0; l < s.L; ++l) {
-    const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
-    const int din = s.din(l);
-    const float* hout = at<float>(reserve, c.hout[l]);
+    if (!streamw && !wg_done[l]) RNNBKT_HIP(layer_wgrad(l, st, sk, side.s));
     for (int d = 0; d < s.dirs; ++d) {
       const int ld = l * s.dirs + d;
       const float* dax = da_of(l, d);
       const float* dahh = gru ? dah_of(l, d) : dax;
-      if (!streamw) {
-        RNNBKT_HIP(gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
-                        nullptr, 0, s.bf16, st, nullptr, sk));
-        RNNBKT_HIP(gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld],
-                        s.H, GH, s.H, n, nullptr, 0, s.bf16, side.s, d == 0 ? pf : pr, sk_rec));
-      }
       if (!persistent) {
         Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
         RNNBKT_HIP(launch_colsum(dax, N, GH, GH, colsum_rows(N), cs, grads + po.b[ld], st));
@@ -1297,10 +1328,10 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       }
     }
   }
-  if (!streamw) {
-    RNNBKT_HIP(mark_join());
-    RNNBKT_HIP(wait_join());
-  }
+  // Everything on the side stream (output-layer gradients, weight
+  // gradients) is ordered before the caller's later work.
+  RNNBKT_HIP(mark_join());
+  RNNBKT_HIP(wait_join());
   return RNNBKT_OK;
 }
 

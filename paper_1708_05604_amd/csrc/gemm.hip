@@ -15,8 +15,10 @@
 // their 16-byte global loads and LDS, where both operands sit as [row][k]
 // bf16 (K-tiles double buffered, one barrier per K-tile); an operand stored
 // K-outer in memory is transposed in registers on the way (each thread
-// loads four k-rows of four columns and writes four 4-k pieces).  Workgroups
-// are renumbered so that the ones sharing an A row block run on one XCD.
+// loads four k-rows of four columns and writes four 4-k pieces), with the
+// 16-byte chunks of each LDS row permuted so that those stores spread over
+// the banks.  Workgroups are renumbered so that the ones sharing an A row
+// block run on one XCD.
 #include <hip/hip_runtime.h>
 
 #include "kernels.h"
@@ -349,6 +351,14 @@ __device__ inline bf4v to_bf4(float a, float b, float c, float d) {
   return bf4v{(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
 }
 
+// LDS element offset of (row, k) in a K-tile: the four 16-byte chunks of a
+// row are permuted by (row / 4) mod 4, so that the 8-byte stores of
+// transposed operands (consecutive threads four rows apart) spread over the
+// banks; the 16-byte fragment reads stay whole.
+__device__ inline int tb_off(int row, int k) {
+  return row * TB_LD + ((((k >> 3) ^ (row >> 2)) & 3) << 3) + (k & 7);
+}
+
 // One operand's K-tile of 128 rows x 32 k in registers, as loaded (fp32).
 struct TileRegs {
   f4 v[4];
@@ -404,14 +414,14 @@ __device__ inline void tb_store(__bf16* S, const TileRegs& R, int tid) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = (tid >> 3) + 32 * i, k = (tid & 7) * 4;
-      *reinterpret_cast<bf4v*>(S + r * TB_LD + k) =
+      *reinterpret_cast<bf4v*>(S + tb_off(r, k)) =
           to_bf4(R.v[i][0], R.v[i][1], R.v[i][2], R.v[i][3]);
     }
   } else {
     const int k = 4 * (tid >> 5), r = 4 * (tid & 31);
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      *reinterpret_cast<bf4v*>(S + (r + e) * TB_LD + k) =
+      *reinterpret_cast<bf4v*>(S + tb_off(r + e, k)) =
           to_bf4(R.v[0][e], R.v[1][e], R.v[2][e], R.v[3][e]);
   }
 }
@@ -463,10 +473,10 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
       bf8 a[4], b[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const bf8*>(a_s + (wm + 16 * i + lr) * TB_LD + 8 * lq);
+        a[i] = *reinterpret_cast<const bf8*>(a_s + tb_off(wm + 16 * i + lr, 8 * lq));
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const bf8*>(b_s + (wn + 16 * j + lr) * TB_LD + 8 * lq);
+        b[j] = *reinterpret_cast<const bf8*>(b_s + tb_off(wn + 16 * j + lr, 8 * lq));
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -514,16 +524,16 @@ hipError_t launch_gemm(const GemmArgs& g, bool a_kc, bool b_kc, bool bf16, hipSt
                            (g.splits > 1 ? g.splits : 1);
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks), block(256);
-#define RNNBKT_GEMM_BF16(AK, BKC)                                            \
+#define RNNBKT_BF16_CASE(AK, BKC)                                            \
   if (a_kc == AK && b_kc == BKC) {                                           \
     hipLaunchKernelGGL((k_gemm_bf16<AK, BKC>), grid, block, 0, st, g);      \
     return hipGetLastError();                                                \
   }
-    RNNBKT_GEMM_BF16(true, true)
-    RNNBKT_GEMM_BF16(true, false)
-    RNNBKT_GEMM_BF16(false, false)
-    RNNBKT_GEMM_BF16(false, true)
-#undef RNNBKT_GEMM_BF16
+    RNNBKT_BF16_CASE(true, true)
+    RNNBKT_BF16_CASE(true, false)
+    RNNBKT_BF16_CASE(false, false)
+    RNNBKT_BF16_CASE(false, true)
+#undef RNNBKT_BF16_CASE
     return hipErrorInvalidValue;
   }
   if (g.K2 > 0) {
