@@ -889,7 +889,11 @@ __device__ void wgrad_role(const WgStreamArgs& a, int wb, float* lds, const Wait
 // threads 0..255 then run the gate-gradient algebra of one (row, unit) each,
 // carrying dc*f (LSTM) or dh*z (GRU) of their row and unit in a register and
 // summing the unit's gate gradients over the steps for the bias gradients.
-template <int G, bool BF16, int NW, int MAXC, bool SPLIT>
+// UP = false: no unit of the launch reads a gradient from a layer above in
+// the kernel (bidirectional layers, the top of a stack): the input segment's
+// fragments and operands are not kept at all, which leaves their registers
+// to the recurrent segment.
+template <int G, bool BF16, int NW, int MAXC, bool SPLIT, bool UP>
 __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
@@ -945,12 +949,14 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   const Slots srec{first, NMMA, GH / CH, lq * CPL};
 
   // Weight fragments: column lr is hidden unit j0 + lr.
-  typename WFrag<BF16>::T wup[MAXC], wrec[MAXC];
+  constexpr int MU = UP ? MAXC : 1;
+  typename WFrag<BF16>::T wup[MU], wrec[MAXC];
   {
     const int j = j0 + lr;
     const float* wu = has_up ? U.wih_up + U.hcol + j : nullptr;
     const float* wh = U.whh + j;
-    load_wfrags<BF16, MAXC>(wup, sup, [&](int k) { return wu ? wu[(int64_t)k * U.din_up] : 0.f; });
+    if constexpr (UP)
+      load_wfrags<BF16, MAXC>(wup, sup, [&](int k) { return wu ? wu[(int64_t)k * U.din_up] : 0.f; });
     load_wfrags<BF16, MAXC>(wrec, srec, [&](int k) { return wh[(int64_t)k * H]; });
   }
   // Gate-gradient threads: 0..255 -> row r0 + (tid >> 4), unit j0 + (tid & 15).
@@ -1000,8 +1006,9 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   };
   float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cprev = 0.f;
   BwdIdx s = bwd_step(tbs, toff, a.T, U.dir, 0);
-  unsigned uup[CPL * MAXC];
-  if (mma_wave) issue_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
+  unsigned uup[CPL * MU];
+  if constexpr (UP)
+    if (mma_wave) issue_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
   for (int k = 0; k < a.T; ++k) {
     BwdIdx nx = s;
     if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
@@ -1014,8 +1021,10 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     if (active && mma_wave) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       // Gradient arriving from the layer above (fetched one step ahead).
-      if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup, a.wait);
-      mma_segment<BF16, MAXC>(acc, uup, wup, sup);
+      if constexpr (UP) {
+        if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup, a.wait);
+        mma_segment<BF16, MAXC>(acc, uup, wup, sup);
+      }
       // Recurrent part.
       const unsigned roff =
           r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
@@ -1026,7 +1035,8 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[mw * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
-    if (k + 1 < a.T && mma_wave) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
+    if constexpr (UP)
+      if (k + 1 < a.T && mma_wave) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
@@ -1315,43 +1325,53 @@ constexpr int bwd_maxc_cap(int nw, bool bf16) {
   return nw == 16 ? (bf16 ? 8 : 16) : bwd_maxc_fit(nw, bf16);
 }
 
-template <int G, bool BF16, int NW, int M, bool SP>
+template <int G, bool BF16, int NW, int M, bool SP, bool UP>
 const void* bwd_kernel_m() {
   if constexpr (M <= bwd_maxc_cap(NW, BF16) && (!SP || NW >= 8) && (SP || NW != 8) &&
                 (M != 5 || (NW == 16 && !SP)))
-    return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, M, SP>);
+    return reinterpret_cast<const void*>(k_bwd_persistent<G, BF16, NW, M, SP, UP>);
   return nullptr;
 }
 
-template <int G, bool BF16, int NW, bool SP>
+template <int G, bool BF16, int NW, bool SP, bool UP>
 const void* bwd_kernel_nw(int maxc) {
   switch (maxc) {
-    case 1: return bwd_kernel_m<G, BF16, NW, 1, SP>();
-    case 2: return bwd_kernel_m<G, BF16, NW, 2, SP>();
-    case 3: return bwd_kernel_m<G, BF16, NW, 3, SP>();
-    case 4: return bwd_kernel_m<G, BF16, NW, 4, SP>();
-    case 5: return bwd_kernel_m<G, BF16, NW, 5, SP>();
-    case 8: return bwd_kernel_m<G, BF16, NW, 8, SP>();
-    case 16: return bwd_kernel_m<G, BF16, NW, 16, SP>();
+    case 1: return bwd_kernel_m<G, BF16, NW, 1, SP, UP>();
+    case 2: return bwd_kernel_m<G, BF16, NW, 2, SP, UP>();
+    case 3: return bwd_kernel_m<G, BF16, NW, 3, SP, UP>();
+    case 4: return bwd_kernel_m<G, BF16, NW, 4, SP, UP>();
+    case 5: return bwd_kernel_m<G, BF16, NW, 5, SP, UP>();
+    case 8: return bwd_kernel_m<G, BF16, NW, 8, SP, UP>();
+    case 16: return bwd_kernel_m<G, BF16, NW, 16, SP, UP>();
   }
   return nullptr;
 }
 
-template <int G, bool BF16>
+template <int G, bool BF16, bool UP>
 const void* bwd_kernel_g(int nw, int maxc, bool split) {
   switch (nw) {
-    case 4: return split ? nullptr : bwd_kernel_nw<G, BF16, 4, false>(maxc);
-    case 8: return split ? bwd_kernel_nw<G, BF16, 8, true>(maxc) : nullptr;
+    case 4: return split ? nullptr : bwd_kernel_nw<G, BF16, 4, false, UP>(maxc);
+    case 8: return split ? bwd_kernel_nw<G, BF16, 8, true, UP>(maxc) : nullptr;
     case 16:
-      return split ? bwd_kernel_nw<G, BF16, 16, true>(maxc) : bwd_kernel_nw<G, BF16, 16, false>(maxc);
+      return split ? bwd_kernel_nw<G, BF16, 16, true, UP>(maxc)
+                   : bwd_kernel_nw<G, BF16, 16, false, UP>(maxc);
   }
   return nullptr;
 }
 
-const void* bwd_kernel(int cell, bool bf16, int nw, int maxc, bool split) {
+const void* bwd_kernel(int cell, bool bf16, int nw, int maxc, bool split, bool up) {
+  if (up) {
+    if (cell == RNNBKT_CELL_LSTM)
+      return bf16 ? bwd_kernel_g<4, true, true>(nw, maxc, split)
+                  : bwd_kernel_g<4, false, true>(nw, maxc, split);
+    return bf16 ? bwd_kernel_g<3, true, true>(nw, maxc, split)
+                : bwd_kernel_g<3, false, true>(nw, maxc, split);
+  }
   if (cell == RNNBKT_CELL_LSTM)
-    return bf16 ? bwd_kernel_g<4, true>(nw, maxc, split) : bwd_kernel_g<4, false>(nw, maxc, split);
-  return bf16 ? bwd_kernel_g<3, true>(nw, maxc, split) : bwd_kernel_g<3, false>(nw, maxc, split);
+    return bf16 ? bwd_kernel_g<4, true, false>(nw, maxc, split)
+                : bwd_kernel_g<4, false, false>(nw, maxc, split);
+  return bf16 ? bwd_kernel_g<3, true, false>(nw, maxc, split)
+              : bwd_kernel_g<3, false, false>(nw, maxc, split);
 }
 
 struct BwdPlan {
@@ -1373,11 +1393,21 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
   if (a.T > kMaxSteps || a.nunits < 1 || a.nunits > kMaxUnits || a.H % kBwdUnits != 0) return p;
   if ((G * a.H) % ch != 0) return p;
   int nch = 0;
+  bool up = false;
   for (int q = 0; q < a.nunits; ++q) {
     const BwdUnit& u = a.u[q];
     if (u.rec_bytes >= kNoRow || (u.up && (u.k_up % ch != 0 || u.up_bytes >= kNoRow))) return p;
     nch = std::max(nch, std::max(u.up ? u.k_up / ch : 0, G * a.H / ch));
+    up = up || u.up != nullptr;
   }
+  // Without an input segment a wave's registers hold the recurrent segment
+  // only: a candidate fits when its compiled kernel needs no scratch.
+  auto fits_regs = [&](int nw, int m, bool split) {
+    if (up) return m <= bwd_maxc_fit(nw, bf16);
+    const void* k = bwd_kernel(cell, bf16, nw, m, split, false);
+    hipFuncAttributes fa{};
+    return k && hipFuncGetAttributes(&fa, k) == hipSuccess && fa.localSizeBytes == 0;
+  };
   struct Cand {
     int nw;
     bool split;
@@ -1388,7 +1418,7 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     const int per = (nch + nmma - 1) / nmma;
     int m = 1;  // slots per wave: 1, 2, 3 or a power of two
     while (m < per) m = m == 2 && per == 3 ? 3 : m * 2;
-    if (m > bwd_maxc_fit(c.nw, bf16)) continue;
+    if (!fits_regs(c.nw, m, c.split)) continue;
     const float cost = m + (c.split ? 0.f : 1.5f) + (c.nw == 16 ? 0.5f : c.nw == 8 ? 0.25f : 0.f);
     if (cost < best) {
       best = cost;
@@ -1421,7 +1451,7 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     p.blocks += p.wg_blocks;
     p.shmem = std::max(p.shmem, subs * kWgSubLds);
   }
-  p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc, p.split);
+  p.kernel = bwd_kernel(cell, bf16, p.nw, p.maxc, p.split, up);
   return p;
 }
 
