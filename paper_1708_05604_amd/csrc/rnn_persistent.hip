@@ -741,6 +741,24 @@ __device__ inline bool wg_clear(const u4 (&v)[2]) {
   return ok;
 }
 
+// Waits until element (k, c0) of A is published: one word, the same for
+// every thread (one load per wave), polled before whole K-tiles are read.
+__device__ inline void wg_wait_word(__amdgpu_buffer_rsrc_t r, int lda, int c0, int k,
+                                    const WaitCtl& w) {
+  const unsigned o = 4u * (unsigned)((int64_t)k * lda + c0);
+  unsigned x = __builtin_amdgcn_raw_buffer_load_b32(r, o, 0, kDeviceScope);
+  for (unsigned polls = 1; x == kSentinel; ++polls) {
+    __builtin_amdgcn_s_sleep(32);
+    poll_fence();
+    x = __builtin_amdgcn_raw_buffer_load_b32(r, o, 0, kDeviceScope);
+    if ((polls & 1023u) == 0 && waits_abandoned(w)) return;
+    if (polls >= w.max_polls) {
+      note_timeout(w);
+      return;
+    }
+  }
+}
+
 // Re-reads this thread's part of an A K-tile until it is all published.
 __device__ inline void wg_settle_a(u4 (&v)[2], __amdgpu_buffer_rsrc_t r, int lda, int c0,
                                    int clim, int k0, int klim, int tid, const WaitCtl& w) {
@@ -841,6 +859,11 @@ __device__ void wgrad_role(const WgStreamArgs& a, int wb, float* lds, const Wait
     const int kbeg = a.off[t_lo], kend = a.off[t_hi];
     u4 ua[2];
     f4 rb[2];
+    // The chunk's last frame, first column of the tile: published at about
+    // the time the rest of the chunk is, and one word to poll instead of
+    // whole K-tiles while the recurrence has not reached the chunk yet (the
+    // per-element check below stays the test of completeness).
+    wg_wait_word(ra, J.lda, m0, kend - 1, w);
     wg_load_a(ua, ra, J.lda, m0, J.M, kbeg, kend, tid);
     wg_load_b(rb, J.B, J.ldb, J.gather, n0, J.N, kbeg, kend, tid);
     for (int k0 = kbeg; k0 < kend; k0 += kWgBK) {
