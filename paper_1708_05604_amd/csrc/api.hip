@@ -964,17 +964,20 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   };
   const uint64_t rec_b = sizeof(float) * (uint64_t)N * GH;
   const uint32_t rec_bytes = rec_b < 0x7FFFFFF0u ? (uint32_t)rec_b : 0x7FFFFFF0u;
-  // Unit (layer l, direction d) of a persistent backward launch.
-  auto make_unit = [&](int l, int d, const float* dh, bool up_published, bool publish_dax) {
+  // Unit (layer l, direction d) of a persistent backward launch.  up: the
+  // layer above runs in the same launch (unidirectional stacks), and this
+  // layer multiplies its gate gradients by W_ih of that layer as they are
+  // published.
+  auto make_unit = [&](int l, int d, const float* dh, bool up, bool publish_dax) {
     BwdUnit u{};
     const int ld = l * s.dirs + d;
-    if (s.dirs == 1 && l + 1 < s.L) {
+    if (up) {
       u.up = da_of(l + 1, 0);
       u.wih_up = params + po.wih[l + 1];
       u.k_up = GH;
       u.din_up = s.din(l + 1);
       u.up_bytes = rec_bytes;
-      u.up_published = up_published ? 1 : 0;
+      u.up_published = 1;
     }
     u.whh = params + po.whh[ld];
     u.dh_in = dh;
@@ -1006,7 +1009,11 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   // Launch plan: unidirectional stacks run top-down, as many layers per
   // launch as stay resident (each layer reads the one above as it is
   // published); bidirectional layers run one layer (both directions) per
-  // launch with the gradient from above computed by a GEMM in between.
+  // launch.  Between launches the gradient w.r.t. the lower layer's output
+  // is a GEMM (dX = dA W_ih of the launch's lowest layer), which the next
+  // launch's top layer reads like dH of the output layer: an input segment
+  // multiplied inside the recurrence would double the weight fragments a
+  // wave holds and spill them for wide layers.
   struct Group {
     int hi, n;
   };
@@ -1021,7 +1028,8 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
         BwdLaunch Lc = base_launch();
         for (int q = 0; q < n; ++q)
           for (int d = 0; d < s.dirs; ++d)
-            Lc.u[q * s.dirs + d] = make_unit(hi - q, d, dha, q > 0, gru && q + 1 < n);
+            Lc.u[q * s.dirs + d] = make_unit(hi - q, d, q == 0 ? dha : nullptr,
+                                             s.dirs == 1 && q > 0, gru && q + 1 < n);
         Lc.nunits = n * s.dirs;
         if (bwd_persistent_blocks(Lc, s.cell, s.bf16, B) > 0) best = n;
       }
@@ -1031,8 +1039,10 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
     }
   }
   if (noalloc) {
-    // A resident plan of a unidirectional stack uses only the first bytes.
-    const size_t need = (persistent && s.dirs == 1) ? c.ws_bwd_resident_uni : c.ws_bwd;
+    // A resident plan of a unidirectional stack in one launch uses only the
+    // first bytes.
+    const size_t need =
+        (persistent && s.dirs == 1 && groups.size() == 1) ? c.ws_bwd_resident_uni : c.ws_bwd;
     RNNBKT_REQUIRE(need <= workspace_bytes, RNNBKT_EUNSUPPORTED,
                    "lstm_bwd_noalloc: this batch needs %zu bytes of scratch, above the %zu "
                    "the library holds",
@@ -1119,15 +1129,15 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       for (int q = 0; q < g.n; ++q) {
         const int l = g.hi - q;
         // Only the group's top layer reads a plain gradient from above: dH of
-        // the output layer, or (bidirectional) the dX GEMM of the layer above.
-        const float* dh = (q == 0 && (l == s.L - 1 || s.dirs == 2)) ? dh_in : nullptr;
+        // the output layer, or the dX GEMM after the launch above.
+        const float* dh = q == 0 ? dh_in : nullptr;
         for (int d = 0; d < s.dirs; ++d)
-          Lc.u[q * s.dirs + d] = make_unit(l, d, dh, q > 0, gru && q + 1 < g.n);
+          Lc.u[q * s.dirs + d] = make_unit(l, d, dh, s.dirs == 1 && q > 0, gru && q + 1 < g.n);
       }
       Lc.nunits = g.n * s.dirs;
       double fl = 0;
       for (int q = 0; q < g.n; ++q) {
-        const double kup = (s.dirs == 1 && g.hi - q + 1 < s.L) ? GH : 0;
+        const double kup = (s.dirs == 1 && q > 0) ? GH : 0;
         for (int t = 0; t < T; ++t) fl += 2.0 * s.dirs * bs[t] * (kup + GH) * s.H;
       }
       if (!prefilled) {
@@ -1198,14 +1208,16 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
         RNNBKT_HIP(launch_bwd_persistent(Lc, s.cell, s.bf16, B, st, &fits));
       }
       RNNBKT_REQUIRE(fits, RNNBKT_EHIP, "lstm_bwd: persistent launch no longer fits");
-      // Bidirectional: gradient w.r.t. the layer below's output, both directions.
+      // Gradient w.r.t. the output of the layer below the launch's lowest
+      // layer: dX = dA W_ih (bidirectional: dA_fwd W_ih,fwd + dA_bwd W_ih,bwd,
+      // one GEMM with two terms).
       const int lo = g.hi - g.n + 1;
-      if (s.dirs == 2 && lo > 0) {
-        // dX = dA_fwd W_ih,fwd + dA_bwd W_ih,bwd: one GEMM with two terms.
-        const Term2 t2{da_of(lo, 1), GH, params + po.wih[lo * 2 + 1], s.din(lo), GH};
-        RNNBKT_HIP(gemm(da_of(lo, 0), GH, true, params + po.wih[lo * 2], s.din(lo), false, dx,
-                        s.din(lo), n, s.din(lo), GH, nullptr, 0, s.bf16, st, nullptr, nullptr,
-                        &t2));
+      if (lo > 0) {
+        Term2 t2{};
+        if (s.dirs == 2) t2 = Term2{da_of(lo, 1), GH, params + po.wih[lo * 2 + 1], s.din(lo), GH};
+        RNNBKT_HIP(gemm(da_of(lo, 0), GH, true, params + po.wih[lo * s.dirs], s.din(lo), false,
+                        dx, s.din(lo), n, s.din(lo), GH, nullptr, 0, s.bf16, st, nullptr, nullptr,
+                        s.dirs == 2 ? &t2 : nullptr));
         dh_in = dx;
         std::swap(dx, spare);
       }
