@@ -254,6 +254,52 @@ def timed_replicated(ep, rep, warmup, steps, torch):
     return useful, secs
 
 
+def latency_floor(w, ep, state, kinds, torch, dev, reps=3):
+    """Latency floor of the recurrences: (sequential step phases of the epoch)
+    x (minimum time per step at M = B).  The minimum is measured on the same
+    resident kernels over a batch of B sequences that all have the epoch's
+    longest length (capped by the staged buffers), where no row group ever
+    idles and the launch prologue is spread over the most steps; the phases
+    are the epoch's launches per batch times each batch's step count.
+    floor_frac = floor / measured recurrence time of the epoch."""
+    desc, params, grads, reserve, workspace, loss = state[:6]
+    nb = len(ep.batches)
+    B = w.batch
+    T0 = min(ep.max_T, ep.max_N // B)
+    gen = torch.Generator().manual_seed(1)
+    x = (0.5 * torch.randn(T0, B, w.input_dim, generator=gen)).to(dev)
+    y = torch.randint(0, w.num_classes, (T0, B), generator=gen, dtype=torch.int32).to(dev)
+    L = np.full(B, T0, np.int32)
+    g2 = torch.zeros_like(grads)
+
+    def once():
+        lib.lstm_fwd(desc, params, x, y, L, reserve, workspace, loss)
+        lib.lstm_bwd(desc, params, L, reserve, workspace, g2)
+
+    once()
+    torch.cuda.synchronize()
+    lib.kernel_timer(True)
+    for _ in range(reps):
+        once()
+    torch.cuda.synchronize()
+    lib.kernel_timer(False)
+    lib.sync_check()
+    t_sum = sum(int(Lb[0]) for Lb in ep.lens)
+    out = {"uniform_batch": {"B": B, "T": T0, "reps": reps}}
+    for kind in ("fwd", "bwd"):
+        u = lib.kernel_timer_read("step_" + kind)
+        per_call = max(1, round(u["launches"] / reps))
+        t_min_us = 1e3 * u["ms"] / (reps * T0 * per_call)
+        per_batch = max(1, round(kinds["step_" + kind]["launches"] / nb))
+        phases = per_batch * t_sum
+        floor_ms = phases * t_min_us / 1e3
+        measured_ms = kinds["step_" + kind]["ms"]
+        out[kind] = {"min_us_per_step": t_min_us, "launches_per_batch": per_batch,
+                     "step_phases": phases, "floor_ms": floor_ms, "measured_ms": measured_ms,
+                     "floor_frac": floor_ms / measured_ms}
+    return out
+
+
 def cpu_sample(w, data, K):
     """The oracle baseline's fixed batch order: the first batch of every
     bucket of epoch 0 (shortest bucket first), then the batch holding the
@@ -555,6 +601,8 @@ def main(argv=None):
         out["recurrence_us_per_timestep"] = {
             "fwd": 1e3 * kinds["step_fwd"]["ms"] / t_sum,
             "bwd": 1e3 * kinds["step_bwd"]["ms"] / t_sum}
+        if args.recurrence == "resident" and args.loss == "frame":
+            out["latency_floor"] = latency_floor(w, ep, state, kinds, torch, dev)
     if cpu is not None:
         out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
