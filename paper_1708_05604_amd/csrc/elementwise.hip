@@ -174,7 +174,11 @@ constexpr int kXentRowsPerWave = 4;
 constexpr int kXentWaves = 4;
 constexpr int kXentMaxPerLane = 16;  // C <= 1024
 
-// One wave per frame: max, log-sum-exp, loss term and gradient row.
+// A wave per kXentRowsPerWave frames: max, log-sum-exp, loss term and
+// gradient row of each.  MPL = ceil(C / 64) elements per lane and row; the
+// loads of all the wave's rows are issued before any reduction, so a wave
+// waits for memory once rather than once per row.
+template <int MPL>
 __global__ __launch_bounds__(256) void k_softmax_xent(float* __restrict__ z,
                                                       const int32_t* __restrict__ y, int64_t N,
                                                       int C, float inv_n,
@@ -182,41 +186,49 @@ __global__ __launch_bounds__(256) void k_softmax_xent(float* __restrict__ z,
   __shared__ float wsum[kXentWaves];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t base = ((int64_t)blockIdx.x * kXentWaves + wave) * kXentRowsPerWave;
+  float v[kXentRowsPerWave][MPL];
+  int label[kXentRowsPerWave];
+#pragma unroll
+  for (int rr = 0; rr < kXentRowsPerWave; ++rr) {
+    const int64_t f = base + rr;
+    const bool ok = f < N;
+    label[rr] = ok ? y[f] : 0;
+#pragma unroll
+    for (int i = 0; i < MPL; ++i) {
+      const int c = lane + 64 * i;
+      v[rr][i] = ok && c < C ? z[f * C + c] : -INFINITY;
+    }
+  }
   float acc = 0.f;
+#pragma unroll
   for (int rr = 0; rr < kXentRowsPerWave; ++rr) {
     const int64_t f = base + rr;
     if (f >= N) break;
-    float* row = z + f * C;
-    float v[kXentMaxPerLane];
     float m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < kXentMaxPerLane; ++i) {
-      const int c = lane + 64 * i;
-      v[i] = c < C ? row[c] : -INFINITY;
-      m = fmaxf(m, v[i]);
-    }
+    for (int i = 0; i < MPL; ++i) m = fmaxf(m, v[rr][i]);
     m = wave_max(m);
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < kXentMaxPerLane; ++i) {
+    for (int i = 0; i < MPL; ++i) {
       const int c = lane + 64 * i;
-      if (c < C) s += expf(v[i] - m);
+      if (c < C) s += expf(v[rr][i] - m);
     }
     s = wave_sum(s);
     const float lse = m + logf(s);
-    const int label = y[f];
     float zy = 0.f;
+    float* row = z + f * C;
 #pragma unroll
-    for (int i = 0; i < kXentMaxPerLane; ++i) {
+    for (int i = 0; i < MPL; ++i) {
       const int c = lane + 64 * i;
       if (c < C) {
-        if (c == label) zy = v[i];
-        const float p = expf(v[i] - lse);
-        row[c] = (p - (c == label ? 1.f : 0.f)) * inv_n;
+        if (c == label[rr]) zy = v[rr][i];
+        const float p = expf(v[rr][i] - lse);
+        row[c] = (p - (c == label[rr] ? 1.f : 0.f)) * inv_n;
       }
     }
     zy = wave_sum(zy);
-    acc += (label >= 0 && label < C) ? lse - zy : NAN;
+    acc += (label[rr] >= 0 && label[rr] < C) ? lse - zy : NAN;
   }
   if (lane == 0) wsum[wave] = acc;
   __syncthreads();
@@ -436,8 +448,21 @@ hipError_t launch_softmax_xent(float* z, const int32_t* y, int64_t N, int32_t C,
   const int64_t rows_per_block = kXentRowsPerWave * kXentWaves;
   const int blocks = (int)((N + rows_per_block - 1) / rows_per_block);
   *num_partials = blocks;
-  hipLaunchKernelGGL(k_softmax_xent, dim3(blocks), dim3(256), 0, st, z, y, N, C,
-                     1.0f / (float)N, partial);
+  const int mpl = (C + 63) / 64;
+  const dim3 g(blocks), t(256);
+  const float inv_n = 1.0f / (float)N;
+  if (mpl <= 1)
+    hipLaunchKernelGGL(k_softmax_xent<1>, g, t, 0, st, z, y, N, C, inv_n, partial);
+  else if (mpl <= 2)
+    hipLaunchKernelGGL(k_softmax_xent<2>, g, t, 0, st, z, y, N, C, inv_n, partial);
+  else if (mpl <= 4)
+    hipLaunchKernelGGL(k_softmax_xent<4>, g, t, 0, st, z, y, N, C, inv_n, partial);
+  else if (mpl <= 8)
+    hipLaunchKernelGGL(k_softmax_xent<8>, g, t, 0, st, z, y, N, C, inv_n, partial);
+  else if (mpl <= kXentMaxPerLane)
+    hipLaunchKernelGGL(k_softmax_xent<kXentMaxPerLane>, g, t, 0, st, z, y, N, C, inv_n, partial);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
