@@ -141,8 +141,9 @@ __device__ inline void load_wfrags(typename WFrag<BF16>::T (&w)[MAXC], const Slo
 // Issues the lane's loads of one segment: piece v of slot i is read at byte
 // offset row_off + 4*(c*CH + koff + 4v) of the array behind `r` when the row
 // exists (row_off != kNoRow) and the piece starts below klim; other pieces
-// read zero.
-template <bool BF16, int MAXC>
+// read zero.  AUX: the loads' cache policy -- device scope for arrays that
+// other workgroups of the launch publish, 0 (cached) for complete ones.
+template <bool BF16, int MAXC, int AUX = kDeviceScope>
 __device__ inline void issue_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
                                      int klim, unsigned (&u)[Chunk<BF16>::CPL * MAXC]) {
   constexpr int CH = Chunk<BF16>::CH;
@@ -155,7 +156,7 @@ __device__ inline void issue_segment(__amdgpu_buffer_rsrc_t r, unsigned row_off,
       const int kk = c * CH + sl.koff + 4 * v;
       const unsigned o =
           (row_off != kNoRow && c < sl.nchunks && kk < klim) ? row_off + 4u * (unsigned)kk : kNoRow;
-      const u4 x = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, kDeviceScope);
+      const u4 x = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, AUX);
 #pragma unroll
       for (int e = 0; e < 4; ++e) u[(i * NV + v) * 4 + e] = x[e];
     }
@@ -492,7 +493,13 @@ __device__ inline void load_tables(const int32_t* bs, const int32_t* off, int T,
 // the state), so one MFMA tile per block yields every pre-activation a
 // unit's update needs.  NW waves split each segment's reduction; waves
 // 0..NT-1 then run the state update of one column block each.
-template <int G, bool BF16, int NW, int MAXC, int NT>
+// MAXC: slots per wave of the widest segment; MR (<= MAXC): slots of the
+// recurrent segment, whose poll is on the step's critical path and is
+// compiled for its own width.  MR < MAXC only where no unit of the launch
+// reads an input that the launch publishes: the input is then read through
+// the caches (the workgroups of a row group share one XCD and read the
+// same input rows).
+template <int G, bool BF16, int NW, int MAXC, int NT, int MR>
 __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   constexpr int CH = Chunk<BF16>::CH;
   constexpr int CPL = Chunk<BF16>::CPL;
@@ -537,7 +544,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   const Slots srec{wave, NW, H / CH, lq * CPL};
 
   // Weight fragments: this lane feeds column lr of every column block.
-  typename WFrag<BF16>::T win[NT][MAXC], wrec[NT][MAXC];
+  typename WFrag<BF16>::T win[NT][MAXC], wrec[NT][MR];
   {
     const int grp = lr >> 2, uu = lr & 3;
 #pragma unroll
@@ -549,7 +556,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
       const float* wi = gi >= 0 ? U.wih + (int64_t)(gi * H + j) * U.kin : nullptr;
       const float* wh = gh >= 0 ? U.whh + (int64_t)(gh * H + j) * H : nullptr;
       load_wfrags<BF16, MAXC>(win[nt], sin, [&](int k) { return (wi && k < U.kin) ? wi[k] : 0.f; });
-      load_wfrags<BF16, MAXC>(wrec[nt], srec, [&](int k) { return wh ? wh[k] : 0.f; });
+      load_wfrags<BF16, MR>(wrec[nt], srec, [&](int k) { return wh ? wh[k] : 0.f; });
     }
   }
   // State-update lanes: wave nt < NT owns row r0 + (lane >> 2), unit
@@ -585,7 +592,10 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   };
   StepIdx s = fwd_step(tbs, toff, a.T, U.dir, 0);
   unsigned uin[CPL * MAXC];
-  issue_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin);
+  auto issue_in = [&](const StepIdx& q) {
+    issue_segment<BF16, MAXC, MR < MAXC ? 0 : kDeviceScope>(rin, in_off(q), sin, U.kin, uin);
+  };
+  issue_in(s);
   for (int k = 0; k < a.T; ++k) {
     StepIdx nx = s;
     if (k + 1 < a.T) nx = fwd_step(tbs, toff, a.T, U.dir, k + 1);
@@ -595,25 +605,27 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
       // Input part (fetched one step ahead; a published input may still be
-      // arriving).
+      // arriving), then the recurrent poll.  (Polling first and multiplying
+      // the input while the poll is in flight made bilstm3's upper-layer
+      // launches slower: 1.92 against 1.37 ms.)
       if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin, a.wait);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
       // Recurrent part.
       const unsigned roff =
           r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + U.hcol) : kNoRow;
-      unsigned urec[CPL * MAXC];
-      issue_segment<BF16, MAXC>(rout, roff, srec, H, urec);
-      settle_segment<BF16, MAXC>(rout, roff, srec, H, urec, a.wait);
+      unsigned urec[CPL * MR];
+      issue_segment<BF16, MR>(rout, roff, srec, H, urec);
+      settle_segment<BF16, MR>(rout, roff, srec, H, urec, a.wait);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        mma_segment<BF16, MAXC>(acc[nt], urec, wrec[nt], srec);
+        mma_segment<BF16, MR>(acc[nt], urec, wrec[nt], srec);
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           red[(wave * NT + nt) * 256 + (lq * 4 + q) * 16 + lr] = acc[nt][q];
       }
     }
-    if (k + 1 < a.T) issue_segment<BF16, MAXC>(rin, in_off(nx), sin, U.kin, uin);
+    if (k + 1 < a.T) issue_in(nx);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const int rr = lane >> 2, u4_ = lane & 3;
@@ -1232,29 +1244,45 @@ int fwd_maxc(int nch, bool bf16) {
   return m <= (bf16 ? 8 : 16) ? m : 0;
 }
 
-template <int G, bool BF16, int NT>
-const void* fwd_kernel_nt(int maxc) {
-  switch (maxc) {
-    case 1: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 1, NT>);
-    case 2: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 2, NT>);
-    case 4: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 4, NT>);
-    case 8: return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 8, NT>);
-  }
-  if constexpr (!BF16)
-    if (maxc == 16) return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, 16, NT>);
+// mr: the recurrent segment's slots, maxc or (an input segment twice as
+// wide, complete before the launch) maxc / 2.
+template <int G, bool BF16, int NT, int M>
+const void* fwd_kernel_m(int mr) {
+  if (mr == M) return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, M, NT, M>);
+  if constexpr (M >= 4 && M <= 8)
+    if (mr == M / 2) return reinterpret_cast<const void*>(k_fwd_persistent<G, BF16, 4, M, NT, M / 2>);
   return nullptr;
 }
 
-const void* fwd_kernel(int cell, bool bf16, int nt, int maxc) {
+template <int G, bool BF16, int NT>
+const void* fwd_kernel_nt(int maxc, int mr) {
+  switch (maxc) {
+    case 1: return fwd_kernel_m<G, BF16, NT, 1>(mr);
+    case 2: return fwd_kernel_m<G, BF16, NT, 2>(mr);
+    case 4: return fwd_kernel_m<G, BF16, NT, 4>(mr);
+    case 8: return fwd_kernel_m<G, BF16, NT, 8>(mr);
+  }
+  if constexpr (!BF16)
+    if (maxc == 16) return fwd_kernel_m<G, BF16, NT, 16>(mr);
+  return nullptr;
+}
+
+const void* fwd_kernel(int cell, bool bf16, int nt, int maxc, int mr) {
   if (cell == RNNBKT_CELL_LSTM) {
     if (nt == 3) return nullptr;
-    if (nt == 4) return bf16 ? fwd_kernel_nt<4, true, 4>(maxc) : nullptr;
-    if (bf16) return nt == 1 ? fwd_kernel_nt<4, true, 1>(maxc) : fwd_kernel_nt<4, true, 2>(maxc);
-    return nt == 1 ? fwd_kernel_nt<4, false, 1>(maxc) : fwd_kernel_nt<4, false, 2>(maxc);
+    if (nt == 4) return bf16 ? fwd_kernel_nt<4, true, 4>(maxc, mr) : nullptr;
+    if (bf16)
+      return nt == 1 ? fwd_kernel_nt<4, true, 1>(maxc, mr)
+                     : fwd_kernel_nt<4, true, 2>(maxc, mr);
+    return nt == 1 ? fwd_kernel_nt<4, false, 1>(maxc, mr)
+                   : fwd_kernel_nt<4, false, 2>(maxc, mr);
   }
-  if (nt >= 3) return bf16 || nt == 4 ? nullptr : fwd_kernel_nt<3, false, 3>(maxc);
-  if (bf16) return nt == 1 ? fwd_kernel_nt<3, true, 1>(maxc) : fwd_kernel_nt<3, true, 2>(maxc);
-  return nt == 1 ? fwd_kernel_nt<3, false, 1>(maxc) : fwd_kernel_nt<3, false, 2>(maxc);
+  if (nt >= 3) return bf16 || nt == 4 ? nullptr : fwd_kernel_nt<3, false, 3>(maxc, mr);
+  if (bf16)
+    return nt == 1 ? fwd_kernel_nt<3, true, 1>(maxc, mr)
+                   : fwd_kernel_nt<3, true, 2>(maxc, mr);
+  return nt == 1 ? fwd_kernel_nt<3, false, 1>(maxc, mr)
+                 : fwd_kernel_nt<3, false, 2>(maxc, mr);
 }
 
 // Workgroups of a recurrence grid of nc clusters of S (see cluster_block).
@@ -1264,7 +1292,7 @@ int rec_grid(int nc, int S) {
 
 struct FwdPlan {
   const void* kernel;
-  int nt, maxc, blocks;
+  int nt, maxc, mr, blocks;
   size_t shmem;
 };
 
@@ -1275,18 +1303,28 @@ struct FwdPlan {
 // 32 of them sharing a CU), and the row-group clusters are kept whole on
 // one XCD (rec_grid).
 FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
-  FwdPlan p{nullptr, 0, 0, 0, 0};
+  FwdPlan p{};
   const int ch = bf16 ? 32 : 16;
   if (a.T > kMaxSteps || a.nunits < 1 || a.nunits > kMaxUnits || a.H % ch != 0) return p;
   int nch = 0;
+  bool published = false;
   for (int q = 0; q < a.nunits; ++q) {
     const FwdUnit& u = a.u[q];
     if (u.kin < 1 || u.kin % 4 != 0 || u.in_bytes >= kNoRow || u.out_bytes >= kNoRow) return p;
     nch = std::max(nch, std::max((u.kin + ch - 1) / ch, a.H / ch));
+    published = published || u.in_published;
   }
   p.nt = a.H >= 256 && a.H % 8 == 0 ? 2 : 1;
   p.maxc = fwd_maxc(nch, bf16);
   if (p.maxc == 0) return p;
+  // An input segment twice as wide as the recurrent one, complete before
+  // the launch: the recurrent poll and products compiled for their own
+  // width, and the input read through the caches (bilstm3's upper layers,
+  // input 2H: 1.50 -> 1.37 ms per launch with the narrower recurrent code,
+  // -> 1.23 ms with cached input reads; cached reads of a launch-complete
+  // input as wide as the layer, gru2's and longtail's second layers,
+  // changed nothing).
+  p.mr = !published && fwd_maxc(a.H / ch, bf16) * 2 == p.maxc ? p.maxc / 2 : p.maxc;
   p.blocks = a.nunits * (a.H / (4 * p.nt)) * ((B + 15) / 16);
   p.shmem = sizeof(float) * 4 * p.nt * 256 + sizeof(int32_t) * (2 * a.T + 1);
   size_t out_lds = 0;
@@ -1296,11 +1334,11 @@ FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
     p.blocks += a.out_blocks;
     p.shmem = std::max(p.shmem, out_lds);
   }
-  p.kernel = fwd_kernel(cell, bf16, p.nt, p.maxc);
+  p.kernel = fwd_kernel(cell, bf16, p.nt, p.maxc, p.mr);
   // Wider workgroups: 12 units for an fp32 GRU, 16 for a bf16 LSTM.
   const int wide = cell == RNNBKT_CELL_GRU ? (bf16 ? 0 : 3) : (bf16 ? 4 : 0);
   if (wide > 0 && p.nt == 2 && a.H % (4 * wide) == 0 && p.blocks > cu_count()) {
-    const void* kw = fwd_kernel(cell, bf16, wide, p.maxc);
+    const void* kw = fwd_kernel(cell, bf16, wide, p.maxc, p.mr);
     const int bw = rec_grid(a.nunits * ((B + 15) / 16), a.H / (4 * wide)) + a.out_blocks;
     const size_t shw =
         std::max(sizeof(float) * 4 * wide * 256 + sizeof(int32_t) * (2 * a.T + 1), out_lds);
