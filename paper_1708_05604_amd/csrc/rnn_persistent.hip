@@ -1040,6 +1040,13 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     }
   };
   float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cprev = 0.f;
+  // Without the split the gate-gradient waves also poll, and loads complete
+  // in issue order, so operands fetched at the top of a step hold up that
+  // wave's poll: with few slots per wave they are fetched one step ahead,
+  // after the step's poll has completed (bilstm3's backward, 2 slots: 1.94
+  // -> 1.71 ms per launch; with 4 slots, longtail's, it was slower: 1.36 ->
+  // 1.42).  With the split, fetching them ahead measured slower too.
+  constexpr bool kAheadOps = !SPLIT && MAXC <= 2;
   BwdIdx s = bwd_step(tbs, toff, a.T, U.dir, 0);
   unsigned uup[CPL * MU];
   if constexpr (UP)
@@ -1050,9 +1057,13 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     const bool active = r0 < s.rows;
     const int64_t f = erow < s.rows ? s.row0 + erow : 0;
     const bool has_prev = erow < s.prev_rows;
-    // Loaded at the top of the step.  (With the split, fetching them one
-    // step ahead instead measured slower.)
-    if (epi) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
+    // Loaded at the top of the step, or (kAheadOps) one step ahead.
+    if constexpr (!kAheadOps) {
+      if (epi) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
+    } else {
+      if (epi && k == 0) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
+    }
+    float ndhv = 0.f, nst0 = 0.f, nst1 = 0.f, nst2 = 0.f, nst3 = 0.f, ncc = 0.f, ncprev = 0.f;
     if (active && mma_wave) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       // Gradient arriving from the layer above (fetched one step ahead).
@@ -1072,6 +1083,8 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     }
     if constexpr (UP)
       if (k + 1 < a.T && mma_wave) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
+    if constexpr (kAheadOps)
+      if (epi && k + 1 < a.T) fetch_ops(nx, ndhv, nst0, nst1, nst2, nst3, ncc, ncprev);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
@@ -1134,6 +1147,15 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       }
     }
     s = nx;
+    if constexpr (kAheadOps) {
+      dhv = ndhv;
+      st0 = nst0;
+      st1 = nst1;
+      st2 = nst2;
+      st3 = nst3;
+      cc = ncc;
+      cprev = ncprev;
+    }
     __syncthreads();  // red is rewritten by the next step
   }
   // Bias gradients of this workgroup: sum its 16 rows in a fixed order and
@@ -1493,9 +1515,12 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
       p.split = c.split;
     }
   }
-  if (p.nw == 0) {
+  if (p.nw == 0 && !up) {
     // Very wide layers: 16 polling waves with spilled registers (5 slots
-    // spill far less than 8, e.g. for 72 chunks).
+    // spill far less than 8, e.g. for 72 chunks).  Not for a launch with an
+    // input segment: the caller then runs the layers in launches of their
+    // own, with the gradient between them from a GEMM (gru2's small batches,
+    // whose two layers would otherwise share a launch with 12 VGPRs spilled).
     const int per = (nch + 15) / 16;
     int m = per == 5 ? 5 : 1;
     while (m < per) m *= 2;
