@@ -418,8 +418,9 @@ struct Term2 {
 hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t ldb, bool b_kc,
                 float* C, int64_t ldc, int M, int N, int K, const float* bias, int accumulate,
                 bool bf16, hipStream_t st, const int32_t* gather = nullptr,
-                float* splitk_buf = nullptr, const Term2* t2 = nullptr) {
+                float* splitk_buf = nullptr, const Term2* t2 = nullptr, bool beside = false) {
   GemmArgs g{};
+  g.beside = beside ? 1 : 0;
   if (t2) {
     g.A2 = t2->A2;
     g.lda2 = t2->lda2;
@@ -1016,6 +1017,7 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   // wave holds and spill them for wide layers.
   struct Group {
     int hi, n;
+    bool frees_cus;  // its resident grid leaves CUs free for work beside it
   };
   std::vector<Group> groups;
   bool persistent = use_persistent();
@@ -1023,6 +1025,7 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
     int hi = s.L - 1;
     while (hi >= 0 && persistent) {
       int best = 0;
+      bool frees = false;
       const int maxn = s.dirs == 1 ? std::min(kMaxUnits, hi + 1) : 1;
       for (int n = 1; n <= maxn; ++n) {
         BwdLaunch Lc = base_launch();
@@ -1031,10 +1034,14 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
             Lc.u[q * s.dirs + d] = make_unit(hi - q, d, q == 0 ? dha : nullptr,
                                              s.dirs == 1 && q > 0, gru && q + 1 < n);
         Lc.nunits = n * s.dirs;
-        if (bwd_persistent_blocks(Lc, s.cell, s.bf16, B) > 0) best = n;
+        const int blocks = bwd_persistent_blocks(Lc, s.cell, s.bf16, B);
+        if (blocks > 0) {
+          best = n;
+          frees = blocks < cu_count();
+        }
       }
       if (best == 0) persistent = false;
-      groups.push_back({hi, best});
+      groups.push_back({hi, best, frees});
       hi -= best;
     }
   }
@@ -1076,7 +1083,8 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   auto wait_join = [&]() { return split ? hipStreamWaitEvent(st, side.join, 0) : hipSuccess; };
   RNNBKT_HIP(fork());
   RNNBKT_HIP(gemm(dz, s.C, false, top, s.Htop, false, grads + po.wout, s.Htop, s.C, s.Htop, n,
-                  nullptr, 0, s.bf16, side.s, nullptr, at<float>(workspace, c.splitk_out)));
+                  nullptr, 0, s.bf16, side.s, nullptr, at<float>(workspace, c.splitk_out),
+                  nullptr, split && persistent && groups.front().frees_cus));
   {
     Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, side.s);
     RNNBKT_HIP(launch_colsum(dz, N, s.C, s.C, colsum_rows(N), at<float>(workspace, c.colsum_out),
@@ -1097,7 +1105,9 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   // over every valid frame: dW_ih on s_ih with split-K buffer buf_ih, dW_hh
   // on s_hh with the buffer of its own stream's products.
   float* sk_rec = at<float>(workspace, c.splitk_rec);
-  auto layer_wgrad = [&](int l, hipStream_t s_ih, float* buf_ih, hipStream_t s_hh) -> hipError_t {
+  // beside: the products run beside the recurrence of the layers below.
+  auto layer_wgrad = [&](int l, hipStream_t s_ih, float* buf_ih, hipStream_t s_hh,
+                         bool beside) -> hipError_t {
     const float* xin = l == 0 ? Xp : at<float>(reserve, c.hout[l - 1]);
     const int din = s.din(l);
     const float* hout = at<float>(reserve, c.hout[l]);
@@ -1106,10 +1116,10 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       const float* dax = da_of(l, d);
       const float* dahh = gru ? dah_of(l, d) : dax;
       hipError_t e = gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
-                          nullptr, 0, s.bf16, s_ih, nullptr, buf_ih);
+                          nullptr, 0, s.bf16, s_ih, nullptr, buf_ih, nullptr, beside);
       if (e != hipSuccess) return e;
       e = gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld], s.H, GH,
-               s.H, n, nullptr, 0, s.bf16, s_hh, d == 0 ? pf : pr, sk_rec);
+               s.H, n, nullptr, 0, s.bf16, s_hh, d == 0 ? pf : pr, sk_rec, nullptr, beside);
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -1228,7 +1238,7 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       if (split && !streamw && &g != &groups.back()) {
         RNNBKT_HIP(fork());
         for (int q = 0; q < g.n; ++q) {
-          RNNBKT_HIP(layer_wgrad(g.hi - q, side.s, sk_rec, side.s));
+          RNNBKT_HIP(layer_wgrad(g.hi - q, side.s, sk_rec, side.s, (&g + 1)->frees_cus));
           wg_done[g.hi - q] = 1;
         }
       }
@@ -1327,7 +1337,7 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   // stream (own split-K buffer), overlapping the other stream's products.
   if (!streamw) RNNBKT_HIP(fork());
   for (int l = 0; l < s.L; ++l) {
-    if (!streamw && !wg_done[l]) RNNBKT_HIP(layer_wgrad(l, st, sk, side.s));
+    if (!streamw && !wg_done[l]) RNNBKT_HIP(layer_wgrad(l, st, sk, side.s, false));
     for (int d = 0; d < s.dirs; ++d) {
       const int ld = l * s.dirs + d;
       const float* dax = da_of(l, d);

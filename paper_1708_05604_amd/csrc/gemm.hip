@@ -433,10 +433,17 @@ __device__ inline int xcd_logical(int b, int n) {
   return x * per + min(x, rem) + b / 8;
 }
 
-template <bool A_KC, bool B_KC>
+// SUB: K-tiles of 32 loaded per stage (the loads of a stage are waited for
+// one stage after they are issued).  SUB = 2 doubles the LDS, so two
+// workgroups fit a CU instead of three: slower alone, but the GEMMs that run
+// beside a resident recurrence (on the CUs it leaves free) then slow its
+// exchange less (bilstm3's backward launches 1.71 -> 1.60 ms).  The caller
+// chooses it only for work beside a grid that leaves CUs free.
+template <bool A_KC, bool B_KC, int SUB>
 __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) __bf16 As[2][TBM * TB_LD];
-  __shared__ __attribute__((aligned(16))) __bf16 Bs[2][TBM * TB_LD];
+  constexpr int kTbSub = SUB;
+  __shared__ __attribute__((aligned(16))) __bf16 As[2][kTbSub][TBM * TB_LD];
+  __shared__ __attribute__((aligned(16))) __bf16 Bs[2][kTbSub][TBM * TB_LD];
   const int mt = (g.M + TBM - 1) / TBM, nt = (g.N + TBM - 1) / TBM;
   const int l = xcd_logical(blockIdx.x, gridDim.x);
   const int n_i = l % nt, m_i = (l / nt) % mt, split = l / (nt * mt);
@@ -457,31 +464,45 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
   auto term = [&](const float* A, int64_t lda, const float* B, int64_t ldb,
                   const int32_t* gather, int kbeg, int kend) {
     if (kbeg >= kend) return;
-    TileRegs ra, rb;
-    tb_fetch<A_KC>(ra, A, lda, nullptr, m0, g.M, kbeg, kend, tid);
-    tb_fetch<B_KC>(rb, B, ldb, gather, n0, g.N, kbeg, kend, tid);
-    for (int k0 = kbeg; k0 < kend; k0 += TBK) {
-      tb_store<A_KC>(As[buf], ra, tid);
-      tb_store<B_KC>(Bs[buf], rb, tid);
-      __syncthreads();
-      if (k0 + TBK < kend) {
-        tb_fetch<A_KC>(ra, A, lda, nullptr, m0, g.M, k0 + TBK, kend, tid);
-        tb_fetch<B_KC>(rb, B, ldb, gather, n0, g.N, k0 + TBK, kend, tid);
+    constexpr int KS = kTbSub * TBK;  // k per stage
+    TileRegs ra[kTbSub], rb[kTbSub];
+#pragma unroll
+    for (int u = 0; u < kTbSub; ++u) {
+      tb_fetch<A_KC>(ra[u], A, lda, nullptr, m0, g.M, kbeg + u * TBK, kend, tid);
+      tb_fetch<B_KC>(rb[u], B, ldb, gather, n0, g.N, kbeg + u * TBK, kend, tid);
+    }
+    for (int k0 = kbeg; k0 < kend; k0 += KS) {
+#pragma unroll
+      for (int u = 0; u < kTbSub; ++u) {
+        tb_store<A_KC>(As[buf][u], ra[u], tid);
+        tb_store<B_KC>(Bs[buf][u], rb[u], tid);
       }
-      const __bf16* a_s = As[buf];
-      const __bf16* b_s = Bs[buf];
-      bf8 a[4], b[4];
+      __syncthreads();
+      if (k0 + KS < kend) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const bf8*>(a_s + tb_off(wm + 16 * i + lr, 8 * lq));
+        for (int u = 0; u < kTbSub; ++u) {
+          tb_fetch<A_KC>(ra[u], A, lda, nullptr, m0, g.M, k0 + KS + u * TBK, kend, tid);
+          tb_fetch<B_KC>(rb[u], B, ldb, gather, n0, g.N, k0 + KS + u * TBK, kend, tid);
+        }
+      }
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        b[j] = *reinterpret_cast<const bf8*>(b_s + tb_off(wn + 16 * j + lr, 8 * lq));
+      for (int u = 0; u < kTbSub; ++u) {
+        if (k0 + u * TBK >= kend) break;  // uniform: a partial last stage
+        const __bf16* a_s = As[buf][u];
+        const __bf16* b_s = Bs[buf][u];
+        bf8 a[4], b[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
+          a[i] = *reinterpret_cast<const bf8*>(a_s + tb_off(wm + 16 * i + lr, 8 * lq));
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          b[j] = *reinterpret_cast<const bf8*>(b_s + tb_off(wn + 16 * j + lr, 8 * lq));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      }
       buf ^= 1;
     }
   };
@@ -524,10 +545,13 @@ hipError_t launch_gemm(const GemmArgs& g, bool a_kc, bool b_kc, bool bf16, hipSt
                            (g.splits > 1 ? g.splits : 1);
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     const dim3 grid((unsigned)blocks), block(256);
-#define RNNBKT_BF16_CASE(AK, BKC)                                            \
-  if (a_kc == AK && b_kc == BKC) {                                           \
-    hipLaunchKernelGGL((k_gemm_bf16<AK, BKC>), grid, block, 0, st, g);      \
-    return hipGetLastError();                                                \
+#define RNNBKT_BF16_CASE(AK, BKC)                                              \
+  if (a_kc == AK && b_kc == BKC) {                                             \
+    if (g.beside)                                                              \
+      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 2>), grid, block, 0, st, g);    \
+    else                                                                       \
+      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 1>), grid, block, 0, st, g);    \
+    return hipGetLastError();                                                  \
   }
     RNNBKT_BF16_CASE(true, true)
     RNNBKT_BF16_CASE(true, false)

@@ -56,6 +56,7 @@ struct GemmArgs {
   const float* B2;
   int64_t lda2, ldb2;
   int32_t K2;
+  int32_t beside;  // 1: runs beside a resident recurrence (bf16: the gentler tiling)
 };
 
 // Output tile of the GEMM kernels, rows x columns: 64 x 64 (fp32), 128 x 128
