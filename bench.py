@@ -424,7 +424,7 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "this build runs on a single GPU; the paper's parallel scheme runs as concurrent "
+              "the library runs on a single GPU; the paper's parallel scheme runs as concurrent "
               "replicas on that GPU (--replicas).", file=sys.stderr)
         return 2
     if args.steps < 1 or args.warmup < 0:
