@@ -136,6 +136,7 @@ struct Carve {
   size_t ws_fwd;
   // workspace (backward)
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
+  size_t wt;  // W_ih of a layer above the first, transposed (both directions), for its dX GEMM
   size_t splitk_out, colsum_out;  // output-layer gradients (run beside the recurrence)
   size_t splitk_rec;              // weight gradients on the side stream
   size_t wgpart;                  // streamed weight gradients: partial tiles of every layer
@@ -232,6 +233,7 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   // Then what only the per-step kernels or bidirectional layers use: the
   // gradient w.r.t. a layer's input between layer launches (ping-pong), the
   // per-step carries and running sums, column-sum partials.
+  c.wt = take(sizeof(float) * 2 * (size_t)s.Htop * GH);
   c.dha = take(sizeof(float) * N * s.Htop);
   c.dhb = take(sizeof(float) * N * s.Htop);
   c.carry = take(sizeof(float) * (size_t)B * s.H);
@@ -1223,11 +1225,21 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       // one GEMM with two terms).
       const int lo = g.hi - g.n + 1;
       if (lo > 0) {
+        // W_ih [G*H x din] of each direction transposed to [din x G*H], so that
+        // the GEMM reads both operands with k contiguous (no transposing LDS
+        // stores in its tile loop).
+        float* wt = at<float>(workspace, c.wt);
+        const int din = s.din(lo);
+        {
+          Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 8.0 * s.dirs * din * GH, st);
+          for (int d = 0; d < s.dirs; ++d)
+            RNNBKT_HIP(launch_transpose(params + po.wih[lo * s.dirs + d], GH, din, din,
+                                        wt + (size_t)d * din * GH, GH, st));
+        }
         Term2 t2{};
-        if (s.dirs == 2) t2 = Term2{da_of(lo, 1), GH, params + po.wih[lo * 2 + 1], s.din(lo), GH};
-        RNNBKT_HIP(gemm(da_of(lo, 0), GH, true, params + po.wih[lo * s.dirs], s.din(lo), false,
-                        dx, s.din(lo), n, s.din(lo), GH, nullptr, 0, s.bf16, st, nullptr, nullptr,
-                        s.dirs == 2 ? &t2 : nullptr));
+        if (s.dirs == 2) t2 = Term2{da_of(lo, 1), GH, wt + (size_t)din * GH, GH, GH};
+        RNNBKT_HIP(gemm(da_of(lo, 0), GH, true, wt, GH, true, dx, din, n, din, GH, nullptr, 0,
+                        s.bf16, st, nullptr, nullptr, s.dirs == 2 ? &t2 : nullptr));
         dh_in = dx;
         std::swap(dx, spare);
       }

@@ -338,6 +338,25 @@ __global__ void k_aggregate(float* __restrict__ reps, int R, int64_t stride, int
   }
 }
 
+// out[c * ld_out + r] = in[r * ld_in + c] for r < rows, c < cols: 32 x 32
+// tiles through LDS (rows of 33 floats: the column reads hit distinct banks).
+__global__ __launch_bounds__(256) void k_transpose(const float* __restrict__ in, int rows, int cols,
+                                                   int64_t ld_in, float* __restrict__ out,
+                                                   int64_t ld_out) {
+  __shared__ float t[32][33];
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int i = ty; i < 32; i += 8) {
+    const int r = r0 + i, c = c0 + tx;
+    if (r < rows && c < cols) t[i][tx] = in[(int64_t)r * ld_in + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 32; i += 8) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) out[(int64_t)c * ld_out + r] = t[tx][i];
+  }
+}
+
 __global__ void k_fill_u32(unsigned* __restrict__ p, int64_t n, unsigned v) {
   const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
   if (i4 + 3 < n) {
@@ -348,6 +367,14 @@ __global__ void k_fill_u32(unsigned* __restrict__ p, int64_t n, unsigned v) {
 }
 
 }  // namespace
+
+hipError_t launch_transpose(const float* in, int32_t rows, int32_t cols, int64_t ld_in, float* out,
+                            int64_t ld_out, hipStream_t st) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((cols + 31) / 32), (unsigned)((rows + 31) / 32));
+  hipLaunchKernelGGL(k_transpose, grid, dim3(256), 0, st, in, rows, cols, ld_in, out, ld_out);
+  return hipGetLastError();
+}
 
 hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned v, hipStream_t st) {
   if (n <= 0) return hipSuccess;

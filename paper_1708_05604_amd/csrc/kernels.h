@@ -408,6 +408,10 @@ hipError_t read_wait_timeouts(unsigned* count);
 hipError_t reset_wait_timeouts();
 constexpr unsigned kPublishSentinel = 0xFFFFFFFFu;
 
+// out[c * ld_out + r] = in[r * ld_in + c] for r < rows, c < cols.
+hipError_t launch_transpose(const float* in, int32_t rows, int32_t cols, int64_t ld_in, float* out,
+                            int64_t ld_out, hipStream_t stream);
+
 // Fills n 32-bit words with `value` (a kernel, so it may sit in a captured graph).
 hipError_t launch_fill_u32(unsigned* p, int64_t n, unsigned value, hipStream_t stream);
 
