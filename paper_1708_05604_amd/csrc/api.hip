@@ -1117,11 +1117,16 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       const int ld = l * s.dirs + d;
       const float* dax = da_of(l, d);
       const float* dahh = gru ? dah_of(l, d) : dax;
+      // The second direction swaps the streams (each keeps its split-K
+      // buffer), so that two streams carry one dW_ih and one dW_hh each.
+      const bool sw = d == 1;
       hipError_t e = gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
-                          nullptr, 0, s.bf16, s_ih, nullptr, buf_ih, nullptr, beside);
+                          nullptr, 0, s.bf16, sw ? s_hh : s_ih, nullptr, sw ? sk_rec : buf_ih,
+                          nullptr, beside);
       if (e != hipSuccess) return e;
       e = gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld], s.H, GH,
-               s.H, n, nullptr, 0, s.bf16, s_hh, d == 0 ? pf : pr, sk_rec, nullptr, beside);
+               s.H, n, nullptr, 0, s.bf16, sw ? s_ih : s_hh, d == 0 ? pf : pr,
+               sw ? buf_ih : sk_rec, nullptr, beside);
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
