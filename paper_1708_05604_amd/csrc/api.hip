@@ -420,9 +420,11 @@ struct Term2 {
 hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t ldb, bool b_kc,
                 float* C, int64_t ldc, int M, int N, int K, const float* bias, int accumulate,
                 bool bf16, hipStream_t st, const int32_t* gather = nullptr,
-                float* splitk_buf = nullptr, const Term2* t2 = nullptr, bool beside = false) {
+                float* splitk_buf = nullptr, const Term2* t2 = nullptr, bool beside = false,
+                bool a_bf16 = false) {
   GemmArgs g{};
   g.beside = beside ? 1 : 0;
+  g.a_bf16 = a_bf16 ? 1 : 0;
   if (t2) {
     g.A2 = t2->A2;
     g.lda2 = t2->lda2;
@@ -612,7 +614,9 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   int nbwd = 0;
   if (persist && s.L * s.dirs * (s.cell == RNNBKT_CELL_GRU ? 2 : 1) <= kFillJobs) {
     for (int q = 0; q < s.L * s.dirs; ++q) {
-      bwd_fill[nbwd++] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.da[q])), N * GH};
+      // (a bf16 LSTM's resident backward publishes packed bf16: half the words)
+      bwd_fill[nbwd++] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.da[q])),
+                          s.bf16 && s.cell != RNNBKT_CELL_GRU ? N * GH / 2 : N * GH};
       if (s.cell == RNNBKT_CELL_GRU)
         bwd_fill[nbwd++] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.dah[q])), N * GH};
     }
@@ -965,7 +969,10 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   auto dah_of = [&](int l, int d) {
     return gru ? at<float>(reserve, c.dah[l * s.dirs + d]) : nullptr;
   };
-  const uint64_t rec_b = sizeof(float) * (uint64_t)N * GH;
+  // A bf16 LSTM's resident backward publishes its gate gradients as packed
+  // bf16 (two per 32-bit word, rounded as every consumer rounds them).
+  const bool pk = s.bf16 && !gru;
+  const uint64_t rec_b = (pk ? 2ull : 4ull) * (uint64_t)N * GH;
   const uint32_t rec_bytes = rec_b < 0x7FFFFFF0u ? (uint32_t)rec_b : 0x7FFFFFF0u;
   // Unit (layer l, direction d) of a persistent backward launch.  up: the
   // layer above runs in the same launch (unidirectional stacks), and this
@@ -1107,6 +1114,8 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
   // over every valid frame: dW_ih on s_ih with split-K buffer buf_ih, dW_hh
   // on s_hh with the buffer of its own stream's products.
   float* sk_rec = at<float>(workspace, c.splitk_rec);
+  // Layers whose gate gradients the resident backward left packed as bf16.
+  std::vector<char> da_pk(s.L, 0);
   // beside: the products run beside the recurrence of the layers below.
   auto layer_wgrad = [&](int l, hipStream_t s_ih, float* buf_ih, hipStream_t s_hh,
                          bool beside) -> hipError_t {
@@ -1122,11 +1131,11 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
       const bool sw = d == 1;
       hipError_t e = gemm(dax, GH, false, xin, din, false, grads + po.wih[ld], din, GH, din, n,
                           nullptr, 0, s.bf16, sw ? s_hh : s_ih, nullptr, sw ? sk_rec : buf_ih,
-                          nullptr, beside);
+                          nullptr, beside, da_pk[l] != 0);
       if (e != hipSuccess) return e;
       e = gemm(dahh, GH, false, hout + d * s.H, s.dirs * s.H, false, grads + po.whh[ld], s.H, GH,
                s.H, n, nullptr, 0, s.bf16, sw ? s_ih : s_hh, d == 0 ? pf : pr,
-               sw ? buf_ih : sk_rec, nullptr, beside);
+               sw ? buf_ih : sk_rec, nullptr, beside, da_pk[l] != 0);
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -1164,7 +1173,7 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
         int nf = 0;
         for (int q = 0; q < Lc.nunits; ++q) {
           const BwdUnit& u = Lc.u[q];
-          fills[nf++] = {reinterpret_cast<unsigned*>(gru ? u.dah : u.da), N * GH};
+          fills[nf++] = {reinterpret_cast<unsigned*>(gru ? u.dah : u.da), pk ? N * GH / 2 : N * GH};
           if (gru && u.publish_dax) fills[nf++] = {reinterpret_cast<unsigned*>(u.da), N * GH};
         }
         for (int q0 = 0; q0 < nf; q0 += kFillJobs)
@@ -1225,6 +1234,7 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
         RNNBKT_HIP(launch_bwd_persistent(Lc, s.cell, s.bf16, B, st, &fits));
       }
       RNNBKT_REQUIRE(fits, RNNBKT_EHIP, "lstm_bwd: persistent launch no longer fits");
+      for (int q = 0; q < g.n; ++q) da_pk[g.hi - q] = pk ? 1 : 0;
       // Gradient w.r.t. the output of the layer below the launch's lowest
       // layer: dX = dA W_ih (bidirectional: dA_fwd W_ih,fwd + dA_bwd W_ih,bwd,
       // one GEMM with two terms).
@@ -1244,7 +1254,8 @@ int32_t backward(const rnnbkt_model_desc* desc, const float* params, const int32
         Term2 t2{};
         if (s.dirs == 2) t2 = Term2{da_of(lo, 1), GH, wt + (size_t)din * GH, GH, GH};
         RNNBKT_HIP(gemm(da_of(lo, 0), GH, true, wt, GH, true, dx, din, n, din, GH, nullptr, 0,
-                        s.bf16, st, nullptr, nullptr, s.dirs == 2 ? &t2 : nullptr));
+                        s.bf16, st, nullptr, nullptr, s.dirs == 2 ? &t2 : nullptr, false,
+                        da_pk[lo] != 0));
         dh_in = dx;
         std::swap(dx, spare);
       }

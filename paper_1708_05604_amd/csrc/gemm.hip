@@ -21,6 +21,8 @@
 // block run on one XCD.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace rnnbkt {
@@ -407,6 +409,81 @@ __device__ inline void tb_fetch(TileRegs& R, const float* P, int64_t ld, const i
   }
 }
 
+// An operand held as bf16 (the packed gate gradients of a bf16 LSTM): the
+// same elements as tb_fetch, half the bytes, kept as loaded (two bf16 per
+// word) until tb_store_bf16 writes them to LDS unchanged.  Widening them at
+// fetch time made the loads complete before the stage's MFMAs (dX and
+// weight-gradient products 1.4x slower).
+struct TileRegsBf {
+  uint2 v[4];
+};
+
+template <bool KC>
+__device__ inline void tb_fetch_bf16(TileRegsBf& R, const float* Pf, int64_t ld, int r0, int rlim,
+                                     int k0, int klim, int tid) {
+  const unsigned short* P = reinterpret_cast<const unsigned short*>(Pf);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint2 x = {0u, 0u};
+    if constexpr (KC) {
+      const int r = (tid >> 3) + 32 * i, k = k0 + (tid & 7) * 4;
+      if (r0 + r < rlim) {
+        const unsigned short* q = P + (int64_t)(r0 + r) * ld + k;
+        if (k + 4 <= klim) {
+          x = *reinterpret_cast<const uint2*>(q);
+        } else {
+          unsigned h[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (k + e < klim) h[e] = q[e];
+          x = uint2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        }
+      }
+    } else {
+      const int k = k0 + 4 * (tid >> 5) + i, r = r0 + 4 * (tid & 31);
+      if (k < klim && r < rlim) {
+        const unsigned short* q = P + (int64_t)k * ld + r;
+        if (r + 4 <= rlim) {
+          x = *reinterpret_cast<const uint2*>(q);
+        } else {
+          unsigned h[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (r + e < rlim) h[e] = q[e];
+          x = uint2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+        }
+      }
+    }
+    R.v[i] = x;
+  }
+}
+
+// tb_store for TileRegsBf: KC rows go to LDS as loaded; otherwise element e
+// of the four k-rows is gathered into row r + e (a transpose of bf16 halves).
+template <bool KC>
+__device__ inline void tb_store_bf16(__bf16* S, const TileRegsBf& R, int tid) {
+  if constexpr (KC) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = (tid >> 3) + 32 * i, k = (tid & 7) * 4;
+      *reinterpret_cast<uint2*>(S + tb_off(r, k)) = R.v[i];
+    }
+  } else {
+    const int k = 4 * (tid >> 5), r = 4 * (tid & 31);
+    const unsigned w[2][4] = {{R.v[0].x, R.v[1].x, R.v[2].x, R.v[3].x},
+                              {R.v[0].y, R.v[1].y, R.v[2].y, R.v[3].y}};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const unsigned* c = w[e >> 1];
+      const uint2 o = (e & 1) == 0
+                          ? uint2{(c[0] & 0xFFFFu) | (c[1] << 16), (c[2] & 0xFFFFu) | (c[3] << 16)}
+                          : uint2{(c[0] >> 16) | (c[1] & 0xFFFF0000u),
+                                  (c[2] >> 16) | (c[3] & 0xFFFF0000u)};
+      *reinterpret_cast<uint2*>(S + tb_off(r + e, k)) = o;
+    }
+  }
+}
+
 // Writes the registers of tb_fetch into S[row][k] (bf16, row pitch TB_LD).
 template <bool KC>
 __device__ inline void tb_store(__bf16* S, const TileRegs& R, int tid) {
@@ -439,7 +516,8 @@ __device__ inline int xcd_logical(int b, int n) {
 // beside a resident recurrence (on the CUs it leaves free) then slow its
 // exchange less (bilstm3's backward launches 1.71 -> 1.60 ms).  The caller
 // chooses it only for work beside a grid that leaves CUs free.
-template <bool A_KC, bool B_KC, int SUB>
+// ABF: the A operands are stored as bf16 (GemmArgs::a_bf16).
+template <bool A_KC, bool B_KC, int SUB, bool ABF>
 __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
   constexpr int kTbSub = SUB;
   __shared__ __attribute__((aligned(16))) __bf16 As[2][kTbSub][TBM * TB_LD];
@@ -465,23 +543,33 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs g) {
                   const int32_t* gather, int kbeg, int kend) {
     if (kbeg >= kend) return;
     constexpr int KS = kTbSub * TBK;  // k per stage
-    TileRegs ra[kTbSub], rb[kTbSub];
+    std::conditional_t<ABF, TileRegsBf, TileRegs> ra[kTbSub];
+    TileRegs rb[kTbSub];
 #pragma unroll
     for (int u = 0; u < kTbSub; ++u) {
-      tb_fetch<A_KC>(ra[u], A, lda, nullptr, m0, g.M, kbeg + u * TBK, kend, tid);
+      if constexpr (ABF)
+        tb_fetch_bf16<A_KC>(ra[u], A, lda, m0, g.M, kbeg + u * TBK, kend, tid);
+      else
+        tb_fetch<A_KC>(ra[u], A, lda, nullptr, m0, g.M, kbeg + u * TBK, kend, tid);
       tb_fetch<B_KC>(rb[u], B, ldb, gather, n0, g.N, kbeg + u * TBK, kend, tid);
     }
     for (int k0 = kbeg; k0 < kend; k0 += KS) {
 #pragma unroll
       for (int u = 0; u < kTbSub; ++u) {
-        tb_store<A_KC>(As[buf][u], ra[u], tid);
+        if constexpr (ABF)
+          tb_store_bf16<A_KC>(As[buf][u], ra[u], tid);
+        else
+          tb_store<A_KC>(As[buf][u], ra[u], tid);
         tb_store<B_KC>(Bs[buf][u], rb[u], tid);
       }
       __syncthreads();
       if (k0 + KS < kend) {
 #pragma unroll
         for (int u = 0; u < kTbSub; ++u) {
-          tb_fetch<A_KC>(ra[u], A, lda, nullptr, m0, g.M, k0 + KS + u * TBK, kend, tid);
+          if constexpr (ABF)
+            tb_fetch_bf16<A_KC>(ra[u], A, lda, m0, g.M, k0 + KS + u * TBK, kend, tid);
+          else
+            tb_fetch<A_KC>(ra[u], A, lda, nullptr, m0, g.M, k0 + KS + u * TBK, kend, tid);
           tb_fetch<B_KC>(rb[u], B, ldb, gather, n0, g.N, k0 + KS + u * TBK, kend, tid);
         }
       }
@@ -547,10 +635,14 @@ hipError_t launch_gemm(const GemmArgs& g, bool a_kc, bool b_kc, bool bf16, hipSt
     const dim3 grid((unsigned)blocks), block(256);
 #define RNNBKT_BF16_CASE(AK, BKC)                                              \
   if (a_kc == AK && b_kc == BKC) {                                             \
-    if (g.beside)                                                              \
-      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 2>), grid, block, 0, st, g);    \
+    if (g.beside && g.a_bf16)                                                  \
+      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 2, true>), grid, block, 0, st, g); \
+    else if (g.beside)                                                         \
+      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 2, false>), grid, block, 0, st, g); \
+    else if (g.a_bf16)                                                         \
+      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 1, true>), grid, block, 0, st, g); \
     else                                                                       \
-      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 1>), grid, block, 0, st, g);    \
+      hipLaunchKernelGGL((k_gemm_bf16<AK, BKC, 1, false>), grid, block, 0, st, g); \
     return hipGetLastError();                                                  \
   }
     RNNBKT_BF16_CASE(true, true)
@@ -560,6 +652,7 @@ hipError_t launch_gemm(const GemmArgs& g, bool a_kc, bool b_kc, bool bf16, hipSt
 #undef RNNBKT_BF16_CASE
     return hipErrorInvalidValue;
   }
+  if (g.a_bf16) return hipErrorInvalidValue;  // bf16-stored operands only on the bf16 path
   if (g.K2 > 0) {
     // fp32: the second term as a second launch accumulating into C.
     GemmArgs g1 = g, g2 = g;

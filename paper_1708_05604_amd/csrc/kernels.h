@@ -57,6 +57,7 @@ struct GemmArgs {
   int64_t lda2, ldb2;
   int32_t K2;
   int32_t beside;  // 1: runs beside a resident recurrence (bf16: the gentler tiling)
+  int32_t a_bf16;  // 1: A (and A2) hold bf16 values, 2 bytes each (bf16 path only)
 };
 
 // Output tile of the GEMM kernels, rows x columns: 64 x 64 (fp32), 128 x 128

@@ -244,6 +244,66 @@ __device__ inline void mma_segment(f4& acc, const unsigned (&u)[Chunk<BF16>::CPL
   }
 }
 
+// Packed bf16 segments (the gate gradients a bf16 LSTM backward publishes):
+// element k of a row at byte row_off + 2k, two elements per 32-bit word (the
+// sentinel test stays per word).  A slot is one 16-byte load of the 8
+// consecutive k it feeds to one MFMA, which takes the words as they are:
+// every consumer of these values rounds them to bf16 anyway, so storing
+// them rounded changes no result and halves what each step exchanges.
+template <int MAXC, int AUX = kDeviceScope>
+__device__ inline void issue_segment_pk(__amdgpu_buffer_rsrc_t r, unsigned row_off, const Slots& sl,
+                                        int klim, unsigned (&u)[4 * MAXC]) {
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = sl.first + i * sl.stride;
+    const int kk = c * 32 + sl.koff;
+    const unsigned o =
+        (row_off != kNoRow && c < sl.nchunks && kk < klim) ? row_off + 2u * (unsigned)kk : kNoRow;
+    const u4 x = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, AUX);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) u[i * 4 + e] = x[e];
+  }
+}
+
+template <int MAXC>
+__device__ inline void settle_segment_pk(__amdgpu_buffer_rsrc_t r, unsigned row_off,
+                                         const Slots& sl, int klim, unsigned (&u)[4 * MAXC],
+                                         const WaitCtl& w) {
+  if (segment_clear(u)) return;
+  for (unsigned polls = 1;; ++polls) {
+    __builtin_amdgcn_s_sleep(1);
+    poll_fence();
+    issue_segment_pk<MAXC>(r, row_off, sl, klim, u);
+    if (segment_clear(u)) return;
+    if ((polls & 1023u) == 0 && waits_abandoned(w)) return;
+    if (polls >= w.max_polls) {
+      report_timeout(w);
+      return;
+    }
+  }
+}
+
+template <int MAXC>
+__device__ inline void mma_segment_pk(f4& acc, const unsigned (&u)[4 * MAXC],
+                                      const bf8 (&w)[MAXC], const Slots& sl) {
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int c = sl.first + i * sl.stride;
+    if (c >= sl.nchunks) break;
+    const u4 x = {u[i * 4], u[i * 4 + 1], u[i * 4 + 2], u[i * 4 + 3]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, x), w[i], acc, 0, 0, 0);
+  }
+}
+
+// Publishes two bf16 values as one word (lo at the lower address); a word
+// equal to the sentinel becomes a pair of canonical NaNs.
+__device__ inline void publish_pk(unsigned* p, float lo, float hi) {
+  unsigned u = (unsigned)__builtin_bit_cast(unsigned short, (__bf16)lo) |
+               ((unsigned)__builtin_bit_cast(unsigned short, (__bf16)hi) << 16);
+  if (u == kSentinel) u = 0x7FC07FC0u;
+  __hip_atomic_store(p, u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Step indices of launch-relative step k for direction d.
 struct StepIdx {
   int t, rows, row0, prev0, prev_rows;
@@ -982,6 +1042,30 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   const int first = mma_wave ? mw : (1 << 20);  // no slots for the others
   const Slots sup{first, NMMA, kup / CH, lq * CPL};
   const Slots srec{first, NMMA, GH / CH, lq * CPL};
+  // A bf16 LSTM publishes its gate gradients as packed bf16 (two per word).
+  constexpr bool PK = BF16 && G == 4;
+  constexpr int WPS = PK ? 4 : CPL;      // 32-bit words a slot loads
+  constexpr unsigned kEB = PK ? 2u : 4u;  // bytes per published element
+  auto seg_issue = [&](__amdgpu_buffer_rsrc_t rr, unsigned off, const Slots& sl, int klim,
+                       auto& u) {
+    if constexpr (PK)
+      issue_segment_pk<MAXC>(rr, off, sl, klim, u);
+    else
+      issue_segment<BF16, MAXC>(rr, off, sl, klim, u);
+  };
+  auto seg_settle = [&](__amdgpu_buffer_rsrc_t rr, unsigned off, const Slots& sl, int klim,
+                        auto& u) {
+    if constexpr (PK)
+      settle_segment_pk<MAXC>(rr, off, sl, klim, u, a.wait);
+    else
+      settle_segment<BF16, MAXC>(rr, off, sl, klim, u, a.wait);
+  };
+  auto seg_mma = [&](f4& acc, const auto& u, const auto& wf, const Slots& sl) {
+    if constexpr (PK)
+      mma_segment_pk<MAXC>(acc, u, wf, sl);
+    else
+      mma_segment<BF16, MAXC>(acc, u, wf, sl);
+  };
 
   // Weight fragments: column lr is hidden unit j0 + lr.
   constexpr int MU = UP ? MAXC : 1;
@@ -1017,7 +1101,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   __syncthreads();
 
   auto up_off = [&](const BwdIdx& q) {
-    return (has_up && r < q.rows) ? 4u * (unsigned)((int64_t)(q.row0 + r) * kup) : kNoRow;
+    return (has_up && r < q.rows) ? kEB * (unsigned)((int64_t)(q.row0 + r) * kup) : kNoRow;
   };
   // Operands of the gate-gradient algebra that do not depend on other
   // workgroups (inactive rows read frame 0 and are ignored).
@@ -1048,9 +1132,9 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   // 1.42).  With the split, fetching them ahead measured slower too.
   constexpr bool kAheadOps = !SPLIT && MAXC <= 2;
   BwdIdx s = bwd_step(tbs, toff, a.T, U.dir, 0);
-  unsigned uup[CPL * MU];
+  unsigned uup[WPS * MU];
   if constexpr (UP)
-    if (mma_wave) issue_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup);
+    if (mma_wave) seg_issue(rup, up_off(s), sup, kup, uup);
   for (int k = 0; k < a.T; ++k) {
     BwdIdx nx = s;
     if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
@@ -1068,21 +1152,21 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       // Gradient arriving from the layer above (fetched one step ahead).
       if constexpr (UP) {
-        if (U.up_published) settle_segment<BF16, MAXC>(rup, up_off(s), sup, kup, uup, a.wait);
-        mma_segment<BF16, MAXC>(acc, uup, wup, sup);
+        if (U.up_published) seg_settle(rup, up_off(s), sup, kup, uup);
+        seg_mma(acc, uup, wup, sup);
       }
       // Recurrent part.
       const unsigned roff =
-          r < s.next_rows ? 4u * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
-      unsigned urec[CPL * MAXC];
-      issue_segment<BF16, MAXC>(rrec, roff, srec, GH, urec);
-      settle_segment<BF16, MAXC>(rrec, roff, srec, GH, urec, a.wait);
-      mma_segment<BF16, MAXC>(acc, urec, wrec, srec);
+          r < s.next_rows ? kEB * (unsigned)((int64_t)(s.next0 + r) * GH) : kNoRow;
+      unsigned urec[WPS * MAXC];
+      seg_issue(rrec, roff, srec, GH, urec);
+      seg_settle(rrec, roff, srec, GH, urec);
+      seg_mma(acc, urec, wrec, srec);
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[mw * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
     if constexpr (UP)
-      if (k + 1 < a.T && mma_wave) issue_segment<BF16, MAXC>(rup, up_off(nx), sup, kup, uup);
+      if (k + 1 < a.T && mma_wave) seg_issue(rup, up_off(nx), sup, kup, uup);
     if constexpr (kAheadOps)
       if (epi && k + 1 < a.T) fetch_ops(nx, ndhv, nst0, nst1, nst2, nst3, ncc, ncprev);
     __syncthreads();
@@ -1102,11 +1186,23 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
         const float di = dc * st2 * st0 * (1.f - st0);
         const float df = dc * cp * st1 * (1.f - st1);
         const float dg = dc * st0 * (1.f - st2 * st2);
-        float* dar = U.da + f * GH;
-        publish(dar + ej, di);
-        publish(dar + H + ej, df);
-        publish(dar + 2 * H + ej, dg);
-        publish(dar + 3 * H + ej, dout);
+        if constexpr (PK) {
+          // Units ej and ej + 1 sit in neighbouring lanes of the same row:
+          // the even lane publishes the pair.
+          const float gv[4] = {di, df, dg, dout};
+          unsigned* dw = reinterpret_cast<unsigned*>(U.da) + ((f * GH + ej) >> 1);
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const float other = __shfl_xor(gv[g], 1);
+            if ((ej & 1) == 0) publish_pk(dw + ((g * H) >> 1), gv[g], other);
+          }
+        } else {
+          float* dar = U.da + f * GH;
+          publish(dar + ej, di);
+          publish(dar + H + ej, df);
+          publish(dar + 2 * H + ej, dg);
+          publish(dar + 3 * H + ej, dout);
+        }
         // c_{t-1} reaches the loss through the forget path and two peepholes
         carry = dc * st1;
         bsum[0] += di;
@@ -1488,11 +1584,11 @@ BwdPlan plan_bwd(const BwdLaunch& a, int cell, bool bf16, int B) {
     nch = std::max(nch, std::max(u.up ? u.k_up / ch : 0, G * a.H / ch));
     up = up || u.up != nullptr;
   }
-  // Without an input segment a wave's registers hold the recurrent segment
-  // only: a candidate fits when its compiled kernel needs no scratch.
+  // A candidate fits when its compiled kernel needs no scratch (a bf16
+  // LSTM's packed gate gradients take half the registers of fp32 ones, so
+  // its launches with an input segment fit more slots than the others).
   auto fits_regs = [&](int nw, int m, bool split) {
-    if (up) return m <= bwd_maxc_fit(nw, bf16);
-    const void* k = bwd_kernel(cell, bf16, nw, m, split, false);
+    const void* k = bwd_kernel(cell, bf16, nw, m, split, up);
     hipFuncAttributes fa{};
     return k && hipFuncGetAttributes(&fa, k) == hipSuccess && fa.localSizeBytes == 0;
   };
