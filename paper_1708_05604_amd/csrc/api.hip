@@ -167,6 +167,7 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   c.dhtop = take(sizeof(float) * N * s.Htop);
   // The backward's gate gradients, exchanged between its workgroups: kept
   // here so that the forward can set their sentinel beside its recurrence.
+  // (A bf16 LSTM's resident backward fills the first half, as bf16 pairs.)
   for (int q = 0; q < s.L * s.dirs; ++q) {
     c.da.push_back(take(sizeof(float) * N * GH));
     c.dah.push_back(s.cell == RNNBKT_CELL_GRU ? take(sizeof(float) * N * GH) : 0);

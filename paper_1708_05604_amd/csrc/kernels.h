@@ -316,13 +316,15 @@ struct FwdLaunch {
 // [W_ih of the layer above ; W_hh], restricted to this workgroup's units.
 struct BwdUnit {
   const float* up;       // layer above: LSTM dA / GRU dAx rows [N x k_up]; nullptr = none
+                         // (bf16 LSTM: bf16 pairs, k_up / 2 words per row, as da below)
   const float* wih_up;   // W_ih of the layer above [k_up x din_up]
   const float* whh;      // [G*H x H]
   const float* dh_in;    // plain gradient w.r.t. this unit's output (column hcol), or nullptr
   const float* stash;    // [N x 4H]
   const float* cst;      // LSTM [N x H]
   const float* hout;     // layer output [N x ldh] (GRU previous state), column hcol
-  float* da;             // LSTM dA / GRU dAx [N x G*H]
+  float* da;             // LSTM dA / GRU dAx [N x G*H]; a bf16 LSTM publishes dA
+                         // rounded to bf16, two per 32-bit word ([N x G*H/2] words)
   float* dah;            // GRU dAh [N x 3H]
   float* bias_part;      // [rgroups x G*H]: per row group, sum over frames of dA / dAx
   float* bias_part_h;    // GRU: [rgroups x 3H] sums of dAh

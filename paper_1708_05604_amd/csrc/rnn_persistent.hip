@@ -22,7 +22,9 @@
 // publishes (h forward, the recurrent gate gradient backward) is filled
 // with a sentinel bit pattern before the launch; every element of it is
 // written exactly once during the launch with a relaxed device-scope atomic
-// store (a value equal to the sentinel is replaced by the canonical NaN), and
+// store (a value equal to the sentinel is replaced by the canonical NaN; a
+// bf16 LSTM's backward stores its gate gradients as bf16 pairs, one word
+// each, a pair equal to the sentinel becoming two canonical NaNs), and
 // a reader polls its elements with device-scope loads until none holds the
 // sentinel.  Single-location coherence of atomics is all this
 // needs: no fence, no cache write-back or invalidation, and a workgroup
