@@ -362,6 +362,28 @@ def test_bf16_lstm_forward_sixteen_units_per_workgroup():
     H.assert_batch_close(spec, data.params, data, order, label="bf16 LSTM H=256 B=80")
 
 
+@pytest.mark.parametrize("B,launches", [(48, 1), (112, 2)])
+def test_bf16_lstm_stack_packed_gate_gradients(B, launches):
+    """bf16 LSTM, two layers of H = 512 (longtail's layer), whose backward
+    publishes its gate gradients as packed bf16 pairs.  B = 48: both layers
+    fit one resident backward launch (16 waves of 4 slots, no scratch), the
+    lower layer multiplying the upper layer's packed gradients inside it.
+    B = 112: one launch per layer, the gradient between them from the dX
+    GEMM reading the packed gradients."""
+    spec = H.Spec(0, 2, 0, 16, 512, 16, synth.BF16)
+    rng = np.random.default_rng(53 + B)
+    lengths = sorted(rng.integers(1, 25, B).tolist(), reverse=True)
+    data = H.data_from_lengths(spec, lengths, seed=53 + B, scale=0.1)
+    order = H.batch_order(data, range(B))
+    lib.kernel_timer(True)
+    try:
+        H.assert_batch_close(spec, data.params, data, order, label=f"bf16 LSTM H=512 B={B}")
+        n = lib.kernel_timer_read("step_bwd")["launches"]
+    finally:
+        lib.kernel_timer(False)
+    assert n == launches, (n, launches)
+
+
 def test_sequence_longer_than_resident_limit():
     """T_max above the 6144 steps whose batch tables the resident kernels keep
     in LDS: the recurrences fall back to one launch per step."""
