@@ -133,6 +133,7 @@ struct Carve {
   // workspace (forward)
   size_t gx[2], loss_part;
   size_t out_done;  // counter of the output-layer workgroups that finished
+  std::vector<size_t> hx;  // bf16: each layer's output as bf16 pairs, for the recurrent polls
   size_t ws_fwd;
   // workspace (backward)
   size_t dha, dhb, carry, peep_acc, splitk, colsum;
@@ -185,6 +186,7 @@ Carve carve(const Shape& s, int T, int B, int64_t N) {
   for (int d = 0; d < 2; ++d) c.gx[d] = d < s.dirs ? take(sizeof(float) * N * GH) : c.gx[0];
   c.loss_part = take(sizeof(float) * ((N + 15) / 16 + 1));
   c.out_done = take(sizeof(unsigned));
+  for (int l = 0; l < s.L; ++l) c.hx.push_back(s.bf16 ? take(2 * (size_t)N * s.dirs * s.H) : 0);
   c.ws_fwd = pos;
 
   pos = common;
@@ -628,17 +630,25 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   note_prefilled(reserve, false);
   bool prefilled = false;
   {
+    // Sentinels: every layer output (bf16: its packed copy, and the output
+    // itself only where a layer above in the same launch polls it), then
+    // the output-layer workgroups' loss partials.
+    std::vector<FillJob> jobs;
+    if (persist) {
+      for (int l = 0; l < s.L; ++l) {
+        if (!(s.bf16 && s.dirs == 2))
+          jobs.push_back({reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l])), N * ldh});
+        if (s.bf16) jobs.push_back({at<unsigned>(workspace, c.hx[l]), N * ldh / 2});
+      }
+      jobs.push_back({reinterpret_cast<unsigned*>(lp), (N + kOutRows - 1) / kOutRows});
+    }
     FillJob pre[kFillJobs];
-    int npre = persist ? s.L : 0;
-    for (int l = 0; l < npre && l < kFillJobs; ++l)
-      pre[l] = {reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l])), N * ldh};
-    // The output-layer workgroups publish their loss partials.
-    if (persist && npre < kFillJobs)
-      pre[npre++] = {reinterpret_cast<unsigned*>(lp), (N + kOutRows - 1) / kOutRows};
+    const int npre = (int)jobs.size();
+    for (int q = 0; q < npre && q < kFillJobs; ++q) pre[q] = jobs[q];
     // Bytes moved: each valid frame's features and label read and written
     // packed, its two neighbour indices written, the tables, the fills.
     double moved = (double)N * (8.0 * s.D + (ctc ? 0.0 : 8.0) + 8.0) + 8.0 * (T + 1);
-    for (int q = 0; q < npre; ++q) moved += 4.0 * (double)pre[q].n;
+    for (const FillJob& j : jobs) moved += 4.0 * (double)j.n;
     Timed tm(RNNBKT_KERNEL_PREPARE, 0.0, moved, st);
     if (B <= kPrepMaxB && npre <= kFillJobs) {
       RNNBKT_HIP(launch_prepare(lengths, B, T, x, ctc ? nullptr : labels, s.D, d_bs, d_off, Xp,
@@ -672,6 +682,10 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     u.bhh = s.cell == RNNBKT_CELL_GRU ? params + po.bhh[ld] : nullptr;
     u.hout = at<float>(reserve, c.hout[l]);
     u.out_bytes = hout_bytes < 0x7FFFFFF0u ? (uint32_t)hout_bytes : 0x7FFFFFF0u;
+    if (s.bf16) {
+      u.hx = at<unsigned>(workspace, c.hx[l]);
+      u.hx_bytes = hout_bytes / 2 < 0x7FFFFFF0u ? (uint32_t)(hout_bytes / 2) : 0x7FFFFFF0u;
+    }
     u.stash = at<float>(reserve, c.stash[ld]);
     u.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
     u.peep = s.peep ? params + po.peep[ld] : nullptr;
@@ -728,7 +742,10 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       int n = 0;
       if (s.dirs == 1) {
         n = stack_fits(l);
-        for (int q = 0; q < n; ++q) L.u[q] = make_unit(l + q, 0, q > 0);
+        for (int q = 0; q < n; ++q) {
+          L.u[q] = make_unit(l + q, 0, q > 0);
+          L.u[q].out_polled = q + 1 < n ? 1 : 0;
+        }
       } else {
         n = 1;
         for (int d = 0; d < 2; ++d) L.u[d] = make_unit(l, d, false);
@@ -740,9 +757,13 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
         for (int q = 0; q < n; ++q) fl += s.dirs * unit_flops(l + q);
         if (!prefilled) {
           Timed tm(RNNBKT_KERNEL_OTHER, 0.0, 0.0, st);
-          for (int q = 0; q < n; ++q)
+          for (int q = 0; q < n; ++q) {
             RNNBKT_HIP(launch_fill_u32(reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l + q])),
                                        N * ldh, kPublishSentinel, st));
+            if (s.bf16)
+              RNNBKT_HIP(launch_fill_u32(at<unsigned>(workspace, c.hx[l + q]), N * ldh / 2,
+                                         kPublishSentinel, st));
+          }
         }
         if (l + n == s.L && stream_out_ok) {
           OutStreamArgs& oa = L.out;

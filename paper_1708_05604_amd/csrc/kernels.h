@@ -253,8 +253,14 @@ struct FwdUnit {
   const float* peep;   // LSTM peepholes [3H] (p_i, p_f, p_o), or nullptr
   uint32_t in_bytes;   // bytes of the array `in` addresses (< 2^31 - 16)
   uint32_t out_bytes;  // bytes of hout (< 2^31 - 16)
+  unsigned* hx;        // bf16: the output again, rounded to bf16, two units per 32-bit word
+                       // ([N x ldh/2] words, same element order as hout): the recurrent
+                       // poll reads it instead of hout
+  uint32_t hx_bytes;   // bytes of hx's array (< 2^31 - 16)
   int32_t ld_in, kin;  // input row stride and length
   int32_t in_published;  // 1: `in` is published by another unit of the same launch
+  int32_t out_polled;    // bf16: 1 if another unit of the same launch polls hout (its
+                         // input); else hout gets plain stores (read after the launch)
   int32_t dir, hcol;     // direction (0 forward in time, 1 reverse) and output column
   int32_t wg_begin;      // first workgroup of this unit
 };

@@ -646,8 +646,32 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   float c_state = 0.f, h_state = 0.f;
   const __amdgpu_buffer_rsrc_t rin = published_rsrc(U.in, U.in_bytes);
   const __amdgpu_buffer_rsrc_t rout = published_rsrc(U.hout, U.out_bytes);
+  // bf16: the recurrent segment is polled from the packed copy of the
+  // output (half the bytes; the products round it to bf16 anyway).
+  const __amdgpu_buffer_rsrc_t rhx =
+      published_rsrc(reinterpret_cast<const float*>(U.hx), U.hx_bytes);
   const int r = r0 + lr;
   __syncthreads();
+  // Publishes element e of the output row layout as half of a bf16 pair:
+  // units ej and ej + 1 sit in neighbouring lanes of one row, and the even
+  // lane stores the word.
+  auto publish_hx = [&](int64_t e, float v) {
+    const float other = __shfl_xor(v, 1);
+    if ((e & 1) == 0) publish_pk(U.hx + (e >> 1), v, other);
+  };
+  // The new state: bf16, first the packed copy the next step polls, then the
+  // output itself (published only where a unit of this launch polls it).
+  auto put_h = [&](int64_t e, float v) {
+    if constexpr (BF16) {
+      publish_hx(e, v);
+      if (U.out_polled)
+        publish(U.hout + e, v);
+      else
+        U.hout[e] = v;
+    } else {
+      publish(U.hout + e, v);
+    }
+  };
 
   auto in_off = [&](const StepIdx& q) {
     return r < q.rows ? 4u * (unsigned)((int64_t)(q.row0 + r) * U.ld_in) : kNoRow;
@@ -674,18 +698,27 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
       // Recurrent part.
-      const unsigned roff =
-          r < s.prev_rows ? 4u * (unsigned)((int64_t)(s.prev0 + r) * a.ldh + U.hcol) : kNoRow;
-      unsigned urec[CPL * MR];
-      issue_segment<BF16, MR>(rout, roff, srec, H, urec);
-      settle_segment<BF16, MR>(rout, roff, srec, H, urec, a.wait);
+      const int64_t rel = (int64_t)(s.prev0 + r) * a.ldh + U.hcol;
+      if constexpr (BF16) {
+        const unsigned roff = r < s.prev_rows ? 2u * (unsigned)rel : kNoRow;
+        unsigned urec[4 * MR];
+        issue_segment_pk<MR>(rhx, roff, srec, H, urec);
+        settle_segment_pk<MR>(rhx, roff, srec, H, urec, a.wait);
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        mma_segment<BF16, MR>(acc[nt], urec, wrec[nt], srec);
+        for (int nt = 0; nt < NT; ++nt) mma_segment_pk<MR>(acc[nt], urec, wrec[nt], srec);
+      } else {
+        const unsigned roff = r < s.prev_rows ? 4u * (unsigned)rel : kNoRow;
+        unsigned urec[CPL * MR];
+        issue_segment<BF16, MR>(rout, roff, srec, H, urec);
+        settle_segment<BF16, MR>(rout, roff, srec, H, urec, a.wait);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MR>(acc[nt], urec, wrec[nt], srec);
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           red[(wave * NT + nt) * 256 + (lq * 4 + q) * 16 + lr] = acc[nt][q];
-      }
     }
     if (k + 1 < a.T) issue_in(nx);
     __syncthreads();
@@ -716,7 +749,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
         if (peep) ao += po * c_state;
         const float og = act_sigmoid(ao);
         h_state = og * act_tanh(c_state);
-        publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
+        put_h(f * a.ldh + U.hcol + ej, h_state);
         st[ej] = ig;
         st[H + ej] = fg;
         st[2 * H + ej] = gg;
@@ -729,7 +762,7 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
         const float n = act_tanh(sg[2] + bi[2] + rg_ * ahn);
         const float hp = has_prev ? h_state : 0.f;
         h_state = (1.f - z) * n + z * hp;
-        publish(U.hout + f * a.ldh + U.hcol + ej, h_state);
+        put_h(f * a.ldh + U.hcol + ej, h_state);
         st[ej] = rg_;
         st[H + ej] = z;
         st[2 * H + ej] = n;
@@ -1436,6 +1469,7 @@ FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
   for (int q = 0; q < a.nunits; ++q) {
     const FwdUnit& u = a.u[q];
     if (u.kin < 1 || u.kin % 4 != 0 || u.in_bytes >= kNoRow || u.out_bytes >= kNoRow) return p;
+    if (bf16 && (!u.hx || u.hx_bytes >= kNoRow)) return p;
     nch = std::max(nch, std::max((u.kin + ch - 1) / ch, a.H / ch));
     published = published || u.in_published;
   }
