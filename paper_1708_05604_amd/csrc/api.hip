@@ -630,13 +630,13 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
   note_prefilled(reserve, false);
   bool prefilled = false;
   {
-    // Sentinels: every layer output (bf16: its packed copy, and the output
-    // itself only where a layer above in the same launch polls it), then
-    // the output-layer workgroups' loss partials.
+    // Sentinels: every layer output (bf16: its packed copy, which the
+    // recurrence and the layer above poll instead), then the output-layer
+    // workgroups' loss partials.
     std::vector<FillJob> jobs;
     if (persist) {
       for (int l = 0; l < s.L; ++l) {
-        if (!(s.bf16 && s.dirs == 2))
+        if (!s.bf16)
           jobs.push_back({reinterpret_cast<unsigned*>(at<float>(reserve, c.hout[l])), N * ldh});
         if (s.bf16) jobs.push_back({at<unsigned>(workspace, c.hx[l]), N * ldh / 2});
       }
@@ -685,6 +685,11 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
     if (s.bf16) {
       u.hx = at<unsigned>(workspace, c.hx[l]);
       u.hx_bytes = hout_bytes / 2 < 0x7FFFFFF0u ? (uint32_t)(hout_bytes / 2) : 0x7FFFFFF0u;
+      if (l > 0) {
+        // the layer below's packed copy (rows of din = dirs*H elements)
+        u.inx = at<unsigned>(workspace, c.hx[l - 1]);
+        u.inx_bytes = u.hx_bytes;
+      }
     }
     u.stash = at<float>(reserve, c.stash[ld]);
     u.cst = s.cell == RNNBKT_CELL_LSTM ? at<float>(reserve, c.cst[ld]) : nullptr;
@@ -744,7 +749,8 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
         n = stack_fits(l);
         for (int q = 0; q < n; ++q) {
           L.u[q] = make_unit(l + q, 0, q > 0);
-          L.u[q].out_polled = q + 1 < n ? 1 : 0;
+          // (bf16: the layer above reads the packed copy instead)
+          L.u[q].out_polled = q + 1 < n && !s.bf16 ? 1 : 0;
         }
       } else {
         n = 1;

@@ -257,10 +257,13 @@ struct FwdUnit {
                        // ([N x ldh/2] words, same element order as hout): the recurrent
                        // poll reads it instead of hout
   uint32_t hx_bytes;   // bytes of hx's array (< 2^31 - 16)
+  const unsigned* inx;  // bf16, above the first layer: the input as bf16 pairs (the packed
+                        // copy of the layer below), read instead of `in`; else nullptr
+  uint32_t inx_bytes;   // bytes of inx's array (< 2^31 - 16)
   int32_t ld_in, kin;  // input row stride and length
   int32_t in_published;  // 1: `in` is published by another unit of the same launch
   int32_t out_polled;    // bf16: 1 if another unit of the same launch polls hout (its
-                         // input); else hout gets plain stores (read after the launch)
+                         // input, when inx is not given); else hout gets plain stores
   int32_t dir, hcol;     // direction (0 forward in time, 1 reverse) and output column
   int32_t wg_begin;      // first workgroup of this unit
 };

@@ -644,7 +644,12 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
     }
   }
   float c_state = 0.f, h_state = 0.f;
-  const __amdgpu_buffer_rsrc_t rin = published_rsrc(U.in, U.in_bytes);
+  // bf16 above the first layer: the input rows come from the packed copy of
+  // the layer below (half the bytes; rounded to bf16 by the products anyway).
+  const bool in_pk = BF16 && U.inx != nullptr;
+  const __amdgpu_buffer_rsrc_t rin =
+      in_pk ? published_rsrc(reinterpret_cast<const float*>(U.inx), U.inx_bytes)
+            : published_rsrc(U.in, U.in_bytes);
   const __amdgpu_buffer_rsrc_t rout = published_rsrc(U.hout, U.out_bytes);
   // bf16: the recurrent segment is polled from the packed copy of the
   // output (half the bytes; the products round it to bf16 anyway).
@@ -674,12 +679,17 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
   };
 
   auto in_off = [&](const StepIdx& q) {
-    return r < q.rows ? 4u * (unsigned)((int64_t)(q.row0 + r) * U.ld_in) : kNoRow;
+    return r < q.rows ? (in_pk ? 2u : 4u) * (unsigned)((int64_t)(q.row0 + r) * U.ld_in) : kNoRow;
   };
   StepIdx s = fwd_step(tbs, toff, a.T, U.dir, 0);
   unsigned uin[CPL * MAXC];
+  // The packed input uses the first 4 words of each slot.
+  unsigned (&uin_pk)[4 * MAXC] = *reinterpret_cast<unsigned (*)[4 * MAXC]>(&uin[0]);
   auto issue_in = [&](const StepIdx& q) {
-    issue_segment<BF16, MAXC, MR < MAXC ? 0 : kDeviceScope>(rin, in_off(q), sin, U.kin, uin);
+    if (in_pk)
+      issue_segment_pk<MAXC, MR < MAXC ? 0 : kDeviceScope>(rin, in_off(q), sin, U.kin, uin_pk);
+    else
+      issue_segment<BF16, MAXC, MR < MAXC ? 0 : kDeviceScope>(rin, in_off(q), sin, U.kin, uin);
   };
   issue_in(s);
   for (int k = 0; k < a.T; ++k) {
@@ -694,9 +704,21 @@ __global__ __launch_bounds__(64 * NW) void k_fwd_persistent(FwdLaunch a) {
       // arriving), then the recurrent poll.  (Polling first and multiplying
       // the input while the poll is in flight made bilstm3's upper-layer
       // launches slower: 1.92 against 1.37 ms.)
-      if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin, a.wait);
+      if constexpr (BF16) {
+        if (in_pk) {
+          if (U.in_published) settle_segment_pk<MAXC>(rin, in_off(s), sin, U.kin, uin_pk, a.wait);
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
+          for (int nt = 0; nt < NT; ++nt) mma_segment_pk<MAXC>(acc[nt], uin_pk, win[nt], sin);
+        } else {
+          if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin, a.wait);
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
+        }
+      } else {
+        if (U.in_published) settle_segment<BF16, MAXC>(rin, in_off(s), sin, U.kin, uin, a.wait);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) mma_segment<BF16, MAXC>(acc[nt], uin, win[nt], sin);
+      }
       // Recurrent part.
       const int64_t rel = (int64_t)(s.prev0 + r) * a.ldh + U.hcol;
       if constexpr (BF16) {
@@ -1470,6 +1492,7 @@ FwdPlan plan_fwd(const FwdLaunch& a, int cell, bool bf16, int B) {
     const FwdUnit& u = a.u[q];
     if (u.kin < 1 || u.kin % 4 != 0 || u.in_bytes >= kNoRow || u.out_bytes >= kNoRow) return p;
     if (bf16 && (!u.hx || u.hx_bytes >= kNoRow)) return p;
+    if (u.inx && (!bf16 || u.inx_bytes >= kNoRow || u.kin % ch != 0)) return p;
     nch = std::max(nch, std::max((u.kin + ch - 1) / ch, a.H / ch));
     published = published || u.in_published;
   }
