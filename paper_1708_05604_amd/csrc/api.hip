@@ -686,7 +686,10 @@ int32_t forward(const rnnbkt_model_desc* desc, const float* params, const float*
       u.hx = at<unsigned>(workspace, c.hx[l]);
       u.hx_bytes = hout_bytes / 2 < 0x7FFFFFF0u ? (uint32_t)(hout_bytes / 2) : 0x7FFFFFF0u;
       if (l > 0) {
-        // the layer below's packed copy (rows of din = dirs*H elements)
+        // the layer below's packed copy (rows of din = dirs*H elements): the
+        // layers that run resident are a prefix of the stack (the first that
+        // does not fit sends itself and those above to the per-step kernels),
+        // so that copy is complete, or published within the same launch
         u.inx = at<unsigned>(workspace, c.hx[l - 1]);
         u.inx_bytes = u.hx_bytes;
       }
