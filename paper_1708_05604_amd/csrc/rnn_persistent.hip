@@ -1192,6 +1192,15 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   unsigned uup[WPS * MU];
   if constexpr (UP)
     if (mma_wave) seg_issue(rup, up_off(s), sup, kup, uup);
+  // The first step's operands are fetched before the loop: fetched inside it
+  // (under k == 0), their registers would count as possibly pending at every
+  // step, and the compiler would wait for all loads in flight -- the next
+  // step's operands included -- before the cell algebra.
+  if constexpr (kAheadOps) {
+    if (epi && a.T > 0) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
+    // and waited for here (vmcnt 0), so that no step starts with them pending
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+  }
   for (int k = 0; k < a.T; ++k) {
     BwdIdx nx = s;
     if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
@@ -1199,11 +1208,8 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     const int64_t f = erow < s.rows ? s.row0 + erow : 0;
     const bool has_prev = erow < s.prev_rows;
     // Loaded at the top of the step, or (kAheadOps) one step ahead.
-    if constexpr (!kAheadOps) {
+    if constexpr (!kAheadOps)
       if (epi) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
-    } else {
-      if (epi && k == 0) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
-    }
     float ndhv = 0.f, nst0 = 0.f, nst1 = 0.f, nst2 = 0.f, nst3 = 0.f, ncc = 0.f, ncprev = 0.f;
     if (active && mma_wave) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
