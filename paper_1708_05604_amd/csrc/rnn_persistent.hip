@@ -1180,7 +1180,14 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       cp_ = U.hout[fp * a.ldh + U.hcol + ej];
     }
   };
-  float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cprev = 0.f;
+  // Operands of the gate-gradient algebra.  Fetched one step ahead
+  // (kAheadOps), one set per step in flight: the loop then runs two steps
+  // per iteration with the sets in turn, so a fetched set is never copied (a
+  // copy would wait for its loads at the end of every step).
+  struct Ops {
+    float dhv = 0.f, st0 = 0.f, st1 = 0.f, st2 = 0.f, st3 = 0.f, cc = 0.f, cprev = 0.f;
+  };
+  Ops oa, ob;
   // Without the split the gate-gradient waves also poll, and loads complete
   // in issue order, so operands fetched at the top of a step hold up that
   // wave's poll: with few slots per wave they are fetched one step ahead,
@@ -1197,11 +1204,11 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
   // step, and the compiler would wait for all loads in flight -- the next
   // step's operands included -- before the cell algebra.
   if constexpr (kAheadOps) {
-    if (epi && a.T > 0) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
+    if (epi && a.T > 0) fetch_ops(s, oa.dhv, oa.st0, oa.st1, oa.st2, oa.st3, oa.cc, oa.cprev);
     // and waited for here (vmcnt 0), so that no step starts with them pending
     __builtin_amdgcn_s_waitcnt(0x0F70);
   }
-  for (int k = 0; k < a.T; ++k) {
+  auto step = [&](int k, Ops& cur, Ops& nxt) {
     BwdIdx nx = s;
     if (k + 1 < a.T) nx = bwd_step(tbs, toff, a.T, U.dir, k + 1);
     const bool active = r0 < s.rows;
@@ -1209,8 +1216,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     const bool has_prev = erow < s.prev_rows;
     // Loaded at the top of the step, or (kAheadOps) one step ahead.
     if constexpr (!kAheadOps)
-      if (epi) fetch_ops(s, dhv, st0, st1, st2, st3, cc, cprev);
-    float ndhv = 0.f, nst0 = 0.f, nst1 = 0.f, nst2 = 0.f, nst3 = 0.f, ncc = 0.f, ncprev = 0.f;
+      if (epi) fetch_ops(s, cur.dhv, cur.st0, cur.st1, cur.st2, cur.st3, cur.cc, cur.cprev);
     if (active && mma_wave) {
       f4 acc = {0.f, 0.f, 0.f, 0.f};
       // Gradient arriving from the layer above (fetched one step ahead).
@@ -1228,10 +1234,14 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) red[mw * 256 + (lq * 4 + q) * 16 + lr] = acc[q];
     }
+    // (kAheadOps) This step's operands, fetched a step ago, are waited for
+    // before anything else is issued (they have long arrived): the compiler
+    // then knows them complete, and the cell algebra waits for no load.
+    if constexpr (kAheadOps) __builtin_amdgcn_s_waitcnt(0x0F70);
     if constexpr (UP)
       if (k + 1 < a.T && mma_wave) seg_issue(rup, up_off(nx), sup, kup, uup);
     if constexpr (kAheadOps)
-      if (epi && k + 1 < a.T) fetch_ops(nx, ndhv, nst0, nst1, nst2, nst3, ncc, ncprev);
+      if (epi && k + 1 < a.T) fetch_ops(nx, nxt.dhv, nxt.st0, nxt.st1, nxt.st2, nxt.st3, nxt.cc, nxt.cprev);
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
@@ -1239,16 +1249,16 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
 #pragma unroll
       for (int w_ = 0; w_ < NMMA; ++w_) dh_red += red[w_ * 256 + threadIdx.x];
       if constexpr (G == 4) {
-        const float dh = dhv + dh_red;
-        const float tc = act_tanh(cc);
-        const float dout = dh * tc * st3 * (1.f - st3);
+        const float dh = cur.dhv + dh_red;
+        const float tc = act_tanh(cur.cc);
+        const float dout = dh * tc * cur.st3 * (1.f - cur.st3);
         // c_t reaches the loss through h_t, the next step and the output peephole
-        float dc = dh * st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
+        float dc = dh * cur.st3 * (1.f - tc * tc) + (has_next ? carry : 0.f);
         if (peep) dc += dout * po;
-        const float cp = has_prev ? cprev : 0.f;
-        const float di = dc * st2 * st0 * (1.f - st0);
-        const float df = dc * cp * st1 * (1.f - st1);
-        const float dg = dc * st0 * (1.f - st2 * st2);
+        const float cp = has_prev ? cur.cprev : 0.f;
+        const float di = dc * cur.st2 * cur.st0 * (1.f - cur.st0);
+        const float df = dc * cp * cur.st1 * (1.f - cur.st1);
+        const float dg = dc * cur.st0 * (1.f - cur.st2 * cur.st2);
         if constexpr (PK) {
           // Units ej and ej + 1 sit in neighbouring lanes of the same row:
           // the even lane publishes the pair.
@@ -1267,7 +1277,7 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
           publish(dar + 3 * H + ej, dout);
         }
         // c_{t-1} reaches the loss through the forget path and two peepholes
-        carry = dc * st1;
+        carry = dc * cur.st1;
         bsum[0] += di;
         bsum[1] += df;
         bsum[2] += dg;
@@ -1276,12 +1286,12 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
           carry += di * pi + df * pf;
           bsumh[0] += di * cp;
           bsumh[1] += df * cp;
-          bsumh[2] += dout * cc;
+          bsumh[2] += dout * cur.cc;
         }
       } else {
-        const float dh = dhv + dh_red + (has_next ? carry : 0.f);
-        const float rr = st0, z = st1, n = st2, ahn = st3;
-        const float hp = has_prev ? cprev : 0.f;
+        const float dh = cur.dhv + dh_red + (has_next ? carry : 0.f);
+        const float rr = cur.st0, z = cur.st1, n = cur.st2, ahn = cur.st3;
+        const float hp = has_prev ? cur.cprev : 0.f;
         const float dn = dh * (1.f - z);
         const float dz = dh * (hp - n);
         const float dan = dn * (1.f - n * n);
@@ -1306,16 +1316,15 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
       }
     }
     s = nx;
-    if constexpr (kAheadOps) {
-      dhv = ndhv;
-      st0 = nst0;
-      st1 = nst1;
-      st2 = nst2;
-      st3 = nst3;
-      cc = ncc;
-      cprev = ncprev;
-    }
     __syncthreads();  // red is rewritten by the next step
+  };
+  if constexpr (kAheadOps) {
+    for (int k = 0; k < a.T; k += 2) {
+      step(k, oa, ob);
+      if (k + 1 < a.T) step(k + 1, ob, oa);
+    }
+  } else {
+    for (int k = 0; k < a.T; ++k) step(k, oa, oa);  // fetched at the top of each step
   }
   // Bias gradients of this workgroup: sum its 16 rows in a fixed order and
   // write one partial per row group (folded over row groups afterwards).
