@@ -1253,9 +1253,17 @@ __global__ __launch_bounds__(64 * NW) void k_bwd_persistent(BwdLaunch a) {
     __syncthreads();
     if (epi && active && erow < s.rows) {
       const bool has_next = erow < s.next_rows;
+      // All the partials are read before the first sum (the scheduling
+      // barrier keeps the reads together), then summed in a fixed order
+      // (bilstm3's backward 1.20 -> 1.11 ms per launch; the same in the
+      // forward's state update made bf16 forwards slower).
+      float part[NMMA];
+#pragma unroll
+      for (int w_ = 0; w_ < NMMA; ++w_) part[w_] = red[w_ * 256 + threadIdx.x];
+      __builtin_amdgcn_sched_barrier(0);
       float dh_red = 0.f;
 #pragma unroll
-      for (int w_ = 0; w_ < NMMA; ++w_) dh_red += red[w_ * 256 + threadIdx.x];
+      for (int w_ = 0; w_ < NMMA; ++w_) dh_red += part[w_];
       if constexpr (G == 4) {
         const float dh = cur.dhv + dh_red;
         const float tc = act_tanh(cur.cc);
