@@ -105,13 +105,18 @@ struct SplitK {
   int kps;
 };
 
-// Slices of the reduction so that a GEMM launches about 512 workgroups (two
-// per CU; 1024 for the fp32 kernel's 64 x 64 tiles: gru2's weight gradients,
-// +3% useful timesteps/s, where the bf16 128 x 128 tiles lost 1% with more),
-// each slice at least 256 deep, for output tiles of `tile` x `tile`.
-SplitK choose_splitk(int64_t M, int64_t N, int64_t K, int tile) {
+// Slices of the reduction so that a GEMM launches about one round of
+// workgroups, each slice at least 256 deep, for output tiles of `tile` x
+// `tile`: 768 for the bf16 kernel (three per CU; alone at bilstm3's shapes
+// dW_hh 113 -> 88 us against 512, and 120 us with 1024, a second round),
+// 256 beside a resident recurrence, which takes half the CUs (bilstm3 +2%
+// useful timesteps/s against 512), 1024 for the fp32 kernel's 64 x 64
+// tiles (gru2's weight gradients: +3% against 512).  The buffers are sized
+// with the largest.
+constexpr int64_t kBesideSplitTarget = 256;
+SplitK choose_splitk(int64_t M, int64_t N, int64_t K, int tile, bool beside = false) {
   const int64_t tiles = ((M + tile - 1) / tile) * ((N + tile - 1) / tile);
-  const int64_t target = tile < 128 ? 1024 : 512;
+  const int64_t target = tile < 128 ? 1024 : beside ? kBesideSplitTarget : 768;
   int64_t S = std::max<int64_t>(1, (target + tiles - 1) / tiles);
   S = std::min<int64_t>(S, std::max<int64_t>(1, K / 256));
   int64_t kps = (K + S - 1) / S;
@@ -453,7 +458,7 @@ hipError_t gemm(const float* A, int64_t lda, bool a_kc, const float* Bm, int64_t
   g.splits = 1;
   g.k_per_split = (K + 31) / 32 * 32;
   if (splitk_buf && !t2) {
-    const SplitK p = choose_splitk(M, N, K, gemm_tile(bf16));
+    const SplitK p = choose_splitk(M, N, K, gemm_tile(bf16), beside);
     g.splits = p.S;
     g.k_per_split = p.kps;
     g.partial = splitk_buf;
