@@ -45,8 +45,9 @@ def _ready():
 
 
 def default_workers() -> int:
-    """The CPUs this process may run on, at most 16 (the CPU share of a
-    one-GPU machine, whatever the host reports)."""
+    """The CPUs this process may run on, at most 16 (a host that shares its
+    cores between several GPUs gives one GPU's process about that many,
+    whatever it reports)."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
