@@ -384,6 +384,21 @@ def test_bf16_lstm_stack_packed_gate_gradients(B, launches):
     assert n == launches, (n, launches)
 
 
+@pytest.mark.parametrize("din", [4, 12])
+def test_bf16_narrow_input_weight_gradient(din):
+    """bf16 bidirectional LSTM whose bottom layer has a handful of input
+    features, not a multiple of 8: its dW_ih (din columns of one 128-wide
+    tile) is reduced over more than 1000 frames in several split-K slices,
+    the last one ragged."""
+    spec = H.Spec(0, 2, 1, din, 64, 8, synth.BF16)
+    rng = np.random.default_rng(61 + din)
+    lengths = sorted(rng.integers(17, 61, 32).tolist(), reverse=True)
+    assert sum(lengths) > 1000 and sum(lengths) % 32 != 0
+    data = H.data_from_lengths(spec, lengths, seed=61 + din, scale=0.1)
+    order = H.batch_order(data, range(32))
+    H.assert_batch_close(spec, data.params, data, order, label=f"bf16 BiLSTM din={din}")
+
+
 def test_sequence_longer_than_resident_limit():
     """T_max above the 6144 steps whose batch tables the resident kernels keep
     in LDS: the recurrences fall back to one launch per step."""
