@@ -24,6 +24,7 @@ same workload on the host cores (all of them, and one thread).
 from __future__ import annotations
 
 import argparse
+import collections
 import json
 import os
 import sys
@@ -151,10 +152,21 @@ class Epoch:
         self.max_N = max(self.useful)
 
 
+# The host runs at most this many training steps ahead of the GPU: an epoch
+# of bilstm3 enqueues about 13,000 launches, and with no bound the runtime's
+# queues fill up and the host blocks inside launch calls; kernels on the
+# caller's stream then started about 11 us apart instead of back to back
+# (kernel trace), and an epoch took 1912-1942 ms from run to run against
+# 1912-1913 ms paced (16 steps ahead: about 0.1 s of work, so the GPU never
+# waits for the host).
+PACE_STEPS = 16
+
+
 def run_steps(ep, state, first, count, torch):
     desc, params, grads, reserve, workspace, loss, lr, opt, ctc_ws = state
     useful = 0
     nb = len(ep.batches)
+    marks = collections.deque()
     for k in range(count):
         i = (first + k) % nb
         if ctc_ws is None:
@@ -168,13 +180,19 @@ def run_steps(ep, state, first, count, torch):
         else:
             lib.adadelta_apply(params, grads, opt[0], opt[1])
         useful += ep.useful[i]
+        mark = torch.cuda.Event()
+        mark.record()
+        marks.append(mark)
+        if len(marks) > PACE_STEPS:
+            marks.popleft().synchronize()
     return useful
 
 
 def timed_epochs(ep, state, warmup, steps, torch):
     """`warmup` untimed epochs, then `steps` epochs back to back with an
-    event between epochs (no host synchronisation inside the timed region),
-    device synchronised on both sides.  Returns the seconds of each epoch."""
+    event between epochs (inside the timed region the host only waits for
+    steps PACE_STEPS behind the one it enqueues), device synchronised on both
+    sides.  Returns the seconds of each epoch."""
     nb = len(ep.batches)
     for _ in range(warmup):
         run_steps(ep, state, 0, nb, torch)
