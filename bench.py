@@ -154,11 +154,9 @@ class Epoch:
 
 # The host runs at most this many training steps ahead of the GPU: an epoch
 # of bilstm3 enqueues about 13,000 launches, and with no bound the runtime's
-# queues fill up and the host blocks inside launch calls; kernels on the
-# caller's stream then started about 11 us apart instead of back to back
-# (kernel trace), and an epoch took 1912-1942 ms from run to run against
-# 1912-1913 ms paced (16 steps ahead: about 0.1 s of work, so the GPU never
-# waits for the host).
+# queues fill up and the host blocks inside launch calls; an epoch then took
+# 1912-1960 ms from run to run, against 1912-1913 ms paced (16 steps ahead:
+# about 0.1 s of work, so the GPU never waits for the host).
 PACE_STEPS = 16
 
 
